@@ -1,0 +1,146 @@
+"""Pins of the oracle's unmasking rules (Section 4.2) and generation loop (Section 3.2)."""
+import itertools
+
+import numpy as np
+import pytest
+
+from oracle import model as M
+from oracle import selection as S
+from oracle import unmask as U
+from oracle import generate as G
+from synthetic import WORKLOADS, TINY, make_weights, initial_tokens, sharpened
+
+rng = np.random.default_rng(11)
+
+
+def test_topn_brute_force():
+    for _ in range(200):
+        b = 8
+        conf = rng.random(b)
+        masked = rng.random(b) < 0.7
+        n = int(rng.integers(1, 9))
+        sel = U.choose(conf, masked, U.TOPN, n)
+        cands = [i for i in range(b) if masked[i]]
+        m = min(n, len(cands))
+        # brute force: the chosen subset has the largest total confidence among all m-subsets
+        best = max(itertools.combinations(cands, m), key=lambda c: sum(conf[i] for i in c), default=())
+        assert set(np.nonzero(sel)[0]) == set(best)
+        assert not np.any(sel & ~masked)
+
+
+def test_threshold_rules():
+    conf = np.array([0.2, 0.95, 0.91, 0.5, 0.99])
+    masked = np.array([True, True, True, True, False])
+    assert list(U.choose(conf, masked, U.THRESHOLD, threshold=0.9)) == [False, True, True, False, False]
+    # none above: only the most confident candidate
+    assert list(U.choose(conf, masked, U.THRESHOLD, threshold=0.97)) == [False, True, False, False, False]
+    # threshold 0: every candidate; threshold >= 1: exactly one
+    assert U.choose(conf, masked, U.THRESHOLD, threshold=0.0).sum() == 4
+    assert U.choose(conf, masked, U.THRESHOLD, threshold=1.0).sum() == 1
+    # strict comparison
+    assert not U.choose(np.array([0.9, 0.1]), np.array([True, True]), U.THRESHOLD, threshold=0.9)[1]
+
+
+def test_ties_and_full_block():
+    conf = np.array([0.5, 0.7, 0.7, 0.7])
+    masked = np.ones(4, bool)
+    assert list(U.choose(conf, masked, U.TOPN, 2)) == [False, True, True, False]
+    assert U.choose(conf, masked, U.TOPN, 4).all()
+    assert not U.choose(conf, np.zeros(4, bool), U.TOPN, 4).any()
+
+
+def _tiny_wl(**kw):
+    return WORKLOADS["tiny"].replace(**kw)
+
+
+def test_tiny_trajectory_invariants():
+    wl = _tiny_wl()
+    w = G.NumpyWeights(make_weights(wl.model, seed=0))
+    st, recs = G.generate(wl, w, initial_tokens(wl).numpy(), keep=False)
+    assert len(recs) == wl.n_blocks * (wl.block_size // wl.n_per_step)
+    assert not np.any(st.tokens == wl.model.mask_id)
+    prompt = initial_tokens(wl).numpy()[:, :wl.prompt_len]
+    assert np.array_equal(st.tokens[:, :wl.prompt_len], prompt)
+    # every step decodes exactly n tokens of its own block
+    for r in recs:
+        assert r.selected.sum() == wl.n_per_step
+
+
+def _unpruned_step_logits(wl, w, tokens, block_idx):
+    """Standard block-wise decoding input [P; B_t; S_t] with plain [MASK]
+    embeddings: every position of the sequence, no selection at all."""
+    L = wl.total_len
+    pos = np.arange(L)
+    x = w.tok_emb[tokens]
+    h = M.forward(x, pos, w, wl.model).hidden
+    P = wl.prompt_len + block_idx * wl.block_size
+    return M.output_stats(h[P:], w, wl.model, wl.topk)
+
+
+def test_full_budgets_equal_unpruned_forward():
+    wl = _tiny_wl(local_budget=10**6, middle_budget=10**6, tail_budget=10**6, alpha=0.0)
+    w = G.NumpyWeights(make_weights(wl.model, seed=1, norm_jitter=0.1))
+    tok0 = initial_tokens(wl, seed=5).numpy()
+    st = G.OracleState.start(tok0, wl.topk)
+    for j, first in [(0, True), (0, False), (1, True), (2, True)]:
+        ref = _unpruned_step_logits(wl, w, st.tokens[0].copy(), j)
+        rec = G.step(wl, w, st, j, first)
+        assert np.max(np.abs(rec.stats[0].logits - ref.logits)) < 1e-12
+
+
+def test_zero_budgets_equal_prefix_block_forward():
+    wl = _tiny_wl(local_budget=0, middle_budget=0, tail_budget=0)
+    w = G.NumpyWeights(make_weights(wl.model, seed=2, norm_jitter=0.1))
+    tok0 = initial_tokens(wl, seed=6).numpy()
+    st = G.OracleState.start(tok0, wl.topk)
+    for j in range(3):
+        P = wl.prompt_len + j * wl.block_size
+        toks = st.tokens[0, :P + wl.block_size].copy()
+        h = M.forward(w.tok_emb[toks], np.arange(P + wl.block_size), w, wl.model).hidden
+        ref = M.output_stats(h[P:], w, wl.model, wl.topk)
+        rec = G.step(wl, w, st, j, True)
+        assert rec.rows.n_suffix == 0
+        assert np.max(np.abs(rec.stats[0].logits - ref.logits)) < 1e-12
+
+
+def test_cached_step_equals_uncached_when_nothing_changed():
+    """Right after a block-start step, a cached step over unchanged inputs
+    reproduces the block-start step's outputs."""
+    wl = _tiny_wl(cache=True, alpha=0.0)
+    w = G.NumpyWeights(make_weights(wl.model, seed=4, norm_jitter=0.1))
+    tok0 = initial_tokens(wl, seed=7).numpy()
+    st = G.OracleState.start(tok0, wl.topk)
+    rec0 = G.step(wl, w, st.copy(), 1, True)       # block-start over the same tokens
+    st1 = st.copy()
+    G.step(wl, w, st1, 1, True)
+    st1.tokens = st.tokens.copy()                  # undo the unmasking
+    rec1 = G.step(wl, w, st1, 1, False)
+    assert not rec1.include_prefix
+    assert np.max(np.abs(rec1.stats[0].logits - rec0.stats[0].logits)) < 1e-12
+
+
+def test_soft_embedding_used_on_next_step():
+    wl = _tiny_wl()
+    w = G.NumpyWeights(make_weights(wl.model, seed=0))
+    st = G.OracleState.start(initial_tokens(wl).numpy(), wl.topk)
+    rec0 = G.step(wl, w, st, 0, True)
+    rec1 = G.step(wl, w, st, 0, False)
+    rows = rec1.rows
+    mask_e = w.tok_emb[wl.model.mask_id]
+    suffix = rows.region >= S.REGION_LOCAL
+    # every retained suffix row now differs from the plain mask embedding
+    assert all(not np.allclose(rec1.x[0, r], mask_e) for r in np.nonzero(suffix)[0])
+    # and equals Eq. 8 with the previous step's top-k
+    r = int(np.nonzero(suffix)[0][0])
+    o = r - rec0.rows.first_out_row
+    ids, wts = rec0.stats[0].topk_ids[o], rec0.stats[0].topk_w[o]
+    want = (1 - wl.alpha) * mask_e + wl.alpha * (wts[:, None] * w.tok_emb[ids]).sum(0)
+    assert np.allclose(rec1.x[0, r], want, atol=1e-14)
+
+
+def test_threshold_workload_terminates():
+    wl = _tiny_wl(rule="threshold", threshold=0.9)
+    w = G.NumpyWeights(make_weights(wl.model, seed=0))
+    st, recs = G.generate(wl, w, initial_tokens(wl).numpy())
+    assert not np.any(st.tokens == wl.model.mask_id)
+    assert len(recs) >= wl.n_blocks

@@ -1,0 +1,281 @@
+/*
+ * ssm.h -- C ABI of the SSM block-wise denoising step on AMD Instinct MI355X (gfx950).
+ *
+ * Structured Suffix Modeling (SSM) decodes a masked diffusion language model
+ * block by block.  At each denoising step the model input is the prefix (the
+ * prompt and every block decoded so far), the current block, and only the
+ * suffix tokens retained by the local / middle / tail rules (Section 3.2,
+ * Eq. 1-5), each at its original RoPE position ("Sparse Input Construction").
+ * Retained suffix tokens are embedded as a mix of the [MASK] embedding and a
+ * soft embedding of the previous step's top-k prediction (Eq. 6-8).  The step
+ * ends by unmasking the most confident positions of the block (Section 4.2).
+ *
+ * One step is four calls, in this order:
+ *   ssm_select_suffix  -> compacted row list (positions, regions, token ids)
+ *   ssm_embed_suffix   -> input embeddings of the compacted rows
+ *   ssm_denoise_step   -> transformer forward, LM head, per-row statistics
+ *   ssm_unmask         -> decode block positions, record suffix predictions
+ *
+ * Conventions shared by every call
+ *   - "d_" pointers are HIP device memory owned by the caller.  The library
+ *     never allocates or frees device memory and keeps no pointer after a
+ *     call returns.  Host pointers (structs, output counts) are read or
+ *     written synchronously during the call.
+ *   - `stream` is a hipStream_t (NULL = the null stream).  Work is enqueued
+ *     on it asynchronously and is ordered with the caller's other work on
+ *     that stream.
+ *   - Arguments are validated on the host before anything is launched; an
+ *     invalid call launches nothing and returns a negative SSM_E_* code with
+ *     a message available from ssm_last_error() (thread-local).
+ *   - No C++ exception crosses the ABI.  Results are deterministic: no
+ *     floating-point reduction depends on scheduling order.
+ *   - Batched sequences share prompt length, generation length and block
+ *     schedule, hence one position list for the whole batch.
+ *   - Element types: token ids and positions int32; region tags int8;
+ *     probabilities and the residual stream float32; weights, KV cache and
+ *     embeddings in the model's dtype (float32 or bfloat16).
+ */
+#ifndef SSM_H
+#define SSM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Return codes. */
+enum {
+  SSM_OK = 0,
+  SSM_E_INVAL = -1,        /* bad argument value or null required pointer     */
+  SSM_E_SHAPE = -2,        /* inconsistent model shape                         */
+  SSM_E_CAPACITY = -3,     /* an output or cache buffer is too small           */
+  SSM_E_HIP = -4,          /* a HIP runtime or launch error                    */
+  SSM_E_UNSUPPORTED = -5   /* valid, but a shape this build has no kernel for  */
+};
+
+/* Middle-region retention (Section 3.2, Eq. 3). */
+enum {
+  SSM_MIDDLE_STRIDED = 0,      /* middle_budget tokens at offsets floor(i*len/M')     */
+  SSM_MIDDLE_BLOCK_START = 1   /* the start token of every middle block (Eq. 3)     */
+};
+
+/* Unmasking rules (Section 4.2 "Vanilla" / "Par."; Section 4.5 margin rule). */
+enum {
+  SSM_UNMASK_TOPN = 0,         /* the n most confident masked positions             */
+  SSM_UNMASK_THRESHOLD = 1,    /* confidence > threshold, at least one per step     */
+  SSM_UNMASK_MARGIN = 2        /* top1 - top2 probability > threshold, at least one */
+};
+
+/* Model element types. */
+enum { SSM_DT_F32 = 0, SSM_DT_BF16 = 1 };
+
+/* Region tag of a compacted row. */
+enum {
+  SSM_REGION_PREFIX = 0, SSM_REGION_BLOCK = 1, SSM_REGION_LOCAL = 2,
+  SSM_REGION_MIDDLE = 3, SSM_REGION_TAIL = 4
+};
+
+/* Prefix KV cache use in ssm_denoise_step (the "PC." setting, Section 4.6). */
+enum {
+  SSM_CACHE_OFF = 0,    /* every row is an input row; the cache buffers are scratch        */
+  SSM_CACHE_WRITE = 1,  /* first step of a block: rows start with the prefix; afterwards   */
+                        /* slots [0, prefix) of every layer hold the prefix keys/values     */
+  SSM_CACHE_READ = 2    /* later step: keys/values of slots [0, n_cached) are the prefix   */
+};
+
+/* ------------------------------------------------------------------------ */
+/* Suffix partition and compaction (Section 3.2, Eq. 1-5; sparse input).    */
+/* ------------------------------------------------------------------------ */
+
+typedef struct ssm_select_params {
+  int32_t prompt_len;      /* P0 >= 0                                                      */
+  int32_t gen_len;         /* G > 0, a multiple of block_size                              */
+  int32_t block_size;      /* b in [1, 1024]                                               */
+  int32_t block_idx;       /* current block j in [0, G/b)                                  */
+  int32_t local_budget;    /* tokens kept whole after the block (Eq. 2 with w*b)  >= 0     */
+  int32_t middle_budget;   /* strided mode: tokens kept in the middle region      >= 0     */
+  int32_t middle_mode;     /* SSM_MIDDLE_*                                                 */
+  int32_t tail_budget;     /* tokens kept in the last block, both ends first (Eq. 4) >= 0  */
+  int32_t include_prefix;  /* 1: rows start with the prefix [0, P0 + j*b); 0: cached step  */
+} ssm_select_params;
+
+/*
+ * Row counts of the compacted sequence, in closed form on the host; no GPU
+ * work.  n_rows = (include_prefix ? P0 + j*b : 0) + b + n_suffix;
+ * first_out_row = the index of the first row of the current block (rows
+ * from there on need logits).  Any output pointer may be NULL.
+ */
+int32_t ssm_select_count(const ssm_select_params* p, int32_t* n_rows, int32_t* n_suffix,
+                         int32_t* first_out_row);
+
+/*
+ * Builds the compacted row list of the sparse input [P; B_t; R_t]: for row r,
+ * d_pos[r] is its absolute position (ascending within prefix, block and R_t),
+ * d_region[r] its SSM_REGION_* tag, and d_tok_c[s*cap + r] the token id of
+ * sequence s at that position (gathered from d_tokens[s*seq_len + pos]).
+ *   d_tokens  [batch, seq_len] int32, seq_len == prompt_len + gen_len
+ *   d_pos     [cap] int32, d_region [cap] int8 (may be NULL), d_tok_c [batch, cap] int32
+ * The row counts are returned synchronously (as ssm_select_count).
+ * SSM_E_CAPACITY if cap < n_rows.
+ */
+int32_t ssm_select_suffix(const ssm_select_params* p, int32_t batch, int32_t seq_len,
+                          const int32_t* d_tokens, int32_t* d_pos, int32_t* d_tok_c,
+                          int8_t* d_region, int32_t cap, int32_t* n_rows, int32_t* n_suffix,
+                          int32_t* first_out_row, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Model description.                                                       */
+/* ------------------------------------------------------------------------ */
+
+/* Device pointers of one decoder layer, row-major, in the model's dtype. */
+typedef struct ssm_layer {
+  const void* attn_norm;   /* [d]                                  */
+  const void* wq;          /* [n_heads*head_dim, d]                */
+  const void* wk;          /* [n_kv_heads*head_dim, d]             */
+  const void* wv;          /* [n_kv_heads*head_dim, d]             */
+  const void* wo;          /* [d, n_heads*head_dim]                */
+  const void* ffn_norm;    /* [d]                                  */
+  const void* w_gate;      /* [ffn_dim, d]                         */
+  const void* w_up;        /* [ffn_dim, d]                         */
+  const void* w_down;      /* [d, ffn_dim]                         */
+} ssm_layer;
+
+/*
+ * Bidirectional pre-norm decoder (LLaDA / Dream shape): RMSNorm, attention
+ * with rotate-half RoPE and grouped-query heads, SwiGLU FFN, final RMSNorm,
+ * untied LM head.  d_model == n_heads*head_dim; n_heads % n_kv_heads == 0.
+ */
+typedef struct ssm_model {
+  int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, ffn_dim, vocab, mask_id;
+  int32_t dtype;           /* SSM_DT_F32 or SSM_DT_BF16                        */
+  float rope_base;         /* e.g. 10000                                       */
+  float rms_eps;           /* e.g. 1e-5                                        */
+  const void* tok_emb;     /* [vocab, d] device                                */
+  const void* final_norm;  /* [d] device                                       */
+  const void* lm_head;     /* [vocab, d] device                                */
+  const ssm_layer* layers; /* HOST array of n_layers device-pointer sets       */
+} ssm_model;
+
+/* Prefix KV cache: k and v are [n_layers, batch, n_kv_heads, capacity, head_dim]
+ * in the model's dtype; keys are stored after RoPE. */
+typedef struct ssm_kv_cache {
+  void* k;
+  void* v;
+  int32_t capacity;
+} ssm_kv_cache;
+
+/* ------------------------------------------------------------------------ */
+/* Soft suffix embedding (Section 3.2, Eq. 6-8).                            */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * d_x[s, r, :] (float32 [batch, n_rows, d]) = the input embedding of row r:
+ *   - E[tok] for prefix and block rows (d_region < SSM_REGION_LOCAL);
+ *   - for a retained suffix row at position p whose prediction was made at
+ *     step prev_step (d_pred_step[s, p] == prev_step >= 0):
+ *       (1 - alpha) E[mask] + alpha * sum_i d_pred_w[s, p, i] E[d_pred_ids[s, p, i]]
+ *     (Eq. 7-8; the weights are the Eq. 6 renormalised top-k probabilities);
+ *   - E[mask] for a retained suffix row without such a prediction.
+ *   d_tok_c [batch, tok_stride] int32 (tok_stride >= n_rows: the `cap` of
+ *   ssm_select_suffix); d_pos, d_region [n_rows];
+ *   d_pred_ids [batch, seq_len, k] int32, d_pred_w [batch, seq_len, k] float32,
+ *   d_pred_step [batch, seq_len] int32.
+ * k in [1, 8]; alpha in [0, 1].
+ */
+int32_t ssm_embed_suffix(const ssm_model* m, int32_t batch, int32_t seq_len,
+                         const int32_t* d_tok_c, int32_t tok_stride, const int32_t* d_pos,
+                         const int8_t* d_region, int32_t n_rows, const int32_t* d_pred_ids,
+                         const float* d_pred_w, const int32_t* d_pred_step, int32_t prev_step,
+                         int32_t k, float alpha, float* d_x, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Transformer forward over the compacted rows, LM head and row statistics. */
+/* ------------------------------------------------------------------------ */
+
+/* Bytes of device workspace ssm_denoise_step needs for up to max_rows rows per
+ * sequence (256-byte aligned pieces). */
+int32_t ssm_workspace_size(const ssm_model* m, int32_t batch, int32_t max_rows, size_t* bytes);
+
+/*
+ * Runs every layer over the n_rows compacted rows of each sequence
+ * (d_x float32 [batch, n_rows, d], rows at positions d_pos[n_rows]), then the
+ * final norm and LM head over the output rows [first_out_row, n_rows)
+ * (n_out = n_rows - first_out_row) and writes, per output row (float32 /
+ * int32, [batch, n_out(, k)]), with the [MASK] id excluded from the vocabulary:
+ *   d_argmax   most probable token (lower id on ties)
+ *   d_conf     its softmax probability
+ *   d_topk_ids the k most probable tokens, most probable first
+ *   d_topk_w   their probabilities renormalised over the k (Eq. 6)
+ * Optional debug outputs (NULL to skip): d_logits_dbg float32 [batch, n_out, vocab],
+ * d_hidden_dbg float32 [batch, n_rows, d] (residual stream after the last layer).
+ * Cache: cache_mode SSM_CACHE_OFF / WRITE require n_cached == 0; READ requires
+ * n_cached > 0 prefix slots written by an earlier WRITE step.  This step's keys
+ * and values go to slots [n_cached, n_cached + n_rows), so capacity >=
+ * n_cached + n_rows.  Attention of every row reads all n_cached + n_rows keys.
+ * d_ws: workspace of ws_bytes >= ssm_workspace_size(batch, n_rows).
+ * k in [1, 8].  The bfloat16 path needs d_model, head_dim*n_heads, ffn_dim and
+ * vocab to be multiples of 128 and head_dim == 128; otherwise SSM_E_UNSUPPORTED.
+ */
+int32_t ssm_denoise_step(const ssm_model* m, const ssm_kv_cache* cache, int32_t cache_mode,
+                         int32_t n_cached, int32_t batch, const int32_t* d_pos, int32_t n_rows,
+                         const float* d_x, int32_t first_out_row, int32_t k, int32_t* d_argmax,
+                         float* d_conf, int32_t* d_topk_ids, float* d_topk_w,
+                         float* d_logits_dbg, float* d_hidden_dbg, void* d_ws, size_t ws_bytes,
+                         void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Confidence-based unmasking and prediction-state update (Section 4.2).    */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * For each sequence s, among the still-masked positions of the block
+ * [block_start, block_start + block_size) of d_tokens [batch, seq_len]:
+ *   TOPN:      the n_per_step highest d_conf (lower position on ties);
+ *   THRESHOLD: every d_conf > threshold, or the single highest if none;
+ *   MARGIN:    every (p1 - p2) > threshold, or the single widest if none,
+ *              where p2 = d_conf * d_topk_w[.,1] / d_topk_w[.,0] (needs k >= 2);
+ * and writes d_argmax there.  Output rows (d_argmax, d_conf [batch, n_out],
+ * d_topk_ids, d_topk_w [batch, n_out, k]) are those of ssm_denoise_step: row i
+ * < block_size is block position block_start + i; row i >= block_size is the
+ * retained suffix position d_pos_out[i].  For those suffix rows the top-k
+ * prediction is stored: d_pred_ids/d_pred_w[s, pos, :] and
+ * d_pred_step[s, pos] = step.
+ * d_selected (uint8 [batch, block_size], may be NULL) receives the decoded
+ * positions, d_masked_left (int32 [batch], may be NULL) the masks left in the block.
+ */
+int32_t ssm_unmask(int32_t* d_tokens, int32_t batch, int32_t seq_len, int32_t block_start,
+                   int32_t block_size, int32_t mask_id, int32_t rule, int32_t n_per_step,
+                   float threshold, const int32_t* d_argmax, const float* d_conf,
+                   const int32_t* d_topk_ids, const float* d_topk_w, int32_t k, int32_t n_out,
+                   const int32_t* d_pos_out, int32_t step, int32_t* d_pred_ids, float* d_pred_w,
+                   int32_t* d_pred_step, uint8_t* d_selected, int32_t* d_masked_left,
+                   void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Launch timing (tracing aid; off by default).                             */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * on != 0: from now on every kernel launcher of the calls above is bracketed
+ * by a pair of HIP events recorded on the call's stream, under a tag naming
+ * the operation ("select", "embed", "rope_table", "rmsnorm", "gemm_qkv",
+ * "attention", "gemm_o", "gemm_gate_up", "gemm_down", "gemm_lm_head",
+ * "rowstats", "unmask").  Each call discards earlier records.  Not
+ * thread-safe; meant for a single profiling thread.
+ */
+int32_t ssm_profile_enable(int32_t on);
+
+/* Number of recorded launches under `tag` and their summed duration in
+ * milliseconds; waits for the recorded events to complete. */
+int32_t ssm_profile_query(const char* tag, int32_t* count, double* total_ms);
+
+/* Message of the last error on this thread ("" if none). */
+const char* ssm_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SSM_H */

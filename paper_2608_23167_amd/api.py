@@ -1,0 +1,137 @@
+"""Python binding of the C ABI: the same four calls (plus the size queries),
+taking torch tensors for device memory and torch's current HIP stream.
+
+Argument marshalling only: every step of the path runs in libssm.so.
+"""
+from __future__ import annotations
+
+import ctypes as C
+from typing import Optional, Tuple
+
+import torch
+
+from . import _lib as L
+from ._lib import check, lib
+
+
+def _stream(stream) -> C.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return C.c_void_p(stream.cuda_stream)
+
+
+def _ptr(t: Optional[torch.Tensor], dtype=None, name="tensor") -> C.c_void_p:
+    if t is None:
+        return C.c_void_p(None)
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    return C.c_void_p(t.data_ptr())
+
+
+def select_params(prompt_len, gen_len, block_size, block_idx, local_budget, middle_budget,
+                  middle_mode, tail_budget, include_prefix) -> L.SelectParams:
+    return L.SelectParams(prompt_len, gen_len, block_size, block_idx, local_budget, middle_budget,
+                          middle_mode, tail_budget, int(bool(include_prefix)))
+
+
+def ssm_select_count(p: L.SelectParams) -> Tuple[int, int, int]:
+    n, s, f = C.c_int32(), C.c_int32(), C.c_int32()
+    check(lib().ssm_select_count(C.byref(p), C.byref(n), C.byref(s), C.byref(f)), "ssm_select_count")
+    return n.value, s.value, f.value
+
+
+def ssm_select_suffix(p: L.SelectParams, tokens: torch.Tensor, pos: torch.Tensor,
+                      tok_c: torch.Tensor, region: Optional[torch.Tensor], stream=None
+                      ) -> Tuple[int, int, int]:
+    B, seq_len = tokens.shape
+    cap = pos.numel()
+    if tok_c.shape != (B, cap):
+        raise ValueError("tok_c must be [batch, cap]")
+    n, s, f = C.c_int32(), C.c_int32(), C.c_int32()
+    rc = lib().ssm_select_suffix(C.byref(p), B, seq_len, _ptr(tokens, torch.int32, "tokens"),
+                                 _ptr(pos, torch.int32, "pos"), _ptr(tok_c, torch.int32, "tok_c"),
+                                 _ptr(region, torch.int8, "region"), cap, C.byref(n), C.byref(s),
+                                 C.byref(f), _stream(stream))
+    check(rc, "ssm_select_suffix")
+    return n.value, s.value, f.value
+
+
+def ssm_embed_suffix(model, tok_c: torch.Tensor, pos: torch.Tensor, region: torch.Tensor,
+                     n_rows: int, pred_ids: torch.Tensor, pred_w: torch.Tensor,
+                     pred_step: torch.Tensor, prev_step: int, k: int, alpha: float,
+                     x: torch.Tensor, stream=None) -> None:
+    B, seq_len = pred_step.shape
+    rc = lib().ssm_embed_suffix(C.byref(model.c_model), B, seq_len,
+                                _ptr(tok_c, torch.int32, "tok_c"), tok_c.shape[1],
+                                _ptr(pos, torch.int32, "pos"), _ptr(region, torch.int8, "region"),
+                                n_rows, _ptr(pred_ids, torch.int32, "pred_ids"),
+                                _ptr(pred_w, torch.float32, "pred_w"),
+                                _ptr(pred_step, torch.int32, "pred_step"), prev_step, k,
+                                float(alpha), _ptr(x, torch.float32, "x"), _stream(stream))
+    check(rc, "ssm_embed_suffix")
+
+
+def ssm_workspace_size(model, batch: int, max_rows: int) -> int:
+    n = C.c_size_t()
+    check(lib().ssm_workspace_size(C.byref(model.c_model), batch, max_rows, C.byref(n)),
+          "ssm_workspace_size")
+    return n.value
+
+
+def ssm_denoise_step(model, cache, cache_mode: int, n_cached: int, pos: torch.Tensor,
+                     n_rows: int, x: torch.Tensor, first_out_row: int, k: int,
+                     argmax: torch.Tensor, conf: torch.Tensor, topk_ids: torch.Tensor,
+                     topk_w: torch.Tensor, ws: torch.Tensor,
+                     logits: Optional[torch.Tensor] = None, hidden: Optional[torch.Tensor] = None,
+                     stream=None) -> None:
+    B = x.shape[0]
+    rc = lib().ssm_denoise_step(C.byref(model.c_model), C.byref(cache.c_cache), cache_mode,
+                                n_cached, B, _ptr(pos, torch.int32, "pos"), n_rows,
+                                _ptr(x, torch.float32, "x"), first_out_row, k,
+                                _ptr(argmax, torch.int32, "argmax"),
+                                _ptr(conf, torch.float32, "conf"),
+                                _ptr(topk_ids, torch.int32, "topk_ids"),
+                                _ptr(topk_w, torch.float32, "topk_w"),
+                                _ptr(logits, torch.float32, "logits"),
+                                _ptr(hidden, torch.float32, "hidden"),
+                                _ptr(ws, torch.uint8, "ws"), ws.numel(), _stream(stream))
+    check(rc, "ssm_denoise_step")
+
+
+def ssm_unmask(tokens: torch.Tensor, block_start: int, block_size: int, mask_id: int, rule: int,
+               n_per_step: int, threshold: float, argmax: torch.Tensor, conf: torch.Tensor,
+               topk_ids: torch.Tensor, topk_w: torch.Tensor, k: int, n_out: int,
+               pos_out: torch.Tensor, step: int, pred_ids: torch.Tensor, pred_w: torch.Tensor,
+               pred_step: torch.Tensor, selected: Optional[torch.Tensor] = None,
+               masked_left: Optional[torch.Tensor] = None, stream=None) -> None:
+    B, seq_len = tokens.shape
+    rc = lib().ssm_unmask(_ptr(tokens, torch.int32, "tokens"), B, seq_len, block_start,
+                          block_size, mask_id, rule, n_per_step, float(threshold),
+                          _ptr(argmax, torch.int32, "argmax"), _ptr(conf, torch.float32, "conf"),
+                          _ptr(topk_ids, torch.int32, "topk_ids"),
+                          _ptr(topk_w, torch.float32, "topk_w"), k, n_out,
+                          _ptr(pos_out, torch.int32, "pos_out"), step,
+                          _ptr(pred_ids, torch.int32, "pred_ids"),
+                          _ptr(pred_w, torch.float32, "pred_w"),
+                          _ptr(pred_step, torch.int32, "pred_step"),
+                          _ptr(selected, torch.uint8, "selected"),
+                          _ptr(masked_left, torch.int32, "masked_left"), _stream(stream))
+    check(rc, "ssm_unmask")
+
+
+PROFILE_TAGS = ("select", "embed", "rope_table", "rmsnorm", "gemm_qkv", "attention", "gemm_o",
+                "gemm_gate_up", "gemm_down", "gemm_lm_head", "rowstats", "unmask")
+
+
+def ssm_profile_enable(on: bool) -> None:
+    check(lib().ssm_profile_enable(int(bool(on))), "ssm_profile_enable")
+
+
+def ssm_profile_query(tag: str) -> Tuple[int, float]:
+    n, ms = C.c_int32(), C.c_double()
+    check(lib().ssm_profile_query(tag.encode(), C.byref(n), C.byref(ms)), "ssm_profile_query")
+    return n.value, ms.value

@@ -1,0 +1,267 @@
+// Non-causal attention of the compacted rows over every key (cached prefix
+// followed by the rows' own keys), with grouped-query heads.
+//
+// bfloat16 path (head_dim 128): one workgroup = 4 waves = 64 query rows of one
+// (sequence, head); keys stream through LDS in tiles of 64.  Each wave
+// computes S^T = K Q^T with v_mfma_f32_16x16x32_bf16 so that a lane ends up
+// holding 4 consecutive keys of one query: the exponentiated scores are then
+// already in the operand layout of the P V product, which is computed as
+// O^T = V^T P^T from a transposed V tile.  The softmax is the online
+// (running max / running sum) form, reduced across the 4 lanes that share a
+// query.  Split-KV over the key range fills the GPU at small row counts; a
+// merge kernel combines the per-split (max, sum, output) triples in order.
+#include "internal.h"
+
+namespace ssm {
+
+constexpr float LOG2E = 1.4426950408889634f;
+
+__global__ void __launch_bounds__(256) attn_bf16_kernel(
+    const bf16_t* __restrict__ Q, const bf16_t* __restrict__ Kc, const bf16_t* __restrict__ Vc,
+    int H, int Hkv, int Mq, int Nk, int cap, int keys_per_split, float scale_log2,
+    bf16_t* __restrict__ O, float* __restrict__ Opart, float* __restrict__ ML) {
+  constexpr int DH = 128, KT = 64, KS = DH + 8, VS = KT + 8;
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[KT * KS];
+  __shared__ __attribute__((aligned(16))) bf16_t Vt[DH * VS];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 4, c16 = lane & 15;
+  const int bh = blockIdx.y, s = bh / H, h = bh % H, kvh = h / (H / Hkv);
+  const int split = blockIdx.z;
+  const int kb = split * keys_per_split, ke = min(Nk, kb + keys_per_split);
+  const int q = blockIdx.x * 64 + wave * 16 + c16;
+
+  const bf16_t* Qh = Q + (size_t)bh * Mq * DH;
+  bf16x8_t qf[4];
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) {
+    if (q < Mq) qf[kk] = *(const bf16x8_t*)(Qh + (size_t)q * DH + 32 * kk + 8 * g);
+    else {
+      uint4 z = {0u, 0u, 0u, 0u};
+      qf[kk] = __builtin_bit_cast(bf16x8_t, z);
+    }
+  }
+  const bf16_t* Kh = Kc + (size_t)(s * Hkv + kvh) * cap * DH;
+  const bf16_t* Vh = Vc + (size_t)(s * Hkv + kvh) * cap * DH;
+
+  f32x4_t o[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) o[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY, l_run = 0.f;
+
+  for (int k0 = kb; k0 < ke; k0 += KT) {
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int c = tid + 256 * i, key = c >> 4, d8 = c & 15;
+      uint4 kv = {0u, 0u, 0u, 0u}, vv = {0u, 0u, 0u, 0u};
+      if (k0 + key < ke) {
+        kv = *(const uint4*)(Kh + (size_t)(k0 + key) * DH + d8 * 8);
+        vv = *(const uint4*)(Vh + (size_t)(k0 + key) * DH + d8 * 8);
+      }
+      *(uint4*)(Ks + key * KS + d8 * 8) = kv;
+      const bf16_t* ve = (const bf16_t*)&vv;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) Vt[(d8 * 8 + e) * VS + key] = ve[e];
+    }
+    __syncthreads();
+
+    // S^T block nb: sc[nb][r] = score(key 16nb + 4g + r, query c16)
+    f32x4_t sc[4];
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb) {
+      sc[nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {
+        const bf16x8_t a = *(const bf16x8_t*)(Ks + (16 * nb + c16) * KS + 32 * kk + 8 * g);
+        sc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[kk], sc[nb], 0, 0, 0);
+      }
+    }
+    float mt = -INFINITY;
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int key = k0 + 16 * nb + 4 * g + r;
+        const float v = key < ke ? sc[nb][r] * scale_log2 : -INFINITY;
+        sc[nb][r] = v;
+        mt = fmaxf(mt, v);
+      }
+    mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
+    mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+    const float m_new = fmaxf(m_run, mt);
+    const float alpha = exp2f(m_run - m_new);
+    l_run *= alpha;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) o[i] *= alpha;
+
+    // P^T operand: slot e of lane group g holds key 32*h2 + 16*(e/4) + 4g + e%4
+    bf16x8_t pb[2];
+#pragma unroll
+    for (int h2 = 0; h2 < 2; ++h2) {
+      uint16_t tmp[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float p = exp2f(sc[2 * h2 + (e >> 2)][e & 3] - m_new);
+        l_run += p;
+        tmp[e] = f2bf(p);
+      }
+      pb[h2] = __builtin_bit_cast(bf16x8_t, *(const uint4*)tmp);
+    }
+#pragma unroll
+    for (int h2 = 0; h2 < 2; ++h2) {
+#pragma unroll
+      for (int db = 0; db < 8; ++db) {
+        const bf16_t* vr = Vt + (16 * db + c16) * VS + 32 * h2 + 4 * g;
+        uint4 a4;
+        const uint2 lo = *(const uint2*)vr;
+        const uint2 hi = *(const uint2*)(vr + 16);
+        a4.x = lo.x; a4.y = lo.y; a4.z = hi.x; a4.w = hi.y;
+        o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a4), pb[h2],
+                                                        o[db], 0, 0, 0);
+      }
+    }
+    m_run = m_new;
+  }
+
+  l_run += __shfl_xor(l_run, 16, 64);
+  l_run += __shfl_xor(l_run, 32, 64);
+  if (q >= Mq) return;
+  // o[db][r] = O^T[dh 16db + 4g + r][query c16]
+  if (Opart == nullptr) {
+    const float inv = 1.0f / l_run;
+    bf16_t* out = O + ((size_t)s * Mq + q) * (size_t)(H * DH) + h * DH;
+#pragma unroll
+    for (int db = 0; db < 8; ++db) {
+      uint16_t tmp[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) tmp[r] = f2bf(o[db][r] * inv);
+      *(uint2*)(out + 16 * db + 4 * g) = *(const uint2*)tmp;
+    }
+  } else {
+    const size_t row = ((size_t)split * gridDim.y + bh) * Mq + q;
+    float* op = Opart + row * DH;
+#pragma unroll
+    for (int db = 0; db < 8; ++db) *(f32x4_t*)(op + 16 * db + 4 * g) = o[db];
+    if (g == 0) { ML[row * 2] = m_run; ML[row * 2 + 1] = l_run; }
+  }
+}
+
+// float32 path: one thread per query row, keys read through the cache.
+template <int DH>
+__global__ void __launch_bounds__(64) attn_f32_kernel(
+    const float* __restrict__ Q, const float* __restrict__ Kc, const float* __restrict__ Vc,
+    int H, int Hkv, int Mq, int Nk, int cap, int keys_per_split, float scale_log2,
+    float* __restrict__ O, float* __restrict__ Opart, float* __restrict__ ML) {
+  const int bh = blockIdx.y, s = bh / H, h = bh % H, kvh = h / (H / Hkv);
+  const int split = blockIdx.z;
+  const int kb = split * keys_per_split, ke = min(Nk, kb + keys_per_split);
+  const int q = blockIdx.x * 64 + threadIdx.x;
+  if (q >= Mq) return;
+  const float* qp = Q + ((size_t)bh * Mq + q) * DH;
+  float qv[DH], ov[DH];
+#pragma unroll
+  for (int c = 0; c < DH; ++c) { qv[c] = qp[c]; ov[c] = 0.f; }
+  const float* Kh = Kc + (size_t)(s * Hkv + kvh) * cap * DH;
+  const float* Vh = Vc + (size_t)(s * Hkv + kvh) * cap * DH;
+  float m_run = -INFINITY, l_run = 0.f;
+  for (int j = kb; j < ke; ++j) {
+    const float* kp = Kh + (size_t)j * DH;
+    float dot = 0.f;
+#pragma unroll
+    for (int c = 0; c < DH; ++c) dot = fmaf(qv[c], kp[c], dot);
+    const float sv = dot * scale_log2;
+    const float m_new = fmaxf(m_run, sv);
+    const float alpha = exp2f(m_run - m_new), p = exp2f(sv - m_new);
+    l_run = l_run * alpha + p;
+    const float* vp = Vh + (size_t)j * DH;
+#pragma unroll
+    for (int c = 0; c < DH; ++c) ov[c] = ov[c] * alpha + p * vp[c];
+    m_run = m_new;
+  }
+  if (Opart == nullptr) {
+    float* out = O + ((size_t)s * Mq + q) * (size_t)(H * DH) + h * DH;
+    const float inv = 1.0f / l_run;
+#pragma unroll
+    for (int c = 0; c < DH; ++c) out[c] = ov[c] * inv;
+  } else {
+    const size_t row = ((size_t)split * gridDim.y + bh) * Mq + q;
+#pragma unroll
+    for (int c = 0; c < DH; ++c) Opart[row * DH + c] = ov[c];
+    ML[row * 2] = m_run;
+    ML[row * 2 + 1] = l_run;
+  }
+}
+
+// Combines the splits of one (sequence, head, query) row, in split order.
+template <typename T>
+__global__ void attn_merge_kernel(const float* __restrict__ Opart, const float* __restrict__ ML,
+                                  int S, int BH, int H, int Mq, int DH, T* __restrict__ O) {
+  const int row = blockIdx.x;               // over BH * Mq
+  const int bh = row / Mq, q = row % Mq, s = bh / H, h = bh % H;
+  float M = -INFINITY;
+  for (int i = 0; i < S; ++i) M = fmaxf(M, ML[((size_t)i * BH * Mq + row) * 2]);
+  float L = 0.f;
+  for (int i = 0; i < S; ++i) {
+    const size_t r = (size_t)i * BH * Mq + row;
+    const float l = ML[r * 2 + 1];
+    if (l > 0.f) L += l * exp2f(ML[r * 2] - M);
+  }
+  const float inv = 1.0f / L;
+  T* out = O + ((size_t)s * Mq + q) * (size_t)(H * DH) + h * DH;
+  for (int c = threadIdx.x; c < DH; c += blockDim.x) {
+    float acc = 0.f;
+    for (int i = 0; i < S; ++i) {
+      const size_t r = (size_t)i * BH * Mq + row;
+      if (ML[r * 2 + 1] > 0.f) acc += Opart[r * DH + c] * exp2f(ML[r * 2] - M);
+    }
+    stf(out + c, acc * inv);
+  }
+}
+
+hipError_t attention(int dtype, const void* q, const void* kc, const void* vc, int B, int H,
+                     int Hkv, int dh, int Mq, int Nk, int cap, void* out, AttnWs ws,
+                     hipStream_t st) {
+  if (Mq == 0) return hipSuccess;
+  const int BH = B * H;
+  const int qtiles = ceil_div(Mq, 64);
+  // split the key range until the grid covers the chip twice over, in whole
+  // 64-key tiles, never leaving a split without keys
+  int S = 1;
+  const int key_tiles = ceil_div(Nk, 64);
+  while (S * 2 <= ws.max_splits && qtiles * BH * S < 512 && S * 2 <= key_tiles) S *= 2;
+  int kps = ceil_div(key_tiles, S) * 64;
+  S = ceil_div(Nk, kps);
+  const float scale_log2 = LOG2E / sqrtf((float)dh);
+  dim3 grid(qtiles, BH, S);
+  float* opart = S > 1 ? ws.opart : nullptr;
+  if (dtype == 1) {
+    hipLaunchKernelGGL(attn_bf16_kernel, grid, dim3(256), 0, st, (const bf16_t*)q,
+                       (const bf16_t*)kc, (const bf16_t*)vc, H, Hkv, Mq, Nk, cap, kps, scale_log2,
+                       (bf16_t*)out, opart, ws.ml);
+  } else {
+    const float* qf = (const float*)q;
+    const float* kf = (const float*)kc;
+    const float* vf = (const float*)vc;
+    float* of = (float*)out;
+    if (dh == 32)
+      hipLaunchKernelGGL(attn_f32_kernel<32>, grid, dim3(64), 0, st, qf, kf, vf, H, Hkv, Mq, Nk,
+                         cap, kps, scale_log2, of, opart, ws.ml);
+    else if (dh == 64)
+      hipLaunchKernelGGL(attn_f32_kernel<64>, grid, dim3(64), 0, st, qf, kf, vf, H, Hkv, Mq, Nk,
+                         cap, kps, scale_log2, of, opart, ws.ml);
+    else
+      hipLaunchKernelGGL(attn_f32_kernel<128>, grid, dim3(64), 0, st, qf, kf, vf, H, Hkv, Mq, Nk,
+                         cap, kps, scale_log2, of, opart, ws.ml);
+  }
+  if (S > 1) {
+    if (dtype == 1)
+      hipLaunchKernelGGL(attn_merge_kernel<bf16_t>, dim3(BH * Mq), dim3(128), 0, st, ws.opart,
+                         ws.ml, S, BH, H, Mq, dh, (bf16_t*)out);
+    else
+      hipLaunchKernelGGL(attn_merge_kernel<float>, dim3(BH * Mq), dim3(128), 0, st, ws.opart,
+                         ws.ml, S, BH, H, Mq, dh, (float*)out);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace ssm

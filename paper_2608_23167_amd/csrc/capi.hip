@@ -1,0 +1,395 @@
+// C ABI of the SSM library: argument validation, workspace layout and the
+// orchestration of one denoising step.  See include/ssm.h for the contract.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "../../include/ssm.h"
+#include "internal.h"
+
+using namespace ssm;
+
+namespace {
+
+thread_local std::string g_err;
+
+int32_t fail(int32_t code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int32_t ok() {
+  g_err.clear();
+  return SSM_OK;
+}
+
+#define HIP_TRY(expr)                                                                   \
+  do {                                                                                  \
+    hipError_t e_ = (expr);                                                             \
+    if (e_ != hipSuccess) return fail(SSM_E_HIP, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+int32_t layout_of(const ssm_select_params* p, SelectLayout& L) {
+  if (!p) return fail(SSM_E_INVAL, "null select params");
+  const int P0 = p->prompt_len, G = p->gen_len, b = p->block_size, j = p->block_idx;
+  if (P0 < 0) return fail(SSM_E_INVAL, "prompt_len %d < 0", P0);
+  if (b < 1 || b > 1024) return fail(SSM_E_INVAL, "block_size %d not in [1, 1024]", b);
+  if (G <= 0 || G % b != 0) return fail(SSM_E_INVAL, "gen_len %d not a positive multiple of block_size %d", G, b);
+  if (j < 0 || j >= G / b) return fail(SSM_E_INVAL, "block_idx %d not in [0, %d)", j, G / b);
+  if (p->local_budget < 0 || p->middle_budget < 0 || p->tail_budget < 0)
+    return fail(SSM_E_INVAL, "negative budget");
+  if (p->middle_mode != SSM_MIDDLE_STRIDED && p->middle_mode != SSM_MIDDLE_BLOCK_START)
+    return fail(SSM_E_INVAL, "unknown middle_mode %d", p->middle_mode);
+  if (p->include_prefix != 0 && p->include_prefix != 1)
+    return fail(SSM_E_INVAL, "include_prefix must be 0 or 1");
+  if ((long long)P0 + G > 0x3fffffff) return fail(SSM_E_INVAL, "sequence too long");
+  // Eq. 1: local = first min(L, n) suffix tokens, tail = last block minus the
+  // local part, middle = what lies between.
+  L.P = P0 + j * b;
+  L.b = b;
+  L.n_prefix = p->include_prefix ? L.P : 0;
+  L.s0 = L.P + b;
+  const int s_end = P0 + G, n = s_end - L.s0;
+  L.n_local = p->local_budget < n ? p->local_budget : n;
+  const int tail_lo = (L.s0 + L.n_local > s_end - b) ? L.s0 + L.n_local : s_end - b;
+  L.mid_lo = L.s0 + L.n_local;
+  L.mid_len = tail_lo - L.mid_lo;
+  L.mid_mode = p->middle_mode;
+  L.mid_first = 0;
+  if (L.mid_len <= 0) {
+    L.n_mid = 0;
+  } else if (p->middle_mode == SSM_MIDDLE_BLOCK_START) {   // Eq. 3
+    const int off = L.mid_lo - L.s0;
+    L.mid_first = L.s0 + ((off + b - 1) / b) * b;
+    const int mid_hi = L.mid_lo + L.mid_len;
+    L.n_mid = L.mid_first < mid_hi ? (mid_hi - L.mid_first + b - 1) / b : 0;
+  } else {
+    L.n_mid = p->middle_budget < L.mid_len ? p->middle_budget : L.mid_len;
+  }
+  L.tail_lo = tail_lo;
+  L.tail_len = s_end - tail_lo;
+  L.n_tail = p->tail_budget < L.tail_len ? p->tail_budget : L.tail_len;   // Eq. 4
+  L.n_suffix = L.n_local + L.n_mid + L.n_tail;                           // Eq. 5
+  L.n_rows = L.n_prefix + b + L.n_suffix;
+  return SSM_OK;
+}
+
+int32_t check_model(const ssm_model* m) {
+  if (!m) return fail(SSM_E_INVAL, "null model");
+  if (m->dtype != SSM_DT_F32 && m->dtype != SSM_DT_BF16) return fail(SSM_E_INVAL, "unknown dtype %d", m->dtype);
+  if (m->n_layers < 0 || m->d_model <= 0 || m->n_heads <= 0 || m->n_kv_heads <= 0 ||
+      m->head_dim <= 0 || m->ffn_dim <= 0 || m->vocab <= 1)
+    return fail(SSM_E_SHAPE, "non-positive model dimension");
+  if (m->d_model != m->n_heads * m->head_dim)
+    return fail(SSM_E_SHAPE, "d_model %d != n_heads %d * head_dim %d", m->d_model, m->n_heads, m->head_dim);
+  if (m->n_heads % m->n_kv_heads != 0)
+    return fail(SSM_E_SHAPE, "n_heads %d not a multiple of n_kv_heads %d", m->n_heads, m->n_kv_heads);
+  if (m->mask_id < 0 || m->mask_id >= m->vocab) return fail(SSM_E_INVAL, "mask_id out of range");
+  if (!m->tok_emb || !m->final_norm || !m->lm_head) return fail(SSM_E_INVAL, "null model tensor");
+  if (m->n_layers > 0 && !m->layers) return fail(SSM_E_INVAL, "null layer array");
+  for (int l = 0; l < m->n_layers; ++l) {
+    const ssm_layer& y = m->layers[l];
+    if (!y.attn_norm || !y.wq || !y.wk || !y.wv || !y.wo || !y.ffn_norm || !y.w_gate || !y.w_up || !y.w_down)
+      return fail(SSM_E_INVAL, "null tensor in layer %d", l);
+  }
+  if (m->dtype == SSM_DT_BF16) {
+    if (m->head_dim != 128) return fail(SSM_E_UNSUPPORTED, "bf16 path needs head_dim 128 (got %d)", m->head_dim);
+    if (m->d_model % 128 || m->ffn_dim % 128 || m->vocab % 128)
+      return fail(SSM_E_UNSUPPORTED, "bf16 path needs d_model, ffn_dim, vocab multiples of 128");
+  } else {
+    if (m->head_dim != 32 && m->head_dim != 64 && m->head_dim != 128)
+      return fail(SSM_E_UNSUPPORTED, "fp32 path needs head_dim 32, 64 or 128");
+    if (m->d_model % 32 || m->ffn_dim % 32 || m->vocab % 32)
+      return fail(SSM_E_UNSUPPORTED, "fp32 path needs d_model, ffn_dim, vocab multiples of 32");
+  }
+  return SSM_OK;
+}
+
+constexpr int ATTN_MAX_SPLITS = 16;
+
+// ---- launch profiling: HIP events around each launcher, per tag ----------
+struct ProfRec {
+  const char* tag;
+  hipEvent_t a, b;
+};
+bool g_prof_on = false;
+std::vector<ProfRec> g_prof;
+std::vector<hipEvent_t> g_event_pool;
+
+hipEvent_t pool_event() {
+  if (!g_event_pool.empty()) {
+    hipEvent_t e = g_event_pool.back();
+    g_event_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+void prof_clear() {
+  for (auto& r : g_prof) {
+    g_event_pool.push_back(r.a);
+    g_event_pool.push_back(r.b);
+  }
+  g_prof.clear();
+}
+
+struct ProfScope {
+  ProfRec rec{nullptr, nullptr, nullptr};
+  hipStream_t st;
+  ProfScope(const char* tag, hipStream_t s) : st(s) {
+    if (!g_prof_on) return;
+    rec.tag = tag;
+    rec.a = pool_event();
+    rec.b = pool_event();
+    if (rec.a) hipEventRecord(rec.a, st);
+  }
+  ~ProfScope() {
+    if (!g_prof_on || !rec.a || !rec.b) return;
+    hipEventRecord(rec.b, st);
+    g_prof.push_back(rec);
+  }
+};
+
+#define PROF_TRY(tag, expr)            \
+  do {                                 \
+    ProfScope ps_(tag, st);            \
+    HIP_TRY(expr);                     \
+  } while (0)
+
+struct WsLayout {
+  size_t resid, xn, q, attn, act, rope, opart, ml, part, logits, total;
+  size_t part_floats;
+};
+
+WsLayout ws_layout(const ssm_model* m, int batch, int max_rows) {
+  const size_t es = m->dtype == SSM_DT_BF16 ? 2 : 4;
+  const size_t Mt = (size_t)batch * max_rows;
+  const size_t d = m->d_model, H = m->n_heads, Hkv = m->n_kv_heads, dh = m->head_dim;
+  const size_t F = m->ffn_dim, V = m->vocab;
+  const size_t qkv = (H + 2 * Hkv) * dh;
+  size_t maxn = qkv;
+  if (2 * F > maxn) maxn = 2 * F;
+  if (V > maxn) maxn = V;
+  WsLayout w{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o = off; off += align256(bytes); return o; };
+  w.resid = take(Mt * d * 4);
+  w.xn = take(Mt * d * es);
+  w.q = take(Mt * H * dh * es);
+  w.attn = take(Mt * H * dh * es);
+  w.act = take(Mt * F * es);
+  w.rope = take((size_t)max_rows * (dh / 2) * 8);
+  w.opart = take((size_t)ATTN_MAX_SPLITS * Mt * H * dh * 4);
+  w.ml = take((size_t)ATTN_MAX_SPLITS * Mt * H * 2 * 4);
+  w.part_floats = gemm_split_ws_floats((int)Mt, (int)maxn);
+  w.part = take(w.part_floats * 4);
+  w.logits = take(Mt * V * 4);
+  w.total = off;
+  return w;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* ssm_last_error(void) { return g_err.c_str(); }
+
+int32_t ssm_select_count(const ssm_select_params* p, int32_t* n_rows, int32_t* n_suffix,
+                         int32_t* first_out_row) {
+  SelectLayout L;
+  int32_t rc = layout_of(p, L);
+  if (rc) return rc;
+  if (n_rows) *n_rows = L.n_rows;
+  if (n_suffix) *n_suffix = L.n_suffix;
+  if (first_out_row) *first_out_row = L.n_prefix;
+  return ok();
+}
+
+int32_t ssm_select_suffix(const ssm_select_params* p, int32_t batch, int32_t seq_len,
+                          const int32_t* d_tokens, int32_t* d_pos, int32_t* d_tok_c,
+                          int8_t* d_region, int32_t cap, int32_t* n_rows, int32_t* n_suffix,
+                          int32_t* first_out_row, void* stream) {
+  SelectLayout L;
+  int32_t rc = layout_of(p, L);
+  if (rc) return rc;
+  if (batch < 1) return fail(SSM_E_INVAL, "batch %d < 1", batch);
+  if (seq_len != p->prompt_len + p->gen_len)
+    return fail(SSM_E_INVAL, "seq_len %d != prompt_len + gen_len", seq_len);
+  if (!d_tokens || !d_pos || !d_tok_c) return fail(SSM_E_INVAL, "null device pointer");
+  if (cap < L.n_rows) return fail(SSM_E_CAPACITY, "cap %d < n_rows %d", cap, L.n_rows);
+  if (n_rows) *n_rows = L.n_rows;
+  if (n_suffix) *n_suffix = L.n_suffix;
+  if (first_out_row) *first_out_row = L.n_prefix;
+  hipStream_t st = (hipStream_t)stream;
+  PROF_TRY("select", launch_select(L, batch, seq_len, d_tokens, d_pos, d_tok_c, d_region, cap, st));
+  return ok();
+}
+
+int32_t ssm_embed_suffix(const ssm_model* m, int32_t batch, int32_t seq_len,
+                         const int32_t* d_tok_c, int32_t tok_stride, const int32_t* d_pos,
+                         const int8_t* d_region, int32_t n_rows, const int32_t* d_pred_ids,
+                         const float* d_pred_w, const int32_t* d_pred_step, int32_t prev_step,
+                         int32_t k, float alpha, float* d_x, void* stream) {
+  if (!m) return fail(SSM_E_INVAL, "null model");
+  if (m->dtype != SSM_DT_F32 && m->dtype != SSM_DT_BF16) return fail(SSM_E_INVAL, "unknown dtype");
+  if (!m->tok_emb || m->d_model <= 0 || m->vocab <= 1 || m->mask_id < 0 || m->mask_id >= m->vocab)
+    return fail(SSM_E_INVAL, "bad embedding table description");
+  if (batch < 1 || seq_len < 1 || n_rows < 0 || tok_stride < n_rows)
+    return fail(SSM_E_INVAL, "bad sizes (batch %d, seq_len %d, n_rows %d, tok_stride %d)", batch, seq_len, n_rows, tok_stride);
+  if (k < 1 || k > 8) return fail(SSM_E_INVAL, "k %d not in [1, 8]", k);
+  if (!(alpha >= 0.f && alpha <= 1.f)) return fail(SSM_E_INVAL, "alpha not in [0, 1]");
+  if (!d_tok_c || !d_pos || !d_region || !d_pred_ids || !d_pred_w || !d_pred_step || !d_x)
+    return fail(SSM_E_INVAL, "null device pointer");
+  hipStream_t st = (hipStream_t)stream;
+  PROF_TRY("embed", launch_embed(m->dtype, m->tok_emb, m->d_model, m->vocab, m->mask_id, batch,
+                                 seq_len, d_tok_c, tok_stride, d_pos, d_region, n_rows, d_pred_ids,
+                                 d_pred_w, d_pred_step, prev_step, k, alpha, d_x, st));
+  return ok();
+}
+
+int32_t ssm_workspace_size(const ssm_model* m, int32_t batch, int32_t max_rows, size_t* bytes) {
+  int32_t rc = check_model(m);
+  if (rc) return rc;
+  if (batch < 1 || max_rows < 1 || !bytes) return fail(SSM_E_INVAL, "bad workspace query");
+  *bytes = ws_layout(m, batch, max_rows).total;
+  return ok();
+}
+
+int32_t ssm_denoise_step(const ssm_model* m, const ssm_kv_cache* cache, int32_t cache_mode,
+                         int32_t n_cached, int32_t batch, const int32_t* d_pos, int32_t n_rows,
+                         const float* d_x, int32_t first_out_row, int32_t k, int32_t* d_argmax,
+                         float* d_conf, int32_t* d_topk_ids, float* d_topk_w,
+                         float* d_logits_dbg, float* d_hidden_dbg, void* d_ws, size_t ws_bytes,
+                         void* stream) {
+  int32_t rc = check_model(m);
+  if (rc) return rc;
+  if (batch < 1 || n_rows < 1) return fail(SSM_E_INVAL, "batch %d / n_rows %d < 1", batch, n_rows);
+  if (first_out_row < 0 || first_out_row >= n_rows)
+    return fail(SSM_E_INVAL, "first_out_row %d not in [0, n_rows)", first_out_row);
+  if (k < 1 || k > 8 || k > m->vocab - 1) return fail(SSM_E_INVAL, "k %d not in [1, 8]", k);
+  if (!d_pos || !d_x || !d_argmax || !d_conf || !d_topk_ids || !d_topk_w || !d_ws)
+    return fail(SSM_E_INVAL, "null device pointer");
+  if (!cache || !cache->k || !cache->v) return fail(SSM_E_INVAL, "null KV cache");
+  if (cache_mode == SSM_CACHE_OFF || cache_mode == SSM_CACHE_WRITE) {
+    if (n_cached != 0) return fail(SSM_E_INVAL, "n_cached must be 0 unless cache_mode is READ");
+  } else if (cache_mode == SSM_CACHE_READ) {
+    if (n_cached < 1) return fail(SSM_E_INVAL, "cache_mode READ needs n_cached >= 1");
+  } else {
+    return fail(SSM_E_INVAL, "unknown cache_mode %d", cache_mode);
+  }
+  if ((long long)n_cached + n_rows > cache->capacity)
+    return fail(SSM_E_CAPACITY, "cache capacity %d < n_cached %d + n_rows %d", cache->capacity, n_cached, n_rows);
+  const WsLayout w = ws_layout(m, batch, n_rows);
+  if (ws_bytes < w.total) return fail(SSM_E_CAPACITY, "workspace %zu < %zu bytes", ws_bytes, w.total);
+
+  hipStream_t st = (hipStream_t)stream;
+  const int dt = m->dtype;
+  const size_t es = dt == SSM_DT_BF16 ? 2 : 4;
+  const int d = m->d_model, H = m->n_heads, Hkv = m->n_kv_heads, dh = m->head_dim;
+  const int F = m->ffn_dim, V = m->vocab;
+  const int Mt = batch * n_rows, n_out = n_rows - first_out_row, Mo = batch * n_out;
+  const int Nk = n_cached + n_rows;
+  char* ws = (char*)d_ws;
+  float* resid = (float*)(ws + w.resid);
+  void* xn = ws + w.xn;
+  void* qb = ws + w.q;
+  void* attn = ws + w.attn;
+  void* act = ws + w.act;
+  float2* rope = (float2*)(ws + w.rope);
+  SplitWs sws{(float*)(ws + w.part), w.part_floats};
+  AttnWs aws{(float*)(ws + w.opart), (float*)(ws + w.ml), ATTN_MAX_SPLITS};
+  float* logits = d_logits_dbg ? d_logits_dbg : (float*)(ws + w.logits);
+  const size_t layer_kv = (size_t)batch * Hkv * cache->capacity * dh * es;
+
+  PROF_TRY("rope_table", launch_rope_table(d_pos, n_rows, dh, m->rope_base, rope, st));
+  HIP_TRY(hipMemcpyAsync(resid, d_x, (size_t)Mt * d * 4, hipMemcpyDeviceToDevice, st));
+  for (int l = 0; l < m->n_layers; ++l) {
+    const ssm_layer& y = m->layers[l];
+    char* kc = (char*)cache->k + l * layer_kv;
+    char* vc = (char*)cache->v + l * layer_kv;
+    PROF_TRY("rmsnorm", launch_rmsnorm(dt, resid, d, y.attn_norm, m->rms_eps, xn, Mt, Mt, 0, 0, st));
+    QKVOut qo{qb, kc, vc, cache->capacity, n_cached, n_rows, rope};
+    PROF_TRY("gemm_qkv", gemm_qkv(dt, xn, Mt, d, y.wq, y.wk, y.wv, H, Hkv, dh, qo, sws, st));
+    PROF_TRY("attention", attention(dt, qb, kc, vc, batch, H, Hkv, dh, n_rows, Nk, cache->capacity, attn, aws, st));
+    PROF_TRY("gemm_o", gemm_resid(dt, attn, Mt, H * dh, y.wo, d, resid, sws, st));
+    PROF_TRY("rmsnorm", launch_rmsnorm(dt, resid, d, y.ffn_norm, m->rms_eps, xn, Mt, Mt, 0, 0, st));
+    PROF_TRY("gemm_gate_up", gemm_swiglu(dt, xn, Mt, d, y.w_gate, y.w_up, F, act, sws, st));
+    PROF_TRY("gemm_down", gemm_resid(dt, act, Mt, F, y.w_down, d, resid, sws, st));
+  }
+  if (d_hidden_dbg)
+    HIP_TRY(hipMemcpyAsync(d_hidden_dbg, resid, (size_t)Mt * d * 4, hipMemcpyDeviceToDevice, st));
+  // final norm of the output rows only: output row o <- row first_out_row + o % n_out of
+  // sequence o / n_out
+  PROF_TRY("rmsnorm", launch_rmsnorm(dt, resid, d, m->final_norm, m->rms_eps, xn, Mo, n_out, n_rows,
+                         first_out_row, st));
+  PROF_TRY("gemm_lm_head", gemm_store(dt, xn, Mo, d, m->lm_head, V, logits, V, sws, st));
+  PROF_TRY("rowstats", launch_rowstats(logits, Mo, V, V, m->mask_id, k, d_argmax, d_conf, d_topk_ids,
+                          d_topk_w, st));
+  return ok();
+}
+
+int32_t ssm_unmask(int32_t* d_tokens, int32_t batch, int32_t seq_len, int32_t block_start,
+                   int32_t block_size, int32_t mask_id, int32_t rule, int32_t n_per_step,
+                   float threshold, const int32_t* d_argmax, const float* d_conf,
+                   const int32_t* d_topk_ids, const float* d_topk_w, int32_t k, int32_t n_out,
+                   const int32_t* d_pos_out, int32_t step, int32_t* d_pred_ids, float* d_pred_w,
+                   int32_t* d_pred_step, uint8_t* d_selected, int32_t* d_masked_left,
+                   void* stream) {
+  if (batch < 1 || seq_len < 1) return fail(SSM_E_INVAL, "bad batch / seq_len");
+  if (block_size < 1 || block_size > 1024) return fail(SSM_E_INVAL, "block_size %d not in [1, 1024]", block_size);
+  if (block_start < 0 || block_start + block_size > seq_len)
+    return fail(SSM_E_INVAL, "block [%d, %d) outside the sequence", block_start, block_start + block_size);
+  if (n_out < block_size) return fail(SSM_E_INVAL, "n_out %d < block_size %d", n_out, block_size);
+  if (k < 1 || k > 8) return fail(SSM_E_INVAL, "k %d not in [1, 8]", k);
+  if (rule != SSM_UNMASK_TOPN && rule != SSM_UNMASK_THRESHOLD && rule != SSM_UNMASK_MARGIN)
+    return fail(SSM_E_INVAL, "unknown rule %d", rule);
+  if (rule == SSM_UNMASK_TOPN && n_per_step < 1) return fail(SSM_E_INVAL, "n_per_step %d < 1", n_per_step);
+  if (rule == SSM_UNMASK_MARGIN && k < 2) return fail(SSM_E_INVAL, "the margin rule needs k >= 2");
+  if (!d_tokens || !d_argmax || !d_conf || !d_topk_ids || !d_topk_w) return fail(SSM_E_INVAL, "null device pointer");
+  if (n_out > block_size && (!d_pos_out || !d_pred_ids || !d_pred_w || !d_pred_step))
+    return fail(SSM_E_INVAL, "null prediction-state pointer");
+  hipStream_t st = (hipStream_t)stream;
+  PROF_TRY("unmask", launch_unmask(d_tokens, batch, seq_len, block_start, block_size, mask_id,
+                                   rule, n_per_step, threshold, d_argmax, d_conf, d_topk_ids,
+                                   d_topk_w, k, n_out, d_pos_out, step, d_pred_ids, d_pred_w,
+                                   d_pred_step, d_selected, d_masked_left, st));
+  return ok();
+}
+
+int32_t ssm_profile_enable(int32_t on) {
+  g_prof_on = on != 0;
+  prof_clear();
+  return ok();
+}
+
+int32_t ssm_profile_query(const char* tag, int32_t* count, double* total_ms) {
+  if (!tag || !count || !total_ms) return fail(SSM_E_INVAL, "null argument");
+  int n = 0;
+  double tot = 0.0;
+  for (auto& r : g_prof) {
+    if (strcmp(r.tag, tag) != 0) continue;
+    hipError_t e = hipEventSynchronize(r.b);
+    if (e != hipSuccess) return fail(SSM_E_HIP, "hipEventSynchronize: %s", hipGetErrorString(e));
+    float ms = 0.f;
+    e = hipEventElapsedTime(&ms, r.a, r.b);
+    if (e != hipSuccess) return fail(SSM_E_HIP, "hipEventElapsedTime: %s", hipGetErrorString(e));
+    ++n;
+    tot += ms;
+  }
+  *count = n;
+  *total_ms = tot;
+  return ok();
+}
+
+}  // extern "C"

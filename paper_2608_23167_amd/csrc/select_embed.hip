@@ -1,0 +1,118 @@
+// Compacted row list of the sparse input (Section 3.2, Eq. 1-5) and the
+// soft suffix embedding of its rows (Section 3.2, Eq. 6-8).
+#include "internal.h"
+
+namespace ssm {
+
+// Row r of [prefix; block; local; middle; tail] -> (position, region).  Every
+// row is computed independently in closed form, so the kernel is a pure
+// coalesced map over rows.
+__device__ __forceinline__ void row_position(const SelectLayout& L, int r, int& p, int& g) {
+  if (r < L.n_prefix) { p = r; g = 0; return; }
+  r -= L.n_prefix;
+  if (r < L.b) { p = L.P + r; g = 1; return; }
+  r -= L.b;
+  if (r < L.n_local) { p = L.s0 + r; g = 2; return; }
+  r -= L.n_local;
+  if (r < L.n_mid) {
+    if (L.mid_mode == 1) p = L.mid_first + r * L.b;
+    else p = L.mid_lo + (int)(((long long)r * L.mid_len) / L.n_mid);
+    g = 3;
+    return;
+  }
+  r -= L.n_mid;
+  if (L.n_tail == 1) p = L.tail_lo + L.tail_len - 1;
+  else p = L.tail_lo + (int)(((long long)r * (L.tail_len - 1)) / (L.n_tail - 1));
+  g = 4;
+}
+
+__global__ void __launch_bounds__(256) select_kernel(SelectLayout L, const int32_t* __restrict__ tokens,
+                                                     int seq_len, int32_t* __restrict__ pos,
+                                                     int32_t* __restrict__ tok_c,
+                                                     int8_t* __restrict__ region, int cap) {
+  const int r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= L.n_rows) return;
+  int p, g;
+  row_position(L, r, p, g);
+  const int s = blockIdx.y;
+  if (s == 0) {
+    pos[r] = p;
+    if (region) region[r] = (int8_t)g;
+  }
+  tok_c[(size_t)s * cap + r] = tokens[(size_t)s * seq_len + p];
+}
+
+hipError_t launch_select(const SelectLayout& L, int batch, int seq_len, const int32_t* tokens,
+                         int32_t* pos, int32_t* tok_c, int8_t* region, int cap, hipStream_t st) {
+  if (L.n_rows == 0) return hipSuccess;
+  dim3 grid(ceil_div(L.n_rows, 256), batch);
+  hipLaunchKernelGGL(select_kernel, grid, dim3(256), 0, st, L, tokens, seq_len, pos, tok_c,
+                     region, cap);
+  return hipGetLastError();
+}
+
+// One workgroup per (row, sequence).  An out-of-range id or position makes
+// the row NaN instead of reading outside the tables.
+template <typename T>
+__global__ void __launch_bounds__(256) embed_kernel(
+    const T* __restrict__ E, int d, int vocab, int mask_id, int seq_len,
+    const int32_t* __restrict__ tok_c, int tok_stride, const int32_t* __restrict__ pos,
+    const int8_t* __restrict__ region, int n_rows, const int32_t* __restrict__ pred_ids,
+    const float* __restrict__ pred_w, const int32_t* __restrict__ pred_step, int prev_step, int k,
+    float alpha, float* __restrict__ x) {
+  const int r = blockIdx.x, s = blockIdx.y;
+  float* out = x + ((size_t)s * n_rows + r) * d;
+  const int p = pos[r];
+  const bool pos_ok = p >= 0 && p < seq_len;
+  const size_t sp = (size_t)s * seq_len + (pos_ok ? p : 0);
+  const bool soft = pos_ok && region[r] >= 2 && prev_step >= 0 && pred_step[sp] == prev_step;
+  if (!soft) {
+    const int tok = tok_c[(size_t)s * tok_stride + r];
+    const bool ok = pos_ok && tok >= 0 && tok < vocab;
+    const T* e = E + (size_t)(ok ? tok : 0) * d;
+    for (int c = threadIdx.x; c < d; c += blockDim.x) out[c] = ok ? ldf(e + c) : __builtin_nanf("");
+    return;
+  }
+  int ids[8];
+  float w[8];
+  bool ok = true;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    ids[i] = 0;
+    w[i] = 0.f;
+    if (i < k) {
+      ids[i] = pred_ids[sp * k + i];
+      w[i] = pred_w[sp * k + i];
+      ok = ok && ids[i] >= 0 && ids[i] < vocab;
+    }
+  }
+  const T* em = E + (size_t)mask_id * d;
+  for (int c = threadIdx.x; c < d; c += blockDim.x) {
+    float acc = 0.f;  // Eq. 7: sum_i w_i e_{id_i}, in the stored order
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      if (i < k) acc = acc + w[i] * ldf(E + (size_t)(ok ? ids[i] : 0) * d + c);
+    const float v = (1.0f - alpha) * ldf(em + c) + alpha * acc;  // Eq. 8
+    out[c] = ok ? v : __builtin_nanf("");
+  }
+}
+
+hipError_t launch_embed(int dtype, const void* E, int d, int vocab, int mask_id, int batch,
+                        int seq_len, const int32_t* tok_c, int tok_stride, const int32_t* pos,
+                        const int8_t* region, int n_rows, const int32_t* pred_ids,
+                        const float* pred_w, const int32_t* pred_step, int prev_step, int k,
+                        float alpha, float* x, hipStream_t st) {
+  if (n_rows == 0) return hipSuccess;
+  dim3 grid(n_rows, batch);
+  if (dtype == 0)
+    hipLaunchKernelGGL(embed_kernel<float>, grid, dim3(256), 0, st, (const float*)E, d, vocab,
+                       mask_id, seq_len, tok_c, tok_stride, pos, region, n_rows, pred_ids, pred_w,
+                       pred_step, prev_step, k, alpha, x);
+  else
+    hipLaunchKernelGGL(embed_kernel<bf16_t>, grid, dim3(256), 0, st, (const bf16_t*)E, d, vocab,
+                       mask_id, seq_len, tok_c, tok_stride, pos, region, n_rows, pred_ids, pred_w,
+                       pred_step, prev_step, k, alpha, x);
+  return hipGetLastError();
+}
+
+}  // namespace ssm

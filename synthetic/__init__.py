@@ -8,10 +8,12 @@ two sides see identical inputs while sharing no computation.
 from .configs import (ModelShape, Workload, TINY, LLADA_8B, DREAM_7B, WORKLOADS,
                       workload, sharpened)
 from .generate import (ModelWeights, LayerWeights, make_weights, make_layer,
-                       prompt_tokens, initial_tokens, seeded_normal, seeded_uniform_ints)
+                       prompt_tokens, initial_tokens, seeded_normal, seeded_uniform_ints,
+                       mid_generation_state)
 
 __all__ = [
     "ModelShape", "Workload", "TINY", "LLADA_8B", "DREAM_7B", "WORKLOADS", "workload",
     "sharpened", "ModelWeights", "LayerWeights", "make_weights", "make_layer",
     "prompt_tokens", "initial_tokens", "seeded_normal", "seeded_uniform_ints",
+    "mid_generation_state",
 ]

@@ -134,3 +134,33 @@ def initial_tokens(wl: Workload, seed: Optional[int] = None, device="cpu") -> to
     p = prompt_tokens(wl, seed, device)
     gen = torch.full((wl.batch, wl.gen_len), wl.model.mask_id, dtype=torch.int32, device=device)
     return torch.cat([p, gen], dim=1).contiguous()
+
+
+def mid_generation_state(wl: Workload, block_idx: int, step: int, seed: int = 0,
+                         decoded_frac: float = 0.5, predicted_frac: float = 0.8):
+    """A seeded decoding state at the start of a step inside block `block_idx`:
+    earlier blocks fully decoded with random ids, part of the current block
+    decoded, and a previous-step prediction (random top-k ids with random
+    descending weights summing to one) on part of the suffix.
+
+    Returns numpy arrays (tokens [B, L], pred_ids [B, L, k], pred_w [B, L, k],
+    pred_step [B, L]); predictions carry the stamp step - 1.
+    """
+    import numpy as np
+    rng = np.random.default_rng(_derive(seed, f"state{block_idx}.{step}") & 0xFFFFFFFF)
+    B, Lt, k = wl.batch, wl.total_len, wl.topk
+    V, mask = wl.model.vocab, wl.model.mask_id
+    tokens = initial_tokens(wl, seed).numpy().copy()
+    P = wl.prompt_len + block_idx * wl.block_size
+    dec = rng.integers(0, V - 1, size=(B, Lt)).astype(np.int32)
+    dec = dec + (dec >= mask)
+    tokens[:, wl.prompt_len:P] = dec[:, wl.prompt_len:P]
+    blk = rng.random((B, wl.block_size)) < decoded_frac
+    tokens[:, P:P + wl.block_size][blk] = dec[:, P:P + wl.block_size][blk]
+    pred_ids = rng.integers(0, V - 1, size=(B, Lt, k)).astype(np.int32)
+    pred_ids = pred_ids + (pred_ids >= mask)
+    w = np.sort(rng.random((B, Lt, k)), axis=-1)[..., ::-1]
+    pred_w = (w / w.sum(-1, keepdims=True)).astype(np.float32)
+    pred_step = np.where(rng.random((B, Lt)) < predicted_frac, step - 1, -1).astype(np.int32)
+    pred_step[:, :P + wl.block_size] = -1
+    return tokens.astype(np.int32), pred_ids, pred_w, pred_step

@@ -1,0 +1,166 @@
+"""The C ABI library loads on a CPU-only host, exports every function
+include/*.h declares, and rejects invalid arguments on the host before any
+GPU work (so these tests need no GPU)."""
+import ctypes as C
+import glob
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    names = set()
+    for h in glob.glob(os.path.join(ROOT, "include", "*.h")):
+        text = open(h).read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        names.update(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(ssm_\w+)\s*\(", text, flags=re.M))
+    return sorted(names)
+
+
+def test_header_declares_the_four_calls():
+    names = declared_functions()
+    for n in ("ssm_select_suffix", "ssm_embed_suffix", "ssm_denoise_step", "ssm_unmask"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    from paper_2608_23167_amd import _lib
+    lib = _lib.lib()
+    for n in declared_functions():
+        assert hasattr(lib, n), n
+    assert set(declared_functions()) == set(_lib.exported_symbols())
+
+
+def _params(**kw):
+    from paper_2608_23167_amd.api import select_params
+    d = dict(prompt_len=32, gen_len=128, block_size=32, block_idx=0, local_budget=32,
+             middle_budget=8, middle_mode=0, tail_budget=4, include_prefix=True)
+    d.update(kw)
+    return select_params(**d)
+
+
+def test_select_count_closed_form():
+    from paper_2608_23167_amd.api import ssm_select_count
+    assert ssm_select_count(_params()) == (108, 44, 32)
+    assert ssm_select_count(_params(block_idx=1)) == (132, 36, 64)
+    assert ssm_select_count(_params(block_idx=3, include_prefix=False)) == (32, 0, 0)
+    assert ssm_select_count(_params(local_budget=10**6)) == (32 + 32 + 96, 96, 32)
+
+
+def test_select_count_matches_oracle_sweep():
+    from oracle import selection as S
+    from paper_2608_23167_amd.api import ssm_select_count
+    for b, nb in ((1, 9), (4, 8), (32, 4)):
+        for j in range(nb):
+            for L, M, T, mode, inc in [(0, 0, 0, 0, 1), (b, 3, 2, 0, 1), (2 * b + 1, 100, 5, 0, 0),
+                                       (b, 0, 2, 1, 1), (3 * b, 7, 1, 1, 0)]:
+                c = S.compacted_rows(7, b * nb, b, j, L, M, mode, T, bool(inc))
+                got = ssm_select_count(_params(prompt_len=7, gen_len=b * nb, block_size=b, block_idx=j,
+                                               local_budget=L, middle_budget=M, middle_mode=mode,
+                                               tail_budget=T, include_prefix=inc))
+                assert got == (len(c.pos), c.n_suffix, c.first_out_row)
+
+
+@pytest.mark.parametrize("bad", [dict(block_idx=4), dict(block_idx=-1), dict(gen_len=100),
+                                 dict(block_size=0), dict(block_size=2048, gen_len=2048),
+                                 dict(local_budget=-1), dict(middle_mode=7), dict(prompt_len=-3),
+                                 dict(include_prefix=2)])
+def test_select_rejects_invalid(bad):
+    from paper_2608_23167_amd import _lib as L
+    from paper_2608_23167_amd.api import ssm_select_count
+    p = _params(**bad)
+    if "include_prefix" in bad:
+        p.include_prefix = bad["include_prefix"]
+    with pytest.raises(L.SSMError) as e:
+        ssm_select_count(p)
+    assert e.value.code == L.SSM_E_INVAL
+
+
+def test_select_suffix_validation_before_launch():
+    from paper_2608_23167_amd import _lib as L
+    lib = L.lib()
+    p = _params()
+    n = C.c_int32()
+    fake = C.c_void_p(0x1000)   # never dereferenced: validation fails first
+    rc = lib.ssm_select_suffix(C.byref(p), 1, 160, fake, fake, fake, None, 10, C.byref(n), None, None, None)
+    assert rc == L.SSM_E_CAPACITY and b"cap" in lib.ssm_last_error()
+    rc = lib.ssm_select_suffix(C.byref(p), 1, 161, fake, fake, fake, None, 500, None, None, None, None)
+    assert rc == L.SSM_E_INVAL
+    rc = lib.ssm_select_suffix(C.byref(p), 0, 160, fake, fake, fake, None, 500, None, None, None, None)
+    assert rc == L.SSM_E_INVAL
+    rc = lib.ssm_select_suffix(C.byref(p), 1, 160, None, fake, fake, None, 500, None, None, None, None)
+    assert rc == L.SSM_E_INVAL
+
+
+def _model(**kw):
+    from paper_2608_23167_amd import _lib as L
+    fake = 0x1000
+    lay = (L.Layer * 2)(*[L.Layer(*([fake] * 9)) for _ in range(2)])
+    d = dict(n_layers=2, d_model=4096, n_heads=32, n_kv_heads=32, head_dim=128, ffn_dim=12288,
+             vocab=126464, mask_id=126463, dtype=L.SSM_DT_BF16)
+    d.update(kw)
+    m = L.Model(d["n_layers"], d["d_model"], d["n_heads"], d["n_kv_heads"], d["head_dim"],
+                d["ffn_dim"], d["vocab"], d["mask_id"], d["dtype"], 10000.0, 1e-5, fake, fake,
+                fake, C.cast(lay, C.POINTER(L.Layer)))
+    m._keep = lay
+    return m
+
+
+@pytest.mark.parametrize("bad,code", [
+    (dict(d_model=4000), -2), (dict(n_kv_heads=5), -2), (dict(mask_id=126464), -1),
+    (dict(dtype=3), -1), (dict(head_dim=64, n_heads=64), -5), (dict(vocab=126465, mask_id=0), -5),
+])
+def test_model_validation(bad, code):
+    from paper_2608_23167_amd import _lib as L
+    lib = L.lib()
+    m = _model(**bad)
+    n = C.c_size_t()
+    assert lib.ssm_workspace_size(C.byref(m), 1, 100, C.byref(n)) == code
+
+
+def test_workspace_size_and_step_validation():
+    from paper_2608_23167_amd import _lib as L
+    lib = L.lib()
+    m = _model()
+    n = C.c_size_t()
+    assert lib.ssm_workspace_size(C.byref(m), 1, 376, C.byref(n)) == 0
+    assert n.value > 376 * 126464 * 4
+    fake = C.c_void_p(0x1000)
+    cache = L.KVCache(0x1000, 0x1000, 400)
+    args = lambda mode, n_cached, rows, k=5, ws=n.value, first=0: (
+        C.byref(m), C.byref(cache), mode, n_cached, 1, fake, rows, fake, first, k, fake, fake,
+        fake, fake, None, None, fake, ws, None)
+    assert lib.ssm_denoise_step(*args(L.SSM_CACHE_READ, 100, 376)) == L.SSM_E_CAPACITY
+    assert lib.ssm_denoise_step(*args(L.SSM_CACHE_WRITE, 10, 120)) == L.SSM_E_INVAL
+    assert lib.ssm_denoise_step(*args(L.SSM_CACHE_READ, 0, 120)) == L.SSM_E_INVAL
+    assert lib.ssm_denoise_step(*args(7, 0, 120)) == L.SSM_E_INVAL
+    assert lib.ssm_denoise_step(*args(0, 0, 120, k=9)) == L.SSM_E_INVAL
+    assert lib.ssm_denoise_step(*args(0, 0, 120, ws=1000)) == L.SSM_E_CAPACITY
+    assert lib.ssm_denoise_step(*args(0, 0, 120, first=120)) == L.SSM_E_INVAL
+
+
+def test_unmask_and_embed_validation():
+    from paper_2608_23167_amd import _lib as L
+    lib = L.lib()
+    f = C.c_void_p(0x1000)
+    base = [f, 1, 200, 64, 32, 999, 0, 1, 0.9, f, f, f, f, 4, 40, f, 3, f, f, f, None, None, None]
+    def with_(**kw):
+        a = list(base)
+        idx = dict(batch=1, seq_len=2, block_start=3, block_size=4, rule=6, n_per_step=7, k=13, n_out=14)
+        for k, v in kw.items():
+            a[idx[k]] = v
+        return a
+    for kw in (dict(block_size=0), dict(block_start=180), dict(rule=5), dict(n_per_step=0),
+               dict(k=9), dict(n_out=10), dict(rule=2, k=1)):
+        assert lib.ssm_unmask(*with_(**kw)) == L.SSM_E_INVAL, kw
+    m = _model()
+    e = [C.byref(m), 1, 100, f, 50, f, f, 50, f, f, f, 3, 5, 0.4, f, None]
+    e2 = list(e); e2[12] = 0
+    assert lib.ssm_embed_suffix(*e2) == L.SSM_E_INVAL
+    e3 = list(e); e3[13] = 1.5
+    assert lib.ssm_embed_suffix(*e3) == L.SSM_E_INVAL
+    e4 = list(e); e4[4] = 10
+    assert lib.ssm_embed_suffix(*e4) == L.SSM_E_INVAL

@@ -1,0 +1,152 @@
+"""GPU step parity against the oracle (teacher-forced: every GPU step starts
+from the oracle's state before that step).
+
+fp32 mode (tiny model): hidden states and logits within max-abs 1e-4.
+bf16 mode (LLaDA / Dream shapes): relative error <= 2e-2 against the fp32
+oracle run on the bf16-rounded weights.  Decisions (argmax, top-k ids,
+unmasking) must agree wherever the oracle's probability margin exceeds 1e-3.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle.generate as OG
+from synthetic import (WORKLOADS, initial_tokens, make_weights, mid_generation_state, sharpened)
+from tests._parity import (check_decisions, gpu_step, load_oracle_state, max_abs, rel_err)
+
+pytestmark = pytest.mark.gpu
+
+MARGIN = 1e-3
+
+
+def _decoder(wl, mw_dev):
+    from paper_2608_23167_amd.decoder import Decoder
+    from paper_2608_23167_amd.model import DeviceModel
+    return Decoder(wl, DeviceModel(wl.model, mw_dev))
+
+
+def _compare_step(out, rec, wl, fp32: bool):
+    B = wl.batch
+    assert np.array_equal(out["pos"], rec.rows.pos)
+    assert np.array_equal(out["region"], rec.rows.region)
+    tol_x = 1e-6 if fp32 else 1e-5
+    assert max_abs(out["x"], rec.x) < tol_x
+    if fp32:
+        assert max_abs(out["hidden"], rec.hidden) < 1e-4
+        for s in range(B):
+            assert max_abs(out["logits"][s], rec.stats[s].logits) < 1e-4
+            assert max_abs(out["conf"][s], rec.stats[s].conf) < 1e-5
+            assert max_abs(out["topk_w"][s], rec.stats[s].topk_w) < 1e-4
+    else:
+        assert rel_err(out["hidden"], rec.hidden) < 2e-2
+        for s in range(B):
+            assert rel_err(out["logits"][s], rec.stats[s].logits) < 2e-2
+    return check_decisions(out, rec, wl, MARGIN)
+
+
+def _compare_unmask(out, rec, wl):
+    """Unmasking decisions must agree where the oracle's ranking margin is wide."""
+    b = wl.block_size
+    for s in range(wl.batch):
+        st = rec.stats[s]
+        conf = st.conf[:b]
+        sel_o = rec.selected[s]
+        sel_g = out["selected"][s]
+        if wl.rule == "topn":
+            chosen = np.sort(conf[sel_o])
+            rest = conf[~sel_o & (rec.tokens_after[s, wl.prompt_len + rec.block_idx * b:][:b] == wl.model.mask_id)]
+            gap = (chosen.min() - rest.max()) if len(rest) and len(chosen) else 1.0
+            if gap > MARGIN:
+                assert np.array_equal(sel_g, sel_o)
+        else:
+            if np.all(np.abs(conf - wl.threshold) > MARGIN):
+                assert np.array_equal(sel_g, sel_o)
+
+
+@pytest.mark.parametrize("sharp", [False, True])
+def test_tiny_fp32_every_step(gpu, sharp):
+    wl = WORKLOADS["tiny"]
+    if sharp:
+        wl = sharpened(wl, 60.0)
+    mw = make_weights(wl.model, seed=0, norm_jitter=0.1, logit_scale=wl.logit_scale)
+    w = OG.NumpyWeights(mw)
+    dec = _decoder(wl, mw.to("cuda"))
+    tok0 = initial_tokens(wl).numpy()
+    st = OG.OracleState.start(tok0, wl.topk)
+    fracs = []
+    for j in range(wl.n_blocks):
+        for i in range(wl.steps_per_block()):
+            before = st.copy()
+            rec = OG.step(wl, w, st, j, i == 0)
+            load_oracle_state(dec, before)
+            out = gpu_step(dec, j, i == 0)
+            fracs.append(_compare_step(out, rec, wl, fp32=True))
+            _compare_unmask(out, rec, wl)
+    if sharp:
+        assert np.mean(fracs) > 0.9
+
+
+def test_tiny_fp32_cached_steps(gpu):
+    """Prefix cache on: block-start steps write the cache, later steps read it."""
+    wl = sharpened(WORKLOADS["tiny"], 60.0).replace(cache=True)
+    mw = make_weights(wl.model, seed=1, norm_jitter=0.1, logit_scale=wl.logit_scale)
+    w = OG.NumpyWeights(mw)
+    dec = _decoder(wl, mw.to("cuda"))
+    st = OG.OracleState.start(initial_tokens(wl, seed=2).numpy(), wl.topk)
+    for j in range(wl.n_blocks):
+        for i in range(wl.steps_per_block()):
+            before = st.copy()
+            rec = OG.step(wl, w, st, j, i == 0)
+            load_oracle_state(dec, before)
+            out = gpu_step(dec, j, i == 0)
+            assert out["info"].include_prefix == (i == 0)
+            _compare_step(out, rec, wl, fp32=True)
+
+
+def _state_from(wl, block_idx, step, seed):
+    t, pi, pw, ps = mid_generation_state(wl, block_idx, step, seed)
+    st = OG.OracleState.start(t, wl.topk)
+    st.pred_ids[:] = pi
+    st.pred_w[:] = pw
+    st.pred_step[:] = ps
+    st.step = step
+    return st
+
+
+def _bf16_case(wl, blocks, seed=0):
+    torch.manual_seed(0)
+    mw_dev = make_weights(wl.model, seed=seed, device="cuda", norm_jitter=0.1,
+                          logit_scale=wl.logit_scale)
+    w = OG.NumpyWeights(mw_dev, dtype=np.float32)
+    dec = _decoder(wl, mw_dev)
+    fracs = []
+    for j, n_steps in blocks:
+        st = _state_from(wl, j, 5 + 3 * j, seed)
+        for i in range(n_steps):
+            before = st.copy()
+            rec = OG.step(wl, w, st, j, i == 0)
+            load_oracle_state(dec, before)
+            out = gpu_step(dec, j, i == 0)
+            fracs.append(_compare_step(out, rec, wl, fp32=False))
+            _compare_unmask(out, rec, wl)
+    return fracs
+
+
+def test_llada_shape_2_layers_bf16(gpu):
+    wl = sharpened(WORKLOADS["llada_gen256"], 30.0)
+    wl = wl.replace(model=wl.model.with_layers(2))
+    fracs = _bf16_case(wl, [(0, 2), (5, 2)])
+    assert np.mean(fracs) > 0.8
+
+
+def test_dream_shape_gqa_2_layers_bf16(gpu):
+    wl = sharpened(WORKLOADS["dream_gen512"], 30.0)
+    wl = wl.replace(model=wl.model.with_layers(2))
+    fracs = _bf16_case(wl, [(0, 1), (14, 1)])
+    assert np.mean(fracs) > 0.8
+
+
+def test_llada_long_shape_2_layers_bf16(gpu):
+    wl = sharpened(WORKLOADS["llada_long2048"], 30.0)
+    wl = wl.replace(model=wl.model.with_layers(2))
+    _bf16_case(wl, [(0, 2), (31, 2)])

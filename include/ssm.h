@@ -71,6 +71,13 @@ enum {
 /* Model element types. */
 enum { SSM_DT_F32 = 0, SSM_DT_BF16 = 1 };
 
+/* Activation precision at the projections of a bfloat16 model. */
+enum {
+  SSM_ACT_BF16 = 0,     /* each projection input is rounded once to bfloat16                 */
+  SSM_ACT_BF16X2 = 1    /* each projection input is kept as a bfloat16 pair hi + lo and both  */
+                        /* parts are multiplied (weights stay bfloat16; twice the MFMA work)  */
+};
+
 /* Region tag of a compacted row. */
 enum {
   SSM_REGION_PREFIX = 0, SSM_REGION_BLOCK = 1, SSM_REGION_LOCAL = 2,
@@ -156,6 +163,7 @@ typedef struct ssm_model {
   const void* final_norm;  /* [d] device                                       */
   const void* lm_head;     /* [vocab, d] device                                */
   const ssm_layer* layers; /* HOST array of n_layers device-pointer sets       */
+  int32_t act_mode;        /* SSM_ACT_*; ignored for float32 models            */
 } ssm_model;
 
 /* Prefix KV cache: k and v are [n_layers, batch, n_kv_heads, capacity, head_dim]
@@ -260,7 +268,7 @@ int32_t ssm_unmask(int32_t* d_tokens, int32_t batch, int32_t seq_len, int32_t bl
 /*
  * on != 0: from now on every kernel launcher of the calls above is bracketed
  * by a pair of HIP events recorded on the call's stream, under a tag naming
- * the operation ("select", "embed", "rope_table", "rmsnorm", "gemm_qkv",
+ * the operation ("select", "embed", "rope_table", "row_rms", "gemm_qkv",
  * "attention", "gemm_o", "gemm_gate_up", "gemm_down", "gemm_lm_head",
  * "rowstats", "unmask").  Each call discards earlier records.  Not
  * thread-safe; meant for a single profiling thread.

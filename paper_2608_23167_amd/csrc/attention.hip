@@ -19,7 +19,7 @@ constexpr float LOG2E = 1.4426950408889634f;
 __global__ void __launch_bounds__(256) attn_bf16_kernel(
     const bf16_t* __restrict__ Q, const bf16_t* __restrict__ Kc, const bf16_t* __restrict__ Vc,
     int H, int Hkv, int Mq, int Nk, int cap, int keys_per_split, float scale_log2,
-    bf16_t* __restrict__ O, float* __restrict__ Opart, float* __restrict__ ML) {
+    float* __restrict__ O, float* __restrict__ Opart, float* __restrict__ ML) {
   constexpr int DH = 128, KT = 64, KS = DH + 8, VS = KT + 8;
   __shared__ __attribute__((aligned(16))) bf16_t Ks[KT * KS];
   __shared__ __attribute__((aligned(16))) bf16_t Vt[DH * VS];
@@ -129,14 +129,9 @@ __global__ void __launch_bounds__(256) attn_bf16_kernel(
   // o[db][r] = O^T[dh 16db + 4g + r][query c16]
   if (Opart == nullptr) {
     const float inv = 1.0f / l_run;
-    bf16_t* out = O + ((size_t)s * Mq + q) * (size_t)(H * DH) + h * DH;
+    float* out = O + ((size_t)s * Mq + q) * (size_t)(H * DH) + h * DH;
 #pragma unroll
-    for (int db = 0; db < 8; ++db) {
-      uint16_t tmp[4];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) tmp[r] = f2bf(o[db][r] * inv);
-      *(uint2*)(out + 16 * db + 4 * g) = *(const uint2*)tmp;
-    }
+    for (int db = 0; db < 8; ++db) *(f32x4_t*)(out + 16 * db + 4 * g) = o[db] * inv;
   } else {
     const size_t row = ((size_t)split * gridDim.y + bh) * Mq + q;
     float* op = Opart + row * DH;
@@ -193,9 +188,8 @@ __global__ void __launch_bounds__(64) attn_f32_kernel(
 }
 
 // Combines the splits of one (sequence, head, query) row, in split order.
-template <typename T>
 __global__ void attn_merge_kernel(const float* __restrict__ Opart, const float* __restrict__ ML,
-                                  int S, int BH, int H, int Mq, int DH, T* __restrict__ O) {
+                                  int S, int BH, int H, int Mq, int DH, float* __restrict__ O) {
   const int row = blockIdx.x;               // over BH * Mq
   const int bh = row / Mq, q = row % Mq, s = bh / H, h = bh % H;
   float M = -INFINITY;
@@ -207,19 +201,19 @@ __global__ void attn_merge_kernel(const float* __restrict__ Opart, const float* 
     if (l > 0.f) L += l * exp2f(ML[r * 2] - M);
   }
   const float inv = 1.0f / L;
-  T* out = O + ((size_t)s * Mq + q) * (size_t)(H * DH) + h * DH;
+  float* out = O + ((size_t)s * Mq + q) * (size_t)(H * DH) + h * DH;
   for (int c = threadIdx.x; c < DH; c += blockDim.x) {
     float acc = 0.f;
     for (int i = 0; i < S; ++i) {
       const size_t r = (size_t)i * BH * Mq + row;
       if (ML[r * 2 + 1] > 0.f) acc += Opart[r * DH + c] * exp2f(ML[r * 2] - M);
     }
-    stf(out + c, acc * inv);
+    out[c] = acc * inv;
   }
 }
 
 hipError_t attention(int dtype, const void* q, const void* kc, const void* vc, int B, int H,
-                     int Hkv, int dh, int Mq, int Nk, int cap, void* out, AttnWs ws,
+                     int Hkv, int dh, int Mq, int Nk, int cap, float* out, AttnWs ws,
                      hipStream_t st) {
   if (Mq == 0) return hipSuccess;
   const int BH = B * H;
@@ -237,12 +231,12 @@ hipError_t attention(int dtype, const void* q, const void* kc, const void* vc, i
   if (dtype == 1) {
     hipLaunchKernelGGL(attn_bf16_kernel, grid, dim3(256), 0, st, (const bf16_t*)q,
                        (const bf16_t*)kc, (const bf16_t*)vc, H, Hkv, Mq, Nk, cap, kps, scale_log2,
-                       (bf16_t*)out, opart, ws.ml);
+                       out, opart, ws.ml);
   } else {
     const float* qf = (const float*)q;
     const float* kf = (const float*)kc;
     const float* vf = (const float*)vc;
-    float* of = (float*)out;
+    float* of = out;
     if (dh == 32)
       hipLaunchKernelGGL(attn_f32_kernel<32>, grid, dim3(64), 0, st, qf, kf, vf, H, Hkv, Mq, Nk,
                          cap, kps, scale_log2, of, opart, ws.ml);
@@ -253,14 +247,9 @@ hipError_t attention(int dtype, const void* q, const void* kc, const void* vc, i
       hipLaunchKernelGGL(attn_f32_kernel<128>, grid, dim3(64), 0, st, qf, kf, vf, H, Hkv, Mq, Nk,
                          cap, kps, scale_log2, of, opart, ws.ml);
   }
-  if (S > 1) {
-    if (dtype == 1)
-      hipLaunchKernelGGL(attn_merge_kernel<bf16_t>, dim3(BH * Mq), dim3(128), 0, st, ws.opart,
-                         ws.ml, S, BH, H, Mq, dh, (bf16_t*)out);
-    else
-      hipLaunchKernelGGL(attn_merge_kernel<float>, dim3(BH * Mq), dim3(128), 0, st, ws.opart,
-                         ws.ml, S, BH, H, Mq, dh, (float*)out);
-  }
+  if (S > 1)
+    hipLaunchKernelGGL(attn_merge_kernel, dim3(BH * Mq), dim3(128), 0, st, ws.opart, ws.ml, S, BH,
+                       H, Mq, dh, out);
   return hipGetLastError();
 }
 

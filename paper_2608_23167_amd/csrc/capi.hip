@@ -101,6 +101,8 @@ int32_t check_model(const ssm_model* m) {
     if (!y.attn_norm || !y.wq || !y.wk || !y.wv || !y.wo || !y.ffn_norm || !y.w_gate || !y.w_up || !y.w_down)
       return fail(SSM_E_INVAL, "null tensor in layer %d", l);
   }
+  if (m->dtype == SSM_DT_BF16 && m->act_mode != SSM_ACT_BF16 && m->act_mode != SSM_ACT_BF16X2)
+    return fail(SSM_E_INVAL, "unknown act_mode %d", m->act_mode);
   if (m->dtype == SSM_DT_BF16) {
     if (m->head_dim != 128) return fail(SSM_E_UNSUPPORTED, "bf16 path needs head_dim 128 (got %d)", m->head_dim);
     if (m->d_model % 128 || m->ffn_dim % 128 || m->vocab % 128)
@@ -168,7 +170,7 @@ struct ProfScope {
   } while (0)
 
 struct WsLayout {
-  size_t resid, xn, q, attn, act, rope, opart, ml, part, logits, total;
+  size_t resid, inv, q, attn, act, rope, opart, ml, part, logits, lmstats, total;
   size_t part_floats;
 };
 
@@ -185,16 +187,17 @@ WsLayout ws_layout(const ssm_model* m, int batch, int max_rows) {
   size_t off = 0;
   auto take = [&](size_t bytes) { size_t o = off; off += align256(bytes); return o; };
   w.resid = take(Mt * d * 4);
-  w.xn = take(Mt * d * es);
+  w.inv = take(Mt * 4);
   w.q = take(Mt * H * dh * es);
-  w.attn = take(Mt * H * dh * es);
-  w.act = take(Mt * F * es);
+  w.attn = take(Mt * H * dh * 4);
+  w.act = take(Mt * F * 4);
   w.rope = take((size_t)max_rows * (dh / 2) * 8);
   w.opart = take((size_t)ATTN_MAX_SPLITS * Mt * H * dh * 4);
   w.ml = take((size_t)ATTN_MAX_SPLITS * Mt * H * 2 * 4);
   w.part_floats = gemm_split_ws_floats((int)Mt, (int)maxn);
   w.part = take(w.part_floats * 4);
-  w.logits = take(Mt * V * 4);
+  w.logits = m->dtype == SSM_DT_BF16 ? take(0) : take(Mt * V * 4);
+  w.lmstats = take(m->dtype == SSM_DT_BF16 ? lm_stats_ws_bytes((int)Mt, (int)V) : 0);
   w.total = off;
   return w;
 }
@@ -295,17 +298,18 @@ int32_t ssm_denoise_step(const ssm_model* m, const ssm_kv_cache* cache, int32_t 
 
   hipStream_t st = (hipStream_t)stream;
   const int dt = m->dtype;
-  const size_t es = dt == SSM_DT_BF16 ? 2 : 4;
+  const bool split = dt == SSM_DT_BF16 && m->act_mode == SSM_ACT_BF16X2;
   const int d = m->d_model, H = m->n_heads, Hkv = m->n_kv_heads, dh = m->head_dim;
   const int F = m->ffn_dim, V = m->vocab;
   const int Mt = batch * n_rows, n_out = n_rows - first_out_row, Mo = batch * n_out;
   const int Nk = n_cached + n_rows;
+  const size_t es = dt == SSM_DT_BF16 ? 2 : 4;
   char* ws = (char*)d_ws;
   float* resid = (float*)(ws + w.resid);
-  void* xn = ws + w.xn;
+  float* inv = (float*)(ws + w.inv);
   void* qb = ws + w.q;
-  void* attn = ws + w.attn;
-  void* act = ws + w.act;
+  float* attn = (float*)(ws + w.attn);
+  float* act = (float*)(ws + w.act);
   float2* rope = (float2*)(ws + w.rope);
   SplitWs sws{(float*)(ws + w.part), w.part_floats};
   AttnWs aws{(float*)(ws + w.opart), (float*)(ws + w.ml), ATTN_MAX_SPLITS};
@@ -318,24 +322,39 @@ int32_t ssm_denoise_step(const ssm_model* m, const ssm_kv_cache* cache, int32_t 
     const ssm_layer& y = m->layers[l];
     char* kc = (char*)cache->k + l * layer_kv;
     char* vc = (char*)cache->v + l * layer_kv;
-    PROF_TRY("rmsnorm", launch_rmsnorm(dt, resid, d, y.attn_norm, m->rms_eps, xn, Mt, Mt, 0, 0, st));
+    // attention block: RMSNorm fused into the QKV projection (1/rms per row here)
+    PROF_TRY("row_rms", launch_row_rms(resid, d, m->rms_eps, inv, Mt, Mt, 0, 0, st));
     QKVOut qo{qb, kc, vc, cache->capacity, n_cached, n_rows, rope};
-    PROF_TRY("gemm_qkv", gemm_qkv(dt, xn, Mt, d, y.wq, y.wk, y.wv, H, Hkv, dh, qo, sws, st));
-    PROF_TRY("attention", attention(dt, qb, kc, vc, batch, H, Hkv, dh, n_rows, Nk, cache->capacity, attn, aws, st));
-    PROF_TRY("gemm_o", gemm_resid(dt, attn, Mt, H * dh, y.wo, d, resid, sws, st));
-    PROF_TRY("rmsnorm", launch_rmsnorm(dt, resid, d, y.ffn_norm, m->rms_eps, xn, Mt, Mt, 0, 0, st));
-    PROF_TRY("gemm_gate_up", gemm_swiglu(dt, xn, Mt, d, y.w_gate, y.w_up, F, act, sws, st));
-    PROF_TRY("gemm_down", gemm_resid(dt, act, Mt, F, y.w_down, d, resid, sws, st));
+    PROF_TRY("gemm_qkv", gemm_qkv(dt, split, GemmA{resid, d, inv, y.attn_norm, Mt, 0, 0}, Mt, d,
+                                  y.wq, y.wk, y.wv, H, Hkv, dh, qo, sws, st));
+    PROF_TRY("attention", attention(dt, qb, kc, vc, batch, H, Hkv, dh, n_rows, Nk,
+                                    cache->capacity, attn, aws, st));
+    PROF_TRY("gemm_o", gemm_resid(dt, split, "o", plain_a(attn, H * dh, Mt), Mt, H * dh, y.wo, d,
+                                  resid, sws, st));
+    // feed-forward block
+    PROF_TRY("row_rms", launch_row_rms(resid, d, m->rms_eps, inv, Mt, Mt, 0, 0, st));
+    PROF_TRY("gemm_gate_up", gemm_swiglu(dt, split, GemmA{resid, d, inv, y.ffn_norm, Mt, 0, 0}, Mt,
+                                         d, y.w_gate, y.w_up, F, act, sws, st));
+    PROF_TRY("gemm_down", gemm_resid(dt, split, "down", plain_a(act, F, Mt), Mt, F, y.w_down, d,
+                                     resid, sws, st));
   }
   if (d_hidden_dbg)
     HIP_TRY(hipMemcpyAsync(d_hidden_dbg, resid, (size_t)Mt * d * 4, hipMemcpyDeviceToDevice, st));
-  // final norm of the output rows only: output row o <- row first_out_row + o % n_out of
-  // sequence o / n_out
-  PROF_TRY("rmsnorm", launch_rmsnorm(dt, resid, d, m->final_norm, m->rms_eps, xn, Mo, n_out, n_rows,
-                         first_out_row, st));
-  PROF_TRY("gemm_lm_head", gemm_store(dt, xn, Mo, d, m->lm_head, V, logits, V, sws, st));
-  PROF_TRY("rowstats", launch_rowstats(logits, Mo, V, V, m->mask_id, k, d_argmax, d_conf, d_topk_ids,
-                          d_topk_w, st));
+  // final norm and LM head over the output rows only: output row o is row
+  // first_out_row + o % n_out of sequence o / n_out
+  PROF_TRY("row_rms", launch_row_rms(resid, d, m->rms_eps, inv, Mo, n_out, n_rows, first_out_row, st));
+  if (dt == SSM_DT_BF16) {
+    PROF_TRY("gemm_lm_head", lm_head_stats(split, GemmA{resid, d, inv, m->final_norm, n_out, n_rows,
+                                                        first_out_row},
+                                           Mo, d, m->lm_head, V, m->mask_id, k, ws + w.lmstats,
+                                           d_logits_dbg, d_argmax, d_conf, d_topk_ids, d_topk_w, st));
+  } else {
+    PROF_TRY("gemm_lm_head", gemm_store(dt, split, GemmA{resid, d, inv, m->final_norm, n_out, n_rows,
+                                                         first_out_row},
+                                        Mo, d, m->lm_head, V, logits, V, sws, st));
+    PROF_TRY("rowstats", launch_rowstats(logits, Mo, V, V, m->mask_id, k, d_argmax, d_conf,
+                                         d_topk_ids, d_topk_w, st));
+  }
   return ok();
 }
 

@@ -30,11 +30,6 @@ hipError_t launch_embed(int dtype, const void* E, int d, int vocab, int mask_id,
                         const float* pred_w, const int32_t* pred_step, int prev_step, int k,
                         float alpha, float* x, hipStream_t st);
 
-// RMSNorm of float32 rows into the storage type.  Output row o reads input
-// row (o / per) * in_stride + in_off + (o % per).
-hipError_t launch_rmsnorm(int dtype, const float* x, int d, const void* g, float eps, void* y,
-                          int n_out_rows, int per, int in_stride, int in_off, hipStream_t st);
-
 // cos/sin of pos[r] * base^(-2i/dh) computed in float64, stored as float2.
 hipError_t launch_rope_table(const int32_t* pos, int n_rows, int dh, float base, float2* tab,
                              hipStream_t st);
@@ -60,16 +55,39 @@ struct SplitWs {
   size_t floats;
 };
 
-hipError_t gemm_qkv(int dtype, const void* xn, int M, int d, const void* wq, const void* wk,
-                    const void* wv, int H, int Hkv, int dh, const QKVOut& out, SplitWs ws,
-                    hipStream_t st);
-hipError_t gemm_resid(int dtype, const void* a, int M, int K, const void* w, int N, float* resid,
-                      SplitWs ws, hipStream_t st);
-hipError_t gemm_swiglu(int dtype, const void* xn, int M, int d, const void* wg, const void* wu,
-                       int F, void* act, SplitWs ws, hipStream_t st);
-hipError_t gemm_store(int dtype, const void* a, int M, int K, const void* w, int N, float* c,
-                      int ldc, SplitWs ws, hipStream_t st);
+// float32 activation operand of a projection, with the fused RMSNorm scales:
+// A[m, k] = a[row(m) * lda + k] * rscale[m] * cscale[k] (a null scale is 1),
+// row(m) = (m / per) * stride + off + m % per.
+struct GemmA {
+  const float* a;
+  int lda;
+  const float* rscale;
+  const void* cscale;     // model dtype
+  int per, stride, off;
+};
+
+inline GemmA plain_a(const float* a, int lda, int M) { return GemmA{a, lda, nullptr, nullptr, M, 0, 0}; }
+
+hipError_t launch_row_rms(const float* x, int d, float eps, float* inv, int n_rows, int per,
+                          int stride, int off, hipStream_t st);
+hipError_t gemm_qkv(int dtype, bool split, const GemmA& a, int M, int d, const void* wq,
+                    const void* wk, const void* wv, int H, int Hkv, int dh, const QKVOut& out,
+                    SplitWs ws, hipStream_t st);
+hipError_t gemm_resid(int dtype, bool split, const char* kind, const GemmA& a, int M, int K,
+                      const void* w, int N, float* resid, SplitWs ws, hipStream_t st);
+hipError_t gemm_swiglu(int dtype, bool split, const GemmA& a, int M, int d, const void* wg,
+                       const void* wu, int F, float* act, SplitWs ws, hipStream_t st);
+hipError_t gemm_store(int dtype, bool split, const GemmA& a, int M, int K, const void* w, int N,
+                      float* c, int ldc, SplitWs ws, hipStream_t st);
 size_t gemm_split_ws_floats(int M, int max_n);
+
+// bfloat16 LM head with the row statistics fused into the GEMM epilogue
+// (per half tile) and merged by a second kernel; logits stored only if
+// `logits` is not null.  N must be a multiple of 128.
+size_t lm_stats_ws_bytes(int M, int N);
+hipError_t lm_head_stats(bool split, const GemmA& a, int M, int K, const void* w, int N,
+                         int mask_id, int k, void* stats_ws, float* logits, int32_t* argmax,
+                         float* conf, int32_t* topk_ids, float* topk_w, hipStream_t st);
 
 // ---- attention -----------------------------------------------------------
 struct AttnWs {
@@ -77,8 +95,9 @@ struct AttnWs {
   float* ml;         // [S, B*H, Mq, 2]
   int max_splits;
 };
+// out: float32 [B * Mq, H * dh]
 hipError_t attention(int dtype, const void* q, const void* kc, const void* vc, int B, int H,
-                     int Hkv, int dh, int Mq, int Nk, int cap, void* out, AttnWs ws,
+                     int Hkv, int dh, int Mq, int Nk, int cap, float* out, AttnWs ws,
                      hipStream_t st);
 
 // ---- unmasking ------------------------------------------------------------

@@ -1,45 +1,7 @@
-// RMSNorm, RoPE angle table and the per-row output statistics of the LM head.
+// RoPE angle table and the per-row output statistics of the LM head.
 #include "internal.h"
 
 namespace ssm {
-
-// ---- RMSNorm: y = x / sqrt(mean(x^2) + eps) * g -------------------------
-template <typename T>
-__global__ void __launch_bounds__(256) rmsnorm_kernel(const float* __restrict__ x, int d,
-                                                      const T* __restrict__ g, float eps,
-                                                      T* __restrict__ y, int per, int in_stride,
-                                                      int in_off) {
-  __shared__ float red[16];
-  const int o = blockIdx.x;
-  const size_t in_row = (size_t)(o / per) * in_stride + in_off + (o % per);
-  const float* xr = x + in_row * d;
-  T* yr = y + (size_t)o * d;
-  float ss = 0.f;
-  if ((d & 3) == 0) {
-    const float4* x4 = (const float4*)xr;
-    for (int c = threadIdx.x; c < d / 4; c += blockDim.x) {
-      float4 v = x4[c];
-      ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
-    }
-  } else {
-    for (int c = threadIdx.x; c < d; c += blockDim.x) ss += xr[c] * xr[c];
-  }
-  ss = block_sum(ss, red);
-  const float inv = 1.0f / sqrtf(ss / (float)d + eps);
-  for (int c = threadIdx.x; c < d; c += blockDim.x) stf(yr + c, xr[c] * inv * ldf(g + c));
-}
-
-hipError_t launch_rmsnorm(int dtype, const float* x, int d, const void* g, float eps, void* y,
-                          int n_out_rows, int per, int in_stride, int in_off, hipStream_t st) {
-  if (n_out_rows == 0) return hipSuccess;
-  if (dtype == 0)
-    hipLaunchKernelGGL(rmsnorm_kernel<float>, dim3(n_out_rows), dim3(256), 0, st, x, d,
-                       (const float*)g, eps, (float*)y, per, in_stride, in_off);
-  else
-    hipLaunchKernelGGL(rmsnorm_kernel<bf16_t>, dim3(n_out_rows), dim3(256), 0, st, x, d,
-                       (const bf16_t*)g, eps, (bf16_t*)y, per, in_stride, in_off);
-  return hipGetLastError();
-}
 
 // ---- RoPE table (rotate-half form), float64 arithmetic -------------------
 __global__ void rope_table_kernel(const int32_t* __restrict__ pos, int n_rows, int half, int dh,

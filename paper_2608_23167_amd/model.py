@@ -16,7 +16,7 @@ class DeviceModel:
     contiguous device tensor of the model dtype; `shape` gives the sizes.
     """
 
-    def __init__(self, shape, weights):
+    def __init__(self, shape, weights, act_mode: int = L.SSM_ACT_BF16X2):
         self.shape = shape
         self.weights = weights
         dt = torch.float32 if shape.dtype == "f32" else torch.bfloat16
@@ -35,7 +35,7 @@ class DeviceModel:
             shape.vocab, shape.mask_id, L.SSM_DT_F32 if shape.dtype == "f32" else L.SSM_DT_BF16,
             float(shape.rope_base), float(shape.rms_eps), weights.tok_emb.data_ptr(),
             weights.final_norm.data_ptr(), weights.lm_head.data_ptr(),
-            C.cast(self._layers, C.POINTER(L.Layer)))
+            C.cast(self._layers, C.POINTER(L.Layer)), int(act_mode))
 
     @property
     def dtype(self):

@@ -223,8 +223,8 @@ int32_t ssm_workspace_size(const ssm_model* m, int32_t batch, int32_t max_rows, 
  * and values go to slots [n_cached, n_cached + n_rows), so capacity >=
  * n_cached + n_rows.  Attention of every row reads all n_cached + n_rows keys.
  * d_ws: workspace of ws_bytes >= ssm_workspace_size(batch, n_rows).
- * k in [1, 8].  The bfloat16 path needs d_model, head_dim*n_heads, ffn_dim and
- * vocab to be multiples of 128 and head_dim == 128; otherwise SSM_E_UNSUPPORTED.
+ * k in [1, 8].  The bfloat16 path needs d_model and ffn_dim to be multiples of
+ * 256, vocab a multiple of 128 and head_dim == 128; otherwise SSM_E_UNSUPPORTED.
  */
 int32_t ssm_denoise_step(const ssm_model* m, const ssm_kv_cache* cache, int32_t cache_mode,
                          int32_t n_cached, int32_t batch, const int32_t* d_pos, int32_t n_rows,
@@ -268,7 +268,7 @@ int32_t ssm_unmask(int32_t* d_tokens, int32_t batch, int32_t seq_len, int32_t bl
 /*
  * on != 0: from now on every kernel launcher of the calls above is bracketed
  * by a pair of HIP events recorded on the call's stream, under a tag naming
- * the operation ("select", "embed", "rope_table", "row_rms", "gemm_qkv",
+ * the operation ("select", "embed", "rope_table", "norm", "gemm_qkv",
  * "attention", "gemm_o", "gemm_gate_up", "gemm_down", "gemm_lm_head",
  * "rowstats", "unmask").  Each call discards earlier records.  Not
  * thread-safe; meant for a single profiling thread.

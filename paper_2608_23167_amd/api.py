@@ -123,7 +123,7 @@ def ssm_unmask(tokens: torch.Tensor, block_start: int, block_size: int, mask_id:
     check(rc, "ssm_unmask")
 
 
-PROFILE_TAGS = ("select", "embed", "rope_table", "row_rms", "gemm_qkv", "attention", "gemm_o",
+PROFILE_TAGS = ("select", "embed", "rope_table", "norm", "gemm_qkv", "attention", "gemm_o",
                 "gemm_gate_up", "gemm_down", "gemm_lm_head", "rowstats", "unmask")
 
 

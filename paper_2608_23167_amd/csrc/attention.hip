@@ -19,7 +19,7 @@ constexpr float LOG2E = 1.4426950408889634f;
 __global__ void __launch_bounds__(256) attn_bf16_kernel(
     const bf16_t* __restrict__ Q, const bf16_t* __restrict__ Kc, const bf16_t* __restrict__ Vc,
     int H, int Hkv, int Mq, int Nk, int cap, int keys_per_split, float scale_log2,
-    float* __restrict__ O, float* __restrict__ Opart, float* __restrict__ ML) {
+    ActOut O, float* __restrict__ Opart, float* __restrict__ ML) {
   constexpr int DH = 128, KT = 64, KS = DH + 8, VS = KT + 8;
   __shared__ __attribute__((aligned(16))) bf16_t Ks[KT * KS];
   __shared__ __attribute__((aligned(16))) bf16_t Vt[DH * VS];
@@ -129,9 +129,19 @@ __global__ void __launch_bounds__(256) attn_bf16_kernel(
   // o[db][r] = O^T[dh 16db + 4g + r][query c16]
   if (Opart == nullptr) {
     const float inv = 1.0f / l_run;
-    float* out = O + ((size_t)s * Mq + q) * (size_t)(H * DH) + h * DH;
+    const size_t base = ((size_t)s * Mq + q) * (size_t)(H * DH) + h * DH;
 #pragma unroll
-    for (int db = 0; db < 8; ++db) *(f32x4_t*)(out + 16 * db + 4 * g) = o[db] * inv;
+    for (int db = 0; db < 8; ++db) {
+      uint16_t hi[4], lo[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float v = o[db][r] * inv;
+        hi[r] = f2bf(v);
+        lo[r] = f2bf(v - bf2f(hi[r]));
+      }
+      *(uint2*)((bf16_t*)O.hi + base + 16 * db + 4 * g) = *(const uint2*)hi;
+      if (O.lo) *(uint2*)(O.lo + base + 16 * db + 4 * g) = *(const uint2*)lo;
+    }
   } else {
     const size_t row = ((size_t)split * gridDim.y + bh) * Mq + q;
     float* op = Opart + row * DH;
@@ -146,7 +156,7 @@ template <int DH>
 __global__ void __launch_bounds__(64) attn_f32_kernel(
     const float* __restrict__ Q, const float* __restrict__ Kc, const float* __restrict__ Vc,
     int H, int Hkv, int Mq, int Nk, int cap, int keys_per_split, float scale_log2,
-    float* __restrict__ O, float* __restrict__ Opart, float* __restrict__ ML) {
+    ActOut O, float* __restrict__ Opart, float* __restrict__ ML) {
   const int bh = blockIdx.y, s = bh / H, h = bh % H, kvh = h / (H / Hkv);
   const int split = blockIdx.z;
   const int kb = split * keys_per_split, ke = min(Nk, kb + keys_per_split);
@@ -174,7 +184,7 @@ __global__ void __launch_bounds__(64) attn_f32_kernel(
     m_run = m_new;
   }
   if (Opart == nullptr) {
-    float* out = O + ((size_t)s * Mq + q) * (size_t)(H * DH) + h * DH;
+    float* out = (float*)O.hi + ((size_t)s * Mq + q) * (size_t)(H * DH) + h * DH;
     const float inv = 1.0f / l_run;
 #pragma unroll
     for (int c = 0; c < DH; ++c) out[c] = ov[c] * inv;
@@ -188,8 +198,9 @@ __global__ void __launch_bounds__(64) attn_f32_kernel(
 }
 
 // Combines the splits of one (sequence, head, query) row, in split order.
+template <typename T>
 __global__ void attn_merge_kernel(const float* __restrict__ Opart, const float* __restrict__ ML,
-                                  int S, int BH, int H, int Mq, int DH, float* __restrict__ O) {
+                                  int S, int BH, int H, int Mq, int DH, ActOut O) {
   const int row = blockIdx.x;               // over BH * Mq
   const int bh = row / Mq, q = row % Mq, s = bh / H, h = bh % H;
   float M = -INFINITY;
@@ -201,19 +212,19 @@ __global__ void attn_merge_kernel(const float* __restrict__ Opart, const float* 
     if (l > 0.f) L += l * exp2f(ML[r * 2] - M);
   }
   const float inv = 1.0f / L;
-  float* out = O + ((size_t)s * Mq + q) * (size_t)(H * DH) + h * DH;
+  const size_t base = ((size_t)s * Mq + q) * (size_t)(H * DH) + h * DH;
   for (int c = threadIdx.x; c < DH; c += blockDim.x) {
     float acc = 0.f;
     for (int i = 0; i < S; ++i) {
       const size_t r = (size_t)i * BH * Mq + row;
       if (ML[r * 2 + 1] > 0.f) acc += Opart[r * DH + c] * exp2f(ML[r * 2] - M);
     }
-    out[c] = acc * inv;
+    O.store<T>(base + c, acc * inv);
   }
 }
 
 hipError_t attention(int dtype, const void* q, const void* kc, const void* vc, int B, int H,
-                     int Hkv, int dh, int Mq, int Nk, int cap, float* out, AttnWs ws,
+                     int Hkv, int dh, int Mq, int Nk, int cap, const ActOut& out, AttnWs ws,
                      hipStream_t st) {
   if (Mq == 0) return hipSuccess;
   const int BH = B * H;
@@ -236,7 +247,7 @@ hipError_t attention(int dtype, const void* q, const void* kc, const void* vc, i
     const float* qf = (const float*)q;
     const float* kf = (const float*)kc;
     const float* vf = (const float*)vc;
-    float* of = out;
+    const ActOut& of = out;
     if (dh == 32)
       hipLaunchKernelGGL(attn_f32_kernel<32>, grid, dim3(64), 0, st, qf, kf, vf, H, Hkv, Mq, Nk,
                          cap, kps, scale_log2, of, opart, ws.ml);
@@ -247,9 +258,14 @@ hipError_t attention(int dtype, const void* q, const void* kc, const void* vc, i
       hipLaunchKernelGGL(attn_f32_kernel<128>, grid, dim3(64), 0, st, qf, kf, vf, H, Hkv, Mq, Nk,
                          cap, kps, scale_log2, of, opart, ws.ml);
   }
-  if (S > 1)
-    hipLaunchKernelGGL(attn_merge_kernel, dim3(BH * Mq), dim3(128), 0, st, ws.opart, ws.ml, S, BH,
-                       H, Mq, dh, out);
+  if (S > 1) {
+    if (dtype == 1)
+      hipLaunchKernelGGL(attn_merge_kernel<bf16_t>, dim3(BH * Mq), dim3(128), 0, st, ws.opart,
+                         ws.ml, S, BH, H, Mq, dh, out);
+    else
+      hipLaunchKernelGGL(attn_merge_kernel<float>, dim3(BH * Mq), dim3(128), 0, st, ws.opart,
+                         ws.ml, S, BH, H, Mq, dh, out);
+  }
   return hipGetLastError();
 }
 

@@ -105,8 +105,8 @@ int32_t check_model(const ssm_model* m) {
     return fail(SSM_E_INVAL, "unknown act_mode %d", m->act_mode);
   if (m->dtype == SSM_DT_BF16) {
     if (m->head_dim != 128) return fail(SSM_E_UNSUPPORTED, "bf16 path needs head_dim 128 (got %d)", m->head_dim);
-    if (m->d_model % 128 || m->ffn_dim % 128 || m->vocab % 128)
-      return fail(SSM_E_UNSUPPORTED, "bf16 path needs d_model, ffn_dim, vocab multiples of 128");
+    if (m->d_model % 256 || m->ffn_dim % 256 || m->vocab % 128)
+      return fail(SSM_E_UNSUPPORTED, "bf16 path needs d_model and ffn_dim multiples of 256, vocab of 128");
   } else {
     if (m->head_dim != 32 && m->head_dim != 64 && m->head_dim != 128)
       return fail(SSM_E_UNSUPPORTED, "fp32 path needs head_dim 32, 64 or 128");
@@ -170,7 +170,7 @@ struct ProfScope {
   } while (0)
 
 struct WsLayout {
-  size_t resid, inv, q, attn, act, rope, opart, ml, part, logits, lmstats, total;
+  size_t resid, xn, xn_lo, q, attn, attn_lo, act, act_lo, rope, opart, ml, part, logits, lmstats, total;
   size_t part_floats;
 };
 
@@ -186,11 +186,16 @@ WsLayout ws_layout(const ssm_model* m, int batch, int max_rows) {
   WsLayout w{};
   size_t off = 0;
   auto take = [&](size_t bytes) { size_t o = off; off += align256(bytes); return o; };
+  // projection operands: float32 for float32 models, bfloat16 hi (+ lo) otherwise
+  const size_t lo_es = (m->dtype == SSM_DT_BF16 && m->act_mode == SSM_ACT_BF16X2) ? 2 : 0;
   w.resid = take(Mt * d * 4);
-  w.inv = take(Mt * 4);
+  w.xn = take(Mt * d * es);
+  w.xn_lo = take(Mt * d * lo_es);
   w.q = take(Mt * H * dh * es);
-  w.attn = take(Mt * H * dh * 4);
-  w.act = take(Mt * F * 4);
+  w.attn = take(Mt * H * dh * es);
+  w.attn_lo = take(Mt * H * dh * lo_es);
+  w.act = take(Mt * F * es);
+  w.act_lo = take(Mt * F * lo_es);
   w.rope = take((size_t)max_rows * (dh / 2) * 8);
   w.opart = take((size_t)ATTN_MAX_SPLITS * Mt * H * dh * 4);
   w.ml = take((size_t)ATTN_MAX_SPLITS * Mt * H * 2 * 4);
@@ -306,10 +311,13 @@ int32_t ssm_denoise_step(const ssm_model* m, const ssm_kv_cache* cache, int32_t 
   const size_t es = dt == SSM_DT_BF16 ? 2 : 4;
   char* ws = (char*)d_ws;
   float* resid = (float*)(ws + w.resid);
-  float* inv = (float*)(ws + w.inv);
+  bf16_t* xn_lo = split ? (bf16_t*)(ws + w.xn_lo) : nullptr;
+  bf16_t* attn_lo = split ? (bf16_t*)(ws + w.attn_lo) : nullptr;
+  bf16_t* act_lo = split ? (bf16_t*)(ws + w.act_lo) : nullptr;
+  const ActOut xn_out{ws + w.xn, xn_lo}, attn_out{ws + w.attn, attn_lo}, act_out{ws + w.act, act_lo};
+  const ActIn xn_in{ws + w.xn, xn_lo, d}, attn_in{ws + w.attn, attn_lo, H * dh},
+      act_in{ws + w.act, act_lo, F};
   void* qb = ws + w.q;
-  float* attn = (float*)(ws + w.attn);
-  float* act = (float*)(ws + w.act);
   float2* rope = (float2*)(ws + w.rope);
   SplitWs sws{(float*)(ws + w.part), w.part_floats};
   AttnWs aws{(float*)(ws + w.opart), (float*)(ws + w.ml), ATTN_MAX_SPLITS};
@@ -322,36 +330,30 @@ int32_t ssm_denoise_step(const ssm_model* m, const ssm_kv_cache* cache, int32_t 
     const ssm_layer& y = m->layers[l];
     char* kc = (char*)cache->k + l * layer_kv;
     char* vc = (char*)cache->v + l * layer_kv;
-    // attention block: RMSNorm fused into the QKV projection (1/rms per row here)
-    PROF_TRY("row_rms", launch_row_rms(resid, d, m->rms_eps, inv, Mt, Mt, 0, 0, st));
+    // attention block
+    PROF_TRY("norm", launch_norm(dt, resid, d, y.attn_norm, m->rms_eps, xn_out, Mt, Mt, 0, 0, st));
     QKVOut qo{qb, kc, vc, cache->capacity, n_cached, n_rows, rope};
-    PROF_TRY("gemm_qkv", gemm_qkv(dt, split, GemmA{resid, d, inv, y.attn_norm, Mt, 0, 0}, Mt, d,
-                                  y.wq, y.wk, y.wv, H, Hkv, dh, qo, sws, st));
+    PROF_TRY("gemm_qkv", gemm_qkv(dt, xn_in, Mt, d, y.wq, y.wk, y.wv, H, Hkv, dh, qo, sws, st));
     PROF_TRY("attention", attention(dt, qb, kc, vc, batch, H, Hkv, dh, n_rows, Nk,
-                                    cache->capacity, attn, aws, st));
-    PROF_TRY("gemm_o", gemm_resid(dt, split, "o", plain_a(attn, H * dh, Mt), Mt, H * dh, y.wo, d,
-                                  resid, sws, st));
+                                    cache->capacity, attn_out, aws, st));
+    PROF_TRY("gemm_o", gemm_resid(dt, "o", attn_in, Mt, H * dh, y.wo, d, resid, sws, st));
     // feed-forward block
-    PROF_TRY("row_rms", launch_row_rms(resid, d, m->rms_eps, inv, Mt, Mt, 0, 0, st));
-    PROF_TRY("gemm_gate_up", gemm_swiglu(dt, split, GemmA{resid, d, inv, y.ffn_norm, Mt, 0, 0}, Mt,
-                                         d, y.w_gate, y.w_up, F, act, sws, st));
-    PROF_TRY("gemm_down", gemm_resid(dt, split, "down", plain_a(act, F, Mt), Mt, F, y.w_down, d,
-                                     resid, sws, st));
+    PROF_TRY("norm", launch_norm(dt, resid, d, y.ffn_norm, m->rms_eps, xn_out, Mt, Mt, 0, 0, st));
+    PROF_TRY("gemm_gate_up", gemm_swiglu(dt, xn_in, Mt, d, y.w_gate, y.w_up, F, act_out, sws, st));
+    PROF_TRY("gemm_down", gemm_resid(dt, "down", act_in, Mt, F, y.w_down, d, resid, sws, st));
   }
   if (d_hidden_dbg)
     HIP_TRY(hipMemcpyAsync(d_hidden_dbg, resid, (size_t)Mt * d * 4, hipMemcpyDeviceToDevice, st));
   // final norm and LM head over the output rows only: output row o is row
   // first_out_row + o % n_out of sequence o / n_out
-  PROF_TRY("row_rms", launch_row_rms(resid, d, m->rms_eps, inv, Mo, n_out, n_rows, first_out_row, st));
+  PROF_TRY("norm", launch_norm(dt, resid, d, m->final_norm, m->rms_eps, xn_out, Mo, n_out, n_rows,
+                               first_out_row, st));
   if (dt == SSM_DT_BF16) {
-    PROF_TRY("gemm_lm_head", lm_head_stats(split, GemmA{resid, d, inv, m->final_norm, n_out, n_rows,
-                                                        first_out_row},
-                                           Mo, d, m->lm_head, V, m->mask_id, k, ws + w.lmstats,
-                                           d_logits_dbg, d_argmax, d_conf, d_topk_ids, d_topk_w, st));
+    PROF_TRY("gemm_lm_head", lm_head_stats(xn_in, Mo, d, m->lm_head, V, m->mask_id, k,
+                                           ws + w.lmstats, d_logits_dbg, d_argmax, d_conf,
+                                           d_topk_ids, d_topk_w, st));
   } else {
-    PROF_TRY("gemm_lm_head", gemm_store(dt, split, GemmA{resid, d, inv, m->final_norm, n_out, n_rows,
-                                                         first_out_row},
-                                        Mo, d, m->lm_head, V, logits, V, sws, st));
+    PROF_TRY("gemm_lm_head", gemm_store_f32(xn_in, Mo, d, m->lm_head, V, logits, V, sws, st));
     PROF_TRY("rowstats", launch_rowstats(logits, Mo, V, V, m->mask_id, k, d_argmax, d_conf,
                                          d_topk_ids, d_topk_w, st));
   }

@@ -1,32 +1,34 @@
-// Projections of the decoder layer: C = A * W^T with A [M, K] float32
-// activations and W [N, K] row-major weights (nn.Linear layout).
+// Projections of the decoder layer: C = A * W^T with A [M, K] activations
+// and W [N, K] row-major weights (nn.Linear layout).
 //
-// A is read as float32 and optionally scaled on the way in: a per-row scale
-// (the RMSNorm factor 1/rms of that row) and a per-column scale (the norm
-// weight), so the normalisation of the decoder block is fused into the
-// projection that consumes it.  Logical row m of A is physical row
-// (m / per) * stride + off + m % per, which lets the LM head read only the
-// output rows of every sequence.
-//
-// bfloat16 path: MFMA v_mfma_f32_16x16x32_bf16, 256 threads (4 waves) per
-// workgroup, BK = 64, fp32 accumulation.  Weights stream through a ring of
-// register stages PW K-steps ahead (HBM latency), activations PA K-steps
-// ahead (L2 latency); both are staged through a double-buffered LDS tile
-// with padded rows.  With SPLIT the scaled activation is stored as two
-// bfloat16 parts hi = bf16(v), lo = bf16(v - hi) and each product is taken
-// twice (hi*W + lo*W): the weights are exact in bfloat16, so the result
-// then carries about 16 significant bits of the activation instead of 8.
-// The output tile is staged through LDS so that the epilogue can combine any
-// two columns of the tile and store coalesced.
+// bfloat16 path.  The activation operand arrives as bfloat16 (hi) or as a
+// bfloat16 pair (hi, lo) with hi + lo = the float32 value to about 16
+// significant bits; with the pair each product is taken twice (hi*W + lo*W),
+// the weights being exact in bfloat16.  MFMA v_mfma_f32_16x16x32_bf16, fp32
+// accumulation.  A workgroup of 512 threads computes a 128 x BN output tile
+// with two kinds of waves (one of each per SIMD):
+//   * staging waves (4-7) stream the weight tile from HBM: a ring of four
+//     K-steps of 16-byte loads in flight per thread, written into a ring of
+//     three LDS buffers two K-steps ahead of their use;
+//   * compute waves (0-3) each own 32 rows x BN columns: they load their
+//     activation fragments straight from global memory (small, shared by
+//     every workgroup, L2-resident) two K-steps ahead, read the weight
+//     fragments from LDS and issue the MFMAs.
+// Splitting the roles keeps the in-order retirement of vector loads from
+// coupling the long HBM latency of the weights to the MFMA issue.  One
+// barrier per K-step (64) hands the LDS buffers over.  The output tile is
+// staged through LDS so that the epilogue can combine any two columns of the
+// tile and store coalesced.
 //
 // Every output tile of BN columns reads its first BN/2 weight rows from one
 // base pointer and its last BN/2 from another.  That is how the fused
 // epilogues get the pairs they need without any weight repacking:
 //   QKV    : columns (c, c + dh/2) of one head -> rotate-half RoPE, then the
 //            query buffer or the KV cache slot of the row;
-//   SwiGLU : gate row j and up row j -> silu(g) * u;
+//   SwiGLU : gate row j and up row j -> silu(g) * u, written as the next
+//            projection's activation (pair);
 //   resid  : plain rows -> residual stream += value;
-//   store  : plain rows -> float32 output (LM head logits).
+//   LM head: per-row softmax statistics of each half tile (merged later).
 // Split-K writes float32 partial tiles that a second kernel sums in a fixed
 // order before applying the same epilogue.
 #include <stdio.h>
@@ -86,14 +88,14 @@ struct PolSwiGLU {
   static constexpr bool PAIRED = true;
   const T *wg, *wu;
   int ldb, F;
-  float* act;
+  ActOut act;
   __device__ __forceinline__ void b_ptrs(int t, int BN, const T*& lo, const T*& hi) const {
     lo = wg + (size_t)t * (BN / 2) * ldb;
     hi = wu + (size_t)t * (BN / 2) * ldb;
   }
   __device__ __forceinline__ void store(int m, int t, int c, int BN, float g, float u) const {
     const float silu = g / (1.0f + expf(-g));
-    act[(size_t)m * F + t * (BN / 2) + c] = silu * u;
+    act.store<T>((size_t)m * F + t * (BN / 2) + c, silu * u);
   }
 };
 
@@ -249,209 +251,174 @@ __device__ __forceinline__ void tile_of(int w, int total, int mt, int& tn, int& 
   tm = t % mt;
 }
 
-template <int BM, int BN, int WM, int WN, int PA, int PW, bool SPLIT, class Pol>
-__global__ void __launch_bounds__(256) gemm_bf16_kernel(Pol pol, GemmA ga, int M, int k_per_split,
-                                                        int mt, float* __restrict__ part,
-                                                        int ldp) {
+// Warp-specialised workgroup of 8 waves, BM = 128 rows x BN columns.
+//  * Waves 4-7 ("staging") stream the weight tile of each K-step (BN rows x 64
+//    k, the HBM-bound stream) through a ring of 4 register stages into a ring
+//    of 3 LDS buffers, two K-steps ahead.  A staging thread holds only BN / 32
+//    x 16 bytes per stage, so the ring is deep at little register cost.
+//  * Waves 0-3 ("compute") each own 32 rows x all BN columns.  They load
+//    their activation fragments (bfloat16 hi and optionally lo, L2-resident)
+//    straight from global memory into registers in the MFMA operand layout,
+//    two K-steps ahead, read the weight fragments from LDS one half-step
+//    ahead of use, and run the MFMAs (v_mfma_f32_16x16x32_bf16) ordered so
+//    that updates of one accumulator are FM * FN instructions apart.
+// Loads retire in issue order per wave; keeping the two streams in different
+// waves lets each wait only for its own data.  LDS carries only the weight
+// tile (written once, read once by each compute wave).  Every K-step ends with
+// one workgroup barrier on both paths.
+template <int BM, int BN, int PW, bool SPLIT, class Pol>
+__global__ void __launch_bounds__(512) gemm_bf16_kernel(Pol pol, const bf16_t* __restrict__ Ahi,
+                                                        const bf16_t* __restrict__ Alo, int lda,
+                                                        int M, int k_per_split, int mt,
+                                                        float* __restrict__ part, int ldp) {
+  static_assert(BM == 128, "4 compute waves of 32 rows");
   constexpr int BK = 64, LS = BK + 8;            // LDS row stride (elements), 144 B
-  constexpr int NWN = BN / WN;
-  static_assert((BM / WM) * NWN == 4, "4 waves");
-  constexpr int FM = WM / 16, FN = WN / 16;
-  constexpr int AR = BM / 32, BCH = BN / 32;     // rows per thread of the A and W tiles
-  static_assert(BCH >= 2 && (BCH % 2) == 0, "BN must be a multiple of 64");
-  static_assert(PA == 1 || PA == 2, "activation prefetch 1 or 2");
-  static_assert(PW == 2 || PW == 4, "weight prefetch 2 or 4");
+  constexpr int FM = 2, FN = BN / 16;            // per compute wave: 32 rows x BN columns
   constexpr int NA = SPLIT ? 2 : 1;
-  constexpr int SMEM_AB = 2 * (NA * BM + BN) * LS * 2;
+  constexpr int WR = BN / 32;                    // weight rows per staging thread per stage
+  constexpr int NBUF = 3;                        // LDS weight buffers
+  (void)PW;
+  constexpr int BUF_ELEMS = BN * LS;
+  constexpr int SMEM_W = NBUF * BUF_ELEMS * 2;
   constexpr int CS = BN + 4;
   constexpr int SMEM_C = BM * CS * 4;
-  constexpr int SMEM = SMEM_AB > SMEM_C ? SMEM_AB : SMEM_C;
+  constexpr int SMEM = SMEM_W > SMEM_C ? SMEM_W : SMEM_C;
   __shared__ __attribute__((aligned(16))) char smem[SMEM];
-  bf16_t* Ah = (bf16_t*)smem;                    // [2][BM][LS]
-  bf16_t* Al = Ah + 2 * BM * LS;                 // [2][BM][LS] (SPLIT only)
-  bf16_t* Bs = Ah + 2 * NA * BM * LS;            // [2][BN][LS]
+  bf16_t* Ws = (bf16_t*)smem;                    // [NBUF][BN][LS]
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / NWN, wn = wave % NWN;
   int t, mtile;
   tile_of(blockIdx.x, gridDim.x, mt, t, mtile);
   const int m0 = mtile * BM, split = blockIdx.y;
   const int kbeg = split * k_per_split;
-  const int nk = k_per_split / BK;
+  const int nk = k_per_split / BK;               // a multiple of 4 (host-checked)
+  const int last = nk - 1;
+  float* Cs = (float*)smem;
 
-  const bf16_t *blo, *bhi;
-  pol.b_ptrs(t, BN, blo, bhi);
-
-  // thread -> (row r0 + 32 i, 8 columns at col) of every tile
-  const int r0 = tid >> 3, col = (tid & 7) * 8;
-  const float* a_row[AR];
-  float a_scale[AR];
+  if (wave < 4) {
+    // ------------------------------ compute waves ------------------------------
+    // activation fragment i, half kk of a K-step: row 32 wave + 16 i + lane % 16,
+    // 8 consecutive k at 32 kk + 8 (lane / 16); rows past M are computed and discarded
+    size_t a_off[FM];
 #pragma unroll
-  for (int i = 0; i < AR; ++i) {
-    const int m = min(m0 + r0 + 32 * i, M - 1);   // rows past M are computed and discarded
-    const int pm = (m / ga.per) * ga.stride + ga.off + m % ga.per;
-    a_row[i] = ga.a + (size_t)pm * ga.lda + kbeg + col;
-    a_scale[i] = ga.rscale ? ga.rscale[m] : 1.0f;
-  }
-  const bf16_t* cs_ptr = ga.cscale ? (const bf16_t*)ga.cscale + kbeg + col : nullptr;
-  const bf16_t* blo_k = blo + (size_t)r0 * pol.ldb + kbeg + col;
-  const bf16_t* bhi_k = bhi + (size_t)r0 * pol.ldb + kbeg + col;
-  const size_t bstride = (size_t)32 * pol.ldb;
-  const int dst0 = r0 * LS + col;
-
-  f32x4_t acc[FM][FN];
+    for (int i = 0; i < FM; ++i)
+      a_off[i] = (size_t)min(m0 + 32 * wave + 16 * i + (lane & 15), M - 1) * lda + kbeg + (lane >> 4) * 8;
+    // weight fragment j, half kk: LDS row 16 j + lane % 16, column 32 kk + 8 (lane / 16)
+    const int wfrag = (lane & 15) * LS + (lane >> 4) * 8;
+    f32x4_t acc[FM][FN];
 #pragma unroll
-  for (int i = 0; i < FM; ++i)
+    for (int i = 0; i < FM; ++i)
 #pragma unroll
-    for (int j = 0; j < FN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      for (int j = 0; j < FN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    u32x4_t a0[NA][FM][2], a1[NA][FM][2];        // activation stages kt (even / odd)
+    bf16x8_t wf0[FN], wf1[FN];                   // weight fragments: two halves of a K-step
 
-  // A stages: 2 x 16 bytes of float32 per row plus the 8 column scales
-  u32x4_t ra0[AR][2], ra1[AR][2], rc0, rc1;
-  // W stages: ring of PW register sets
-  u32x4_t rw0[BCH], rw1[BCH], rw2[BCH], rw3[BCH];
-
-#define LOAD_A(RA, RC, KT)                                                            \
+#define LOAD_A(RA, KT)                                                                \
   do {                                                                                \
-    _Pragma("unroll") for (int i = 0; i < AR; ++i) {                                  \
-      RA[i][0] = *(const u32x4_t*)(a_row[i] + (KT) * BK);                            \
-      RA[i][1] = *(const u32x4_t*)(a_row[i] + (KT) * BK + 4);                        \
-    }                                                                                 \
-    if (cs_ptr) RC = *(const u32x4_t*)(cs_ptr + (KT) * BK);                           \
-  } while (0)
-#define LOAD_W(RW, KT)                                                                \
-  do {                                                                                \
-    _Pragma("unroll") for (int i = 0; i < BCH / 2; ++i) {                             \
-      RW[i] = *(const u32x4_t*)(blo_k + i * bstride + (KT) * BK);                    \
-      RW[i + BCH / 2] = *(const u32x4_t*)(bhi_k + i * bstride + (KT) * BK);          \
-    }                                                                                 \
-  } while (0)
-#define STORE_A(RA, RC, BUF)                                                          \
-  do {                                                                                \
-    float cs_[8];                                                                     \
-    {                                                                                 \
-      const bf16x8_t cv_ = __builtin_bit_cast(bf16x8_t, RC);                         \
-      _Pragma("unroll") for (int e = 0; e < 8; ++e) cs_[e] = cs_ptr ? (float)cv_[e] : 1.0f; \
-    }                                                                                 \
-    _Pragma("unroll") for (int i = 0; i < AR; ++i) {                                  \
-      const f32x4_t v0_ = __builtin_bit_cast(f32x4_t, RA[i][0]);                     \
-      const f32x4_t v1_ = __builtin_bit_cast(f32x4_t, RA[i][1]);                     \
-      bf16x8_t hi_, lo_;                                                              \
-      _Pragma("unroll") for (int e = 0; e < 8; ++e) {                                 \
-        const float v_ = (e < 4 ? v0_[e & 3] : v1_[e & 3]) * a_scale[i] * cs_[e];    \
-        hi_[e] = (__bf16)v_;                                                          \
-        if (SPLIT) lo_[e] = (__bf16)(v_ - (float)hi_[e]);                             \
-      }                                                                               \
-      *(bf16x8_t*)(Ah + (BUF) * BM * LS + dst0 + i * 32 * LS) = hi_;                  \
-      if (SPLIT) *(bf16x8_t*)(Al + (BUF) * BM * LS + dst0 + i * 32 * LS) = lo_;       \
-    }                                                                                 \
-  } while (0)
-#define STORE_W(RW, BUF)                                                              \
-  do {                                                                                \
-    _Pragma("unroll") for (int i = 0; i < BCH; ++i)                                   \
-        *(u32x4_t*)(Bs + (BUF) * BN * LS + dst0 + i * 32 * LS) = RW[i];               \
-  } while (0)
-#define COMPUTE(BUF)                                                                  \
-  do {                                                                                \
-    const int ao_ = (BUF) * BM * LS + (wm * WM + (lane & 15)) * LS + (lane >> 4) * 8; \
-    const bf16_t* bs_ = Bs + (BUF) * BN * LS + (wn * WN + (lane & 15)) * LS + (lane >> 4) * 8; \
+    _Pragma("unroll") for (int i = 0; i < FM; ++i)                                    \
     _Pragma("unroll") for (int kk = 0; kk < 2; ++kk) {                                \
-      bf16x8_t bfr[FN];                                                               \
-      _Pragma("unroll") for (int j = 0; j < FN; ++j)                                  \
-          bfr[j] = *(const bf16x8_t*)(bs_ + j * 16 * LS + kk * 32);                   \
-      _Pragma("unroll") for (int i = 0; i < FM; ++i) {                                \
-        const bf16x8_t ah_ = *(const bf16x8_t*)(Ah + ao_ + i * 16 * LS + kk * 32);    \
-        _Pragma("unroll") for (int j = 0; j < FN; ++j)                                \
-            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah_, bfr[j], acc[i][j], 0, 0, 0); \
-        if (SPLIT) {                                                                  \
-          const bf16x8_t al_ = *(const bf16x8_t*)(Al + ao_ + i * 16 * LS + kk * 32);  \
-          _Pragma("unroll") for (int j = 0; j < FN; ++j)                              \
-              acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al_, bfr[j], acc[i][j], 0, 0, 0); \
-        }                                                                             \
-      }                                                                               \
+      RA[0][i][kk] = *(const u32x4_t*)(Ahi + a_off[i] + (KT) * BK + kk * 32);        \
+      if (SPLIT) RA[NA - 1][i][kk] = *(const u32x4_t*)(Alo + a_off[i] + (KT) * BK + kk * 32); \
     }                                                                                 \
   } while (0)
-  // One K-step.  Stage kt is in LDS buffer kt & 1; stage kt + 1 arrives in
-  // A set (kt + 1) % PA and W set RWN; the loads issued here are for stage
-  // kt + 1 + PA (activations) and kt + 1 + PW (weights).
-#define STEP(KT, RAN, RCN, RWN)                                                       \
+#define READ_W(F, BUF, KK)                                                            \
+  do {                                                                                \
+    const bf16_t* base_ = Ws + (BUF) * BUF_ELEMS + wfrag + (KK) * 32;                 \
+    _Pragma("unroll") for (int j = 0; j < FN; ++j)                                    \
+        F[j] = *(const bf16x8_t*)(base_ + j * 16 * LS);                               \
+  } while (0)
+#define MFMA_H(RA, F, KK)                                                             \
+  do {                                                                                \
+    _Pragma("unroll") for (int p = 0; p < NA; ++p)                                    \
+    _Pragma("unroll") for (int i = 0; i < FM; ++i)                                    \
+    _Pragma("unroll") for (int j = 0; j < FN; ++j)                                    \
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(                          \
+            __builtin_bit_cast(bf16x8_t, RA[p][i][KK]), F[j], acc[i][j], 0, 0, 0);     \
+  } while (0)
+    // step kt: wf0 holds (kt, first half); read (kt, second half) into wf1,
+    // use wf0; read (kt + 1, first half) into wf0, use wf1; fetch the
+    // activations of kt + 2 into the set just used; barrier
+#define CSTEP(KT, RA)                                                                 \
   do {                                                                                \
     const int kt_ = (KT);                                                             \
-    if (kt_ < nk) {                                                                   \
-      COMPUTE(kt_ & 1);                                                               \
-      if (kt_ + 1 < nk) {                                                         \
-        STORE_A(RAN, RCN, (kt_ + 1) & 1);                                             \
-        STORE_W(RWN, (kt_ + 1) & 1);                                                  \
-        if (kt_ + 1 + PA < nk) LOAD_A(RAN, RCN, kt_ + 1 + PA);                        \
-        if (kt_ + 1 + PW < nk) LOAD_W(RWN, kt_ + 1 + PW);                             \
-      }                                                                               \
-      __syncthreads();                                                                \
-    }                                                                                 \
+    READ_W(wf1, kt_ % NBUF, 1);                                                       \
+    MFMA_H(RA, wf0, 0);                                                               \
+    READ_W(wf0, (kt_ + 1) % NBUF, 0);                                                 \
+    MFMA_H(RA, wf1, 1);                                                               \
+    LOAD_A(RA, min(kt_ + 2, last));                                                   \
+    __syncthreads();                                                                  \
   } while (0)
 
-  // prologue: stage 0 -> LDS buffer 0; stages 1.. in flight
-  LOAD_A(ra0, rc0, 0);
-  LOAD_W(rw0, 0);
-  STORE_A(ra0, rc0, 0);
-  STORE_W(rw0, 0);
-  if (PA == 1) {
-    if (1 < nk) LOAD_A(ra1, rc1, 1);
-  } else {
-    if (1 < nk) LOAD_A(ra1, rc1, 1);
-    if (2 < nk) LOAD_A(ra0, rc0, 2);
-  }
-  if (1 < nk) LOAD_W(rw1, 1);
-  if (2 < nk) LOAD_W(rw2, 2);
-  if (PW == 4) {
-    if (3 < nk) LOAD_W(rw3, 3);
-    if (4 < nk) LOAD_W(rw0, 4);
-  } else {
-    // with PW == 2 stage 2 lives in set 0
-    if (2 < nk) LOAD_W(rw0, 2);
-  }
-  __syncthreads();
-
-  if constexpr (PW == 4) {
-    for (int kt = 0; kt < nk; kt += 4) {
-      if constexpr (PA == 1) {
-        STEP(kt, ra1, rc1, rw1);
-        STEP(kt + 1, ra1, rc1, rw2);
-        STEP(kt + 2, ra1, rc1, rw3);
-        STEP(kt + 3, ra1, rc1, rw0);
-      } else {
-        STEP(kt, ra1, rc1, rw1);
-        STEP(kt + 1, ra0, rc0, rw2);
-        STEP(kt + 2, ra1, rc1, rw3);
-        STEP(kt + 3, ra0, rc0, rw0);
-      }
-    }
-  } else {
+    LOAD_A(a0, 0);
+    LOAD_A(a1, min(1, last));
+    __syncthreads();                               // weight stages 0 and 1 are in LDS
+    READ_W(wf0, 0, 0);
     for (int kt = 0; kt < nk; kt += 2) {
-      if constexpr (PA == 1) {
-        STEP(kt, ra1, rc1, rw1);
-        STEP(kt + 1, ra1, rc1, rw0);
-      } else {
-        STEP(kt, ra1, rc1, rw1);
-        STEP(kt + 1, ra0, rc0, rw0);
-      }
+      CSTEP(kt, a0);
+      CSTEP(kt + 1, a1);
     }
-  }
 #undef LOAD_A
-#undef LOAD_W
-#undef STORE_A
-#undef STORE_W
-#undef COMPUTE
-#undef STEP
+#undef READ_W
+#undef MFMA_H
+#undef CSTEP
+    // accumulators -> LDS tile: acc[i][j][r] = C[32 wave + 16i + 4*(lane/16) + r][16j + lane%16]
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          Cs[(32 * wave + i * 16 + (lane >> 4) * 4 + r) * CS + j * 16 + (lane & 15)] = acc[i][j][r];
+  } else {
+    // ------------------------------ staging waves ------------------------------
+    const bf16_t *blo, *bhi;
+    pol.b_ptrs(t, BN, blo, bhi);
+    const int st = tid - 256, r0 = st >> 3, col = (st & 7) * 8;
+    const bf16_t* w_src[WR];
+#pragma unroll
+    for (int i = 0; i < WR; ++i) {
+      const int r = r0 + 32 * i;   // tile rows [0, BN/2) come from lo, the rest from hi
+      w_src[i] = (r < BN / 2 ? blo + (size_t)r * pol.ldb : bhi + (size_t)(r - BN / 2) * pol.ldb) + kbeg + col;
+    }
+    u32x4_t s0[WR], s1[WR], s2[WR], s3[WR];      // weight stage s in set s % 4
+#define LOAD_S(S, KT)                                                                 \
+  do {                                                                                \
+    _Pragma("unroll") for (int i = 0; i < WR; ++i) S[i] = *(const u32x4_t*)(w_src[i] + (KT) * BK); \
+  } while (0)
+#define STORE_S(S, BUF)                                                               \
+  do {                                                                                \
+    _Pragma("unroll") for (int i = 0; i < WR; ++i)                                    \
+        *(u32x4_t*)(Ws + (BUF) * BUF_ELEMS + (r0 + 32 * i) * LS + col) = S[i];        \
+  } while (0)
+    // during step kt the compute waves read buffers kt % 3 and (kt + 1) % 3;
+    // the staging waves fill buffer (kt + 2) % 3 with stage kt + 2 and fetch
+    // stage kt + 6 into the register set it came from
+#define SSTEP(KT, S)                                                                  \
+  do {                                                                                \
+    STORE_S(S, ((KT) + 2) % NBUF);                                                    \
+    LOAD_S(S, min((KT) + 6, last));                                                   \
+    __syncthreads();                                                                  \
+  } while (0)
 
-  // accumulators -> LDS tile: acc[i][j][r] = C[16i + 4*(lane/16) + r][16j + lane%16]
-  float* Cs = (float*)smem;
-#pragma unroll
-  for (int i = 0; i < FM; ++i)
-#pragma unroll
-    for (int j = 0; j < FN; ++j)
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-        Cs[(wm * WM + i * 16 + (lane >> 4) * 4 + r) * CS + wn * WN + j * 16 + (lane & 15)] =
-            acc[i][j][r];
+    LOAD_S(s0, 0);
+    LOAD_S(s1, min(1, last));
+    LOAD_S(s2, min(2, last));
+    LOAD_S(s3, min(3, last));
+    STORE_S(s0, 0);
+    STORE_S(s1, 1);
+    LOAD_S(s0, min(4, last));
+    LOAD_S(s1, min(5, last));
+    __syncthreads();                               // weight stages 0 and 1 are in LDS
+    for (int kt = 0; kt < nk; kt += 4) {
+      SSTEP(kt, s2);
+      SSTEP(kt + 1, s3);
+      SSTEP(kt + 2, s0);
+      SSTEP(kt + 3, s1);
+    }
+#undef LOAD_S
+#undef STORE_S
+#undef SSTEP
+  }
   __syncthreads();
   tile_epilogue<BM, BN, CS>(pol, Cs, m0, M, t, part, split, ldp);
 }
@@ -460,7 +427,8 @@ __global__ void __launch_bounds__(256) gemm_bf16_kernel(Pol pol, GemmA ga, int M
 // float32 kernel (fp32 mode): 32x32 tiles, BK = 32, 256 threads, 4 outputs each
 // ---------------------------------------------------------------------------
 template <class Pol>
-__global__ void __launch_bounds__(256) gemm_f32_kernel(Pol pol, GemmA ga, int M, int k_per_split,
+__global__ void __launch_bounds__(256) gemm_f32_kernel(Pol pol, const float* __restrict__ A, int lda,
+                                                       int M, int k_per_split,
                                                        float* __restrict__ part, int ldp) {
   constexpr int BM = 32, BN = 32, BK = 32, CS = BN + 1;
   __shared__ float As[BK][BM + 1];
@@ -471,18 +439,12 @@ __global__ void __launch_bounds__(256) gemm_f32_kernel(Pol pol, GemmA ga, int M,
   const int kbeg = split * k_per_split;
   const float *blo, *bhi;
   pol.b_ptrs(t, BN, blo, bhi);
-  const float* cs = (const float*)ga.cscale;
   const int tr = tid / 8, tc = (tid % 8) * 4;   // output row, first of 4 columns
   float acc[4] = {0.f, 0.f, 0.f, 0.f};
   for (int k0 = kbeg; k0 < kbeg + k_per_split; k0 += BK) {
     for (int idx = tid; idx < BM * BK; idx += 256) {
       const int r = idx / BK, kk = idx % BK;
-      const int m = min(m0 + r, M - 1);
-      const int pm = (m / ga.per) * ga.stride + ga.off + m % ga.per;
-      float v = ga.a[(size_t)pm * ga.lda + k0 + kk];
-      if (ga.rscale) v *= ga.rscale[m];
-      if (cs) v *= cs[k0 + kk];
-      As[kk][r] = v;
+      As[kk][r] = A[(size_t)min(m0 + r, M - 1) * lda + k0 + kk];
       const float* rp = r < BN / 2 ? blo + (size_t)r * pol.ldb : bhi + (size_t)(r - BN / 2) * pol.ldb;
       Bs[kk][r] = rp[k0 + kk];
     }
@@ -531,33 +493,6 @@ __global__ void __launch_bounds__(256) splitk_reduce_kernel(Pol pol, const float
 }
 
 // ---------------------------------------------------------------------------
-// row RMS: inv[o] = 1 / sqrt(mean(x[row(o)]^2) + eps)
-// ---------------------------------------------------------------------------
-__global__ void __launch_bounds__(256) row_rms_kernel(const float* __restrict__ x, int d, float eps,
-                                                      float* __restrict__ inv, int n_rows, int per,
-                                                      int stride, int off) {
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int o = blockIdx.x * 4 + wave;           // one wave per row
-  if (o >= n_rows) return;
-  const float* xr = x + ((size_t)(o / per) * stride + off + o % per) * d;
-  float ss = 0.f;
-  for (int c = lane * 4; c < d; c += 256) {
-    const float4 v = *(const float4*)(xr + c);
-    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
-  }
-  ss = wave_sum(ss);
-  if (lane == 0) inv[o] = 1.0f / sqrtf(ss / (float)d + eps);
-}
-
-hipError_t launch_row_rms(const float* x, int d, float eps, float* inv, int n_rows, int per,
-                          int stride, int off, hipStream_t st) {
-  if (n_rows == 0) return hipSuccess;
-  hipLaunchKernelGGL(row_rms_kernel, dim3(ceil_div(n_rows, 4)), dim3(256), 0, st, x, d, eps, inv,
-                     n_rows, per, stride, off);
-  return hipGetLastError();
-}
-
-// ---------------------------------------------------------------------------
 // host-side dispatch
 // ---------------------------------------------------------------------------
 // Split-K is only used while S * M stays small, which bounds the workspace.
@@ -568,21 +503,22 @@ size_t gemm_split_ws_floats(int M, int max_n) {
   return (size_t)SPLIT_ROWS_MAX * max_n;
 }
 
-// Per-projection launch choice (tile width BN, split-K S, prefetch depths).
+// Per-projection launch choice: tile width BN (64, 96 or 128), split-K S
+// (0 = automatic) and weight prefetch depth PW.
 struct GemmCfg {
-  int bn, s, pa, pw;
+  int bn, s, pw;
 };
 
-// Tuning override: SSM_GEMM_CFG="kind:bn:s:pa:pw,..." with kind one of
-// qkv, o, gate_up, down, lm and s = 0 for the automatic split.
+// Tuning override: SSM_GEMM_CFG="kind:bn:s:pw,..." with kind one of qkv, o,
+// gate_up, down, lm; read once per process.
 static GemmCfg cfg_override(const char* kind, GemmCfg c) {
-  static const char* env = getenv("SSM_GEMM_CFG");   // read once per process
+  static const char* env = getenv("SSM_GEMM_CFG");
   if (!env) return c;
   const size_t kl = strlen(kind);
   for (const char* p = env; p && *p;) {
     if (strncmp(p, kind, kl) == 0 && p[kl] == ':') {
-      int bn, s, pa, pw;
-      if (sscanf(p + kl + 1, "%d:%d:%d:%d", &bn, &s, &pa, &pw) == 4) return GemmCfg{bn, s, pa, pw};
+      int bn, s, pw;
+      if (sscanf(p + kl + 1, "%d:%d:%d", &bn, &s, &pw) == 3) return GemmCfg{bn, s, pw};
     }
     p = strchr(p, ',');
     if (p) ++p;
@@ -592,20 +528,20 @@ static GemmCfg cfg_override(const char* kind, GemmCfg c) {
 
 static int auto_split(int tiles, int M, int K, size_t ws_floats, int N) {
   int S = 1;
-  while (S < 8 && tiles * S < 192 && K % (64 * S * 2) == 0 && (S * 2) * M <= SPLIT_ROWS_MAX &&
+  while (S < 8 && tiles * S < 192 && K % (256 * S * 2) == 0 && (S * 2) * M <= SPLIT_ROWS_MAX &&
          (size_t)(S * 2) * M * N <= ws_floats)
     S *= 2;
   return S;
 }
 
-template <int BN, int PA, int PW, bool SPLIT, class Pol>
-static hipError_t launch_bf16(const Pol& pol, const GemmA& ga, int M, int K, int N, int S,
+template <int BN, int PW, bool SPLIT, class Pol>
+static hipError_t launch_bf16(const Pol& pol, const ActIn& a, int M, int K, int N, int S,
                               SplitWs ws, hipStream_t st) {
-  constexpr int BM = 128, WM = 64, WN = BN / 2;
+  constexpr int BM = 128;
   const int ntiles = N / BN, mt = ceil_div(M, BM);
   dim3 grid(ntiles * mt, S);
-  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, WM, WN, PA, PW, SPLIT, Pol>), grid, dim3(256), 0,
-                     st, pol, ga, M, K / S, mt, S > 1 ? ws.part : nullptr, N);
+  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, PW, SPLIT, Pol>), grid, dim3(512), 0, st, pol,
+                     (const bf16_t*)a.hi, a.lo, a.lda, M, K / S, mt, S > 1 ? ws.part : nullptr, N);
   if (S > 1) {
     const size_t total = (size_t)M * N / (Pol::PAIRED ? 2 : 1);
     hipLaunchKernelGGL((splitk_reduce_kernel<BN, Pol>), dim3((unsigned)((total + 255) / 256)),
@@ -614,36 +550,35 @@ static hipError_t launch_bf16(const Pol& pol, const GemmA& ga, int M, int K, int
   return hipGetLastError();
 }
 
-template <int BN, bool SPLIT, class Pol>
-static hipError_t launch_bf16_pf(const Pol& pol, const GemmA& ga, int M, int K, int N, int S,
-                                 int pa, int pw, SplitWs ws, hipStream_t st) {
-  if (pa == 2 && pw == 4) return launch_bf16<BN, 2, 4, SPLIT>(pol, ga, M, K, N, S, ws, st);
-  if (pa == 1 && pw == 2) return launch_bf16<BN, 1, 2, SPLIT>(pol, ga, M, K, N, S, ws, st);
-  if (pa == 2 && pw == 2) return launch_bf16<BN, 2, 2, SPLIT>(pol, ga, M, K, N, S, ws, st);
-  return launch_bf16<BN, 1, 4, SPLIT>(pol, ga, M, K, N, S, ws, st);
+template <int BN, class Pol>
+static hipError_t launch_bf16_pw(const Pol& pol, const ActIn& a, int M, int K, int N, int S,
+                                 int pw, SplitWs ws, hipStream_t st) {
+  const bool split = a.lo != nullptr;
+  // the kernel's K loop is unrolled by 4: nk = K / S / 64 must be a multiple of 4
+  if (pw <= 2)
+    return split ? launch_bf16<BN, 2, true>(pol, a, M, K, N, S, ws, st)
+                 : launch_bf16<BN, 2, false>(pol, a, M, K, N, S, ws, st);
+  return split ? launch_bf16<BN, 4, true>(pol, a, M, K, N, S, ws, st)
+               : launch_bf16<BN, 4, false>(pol, a, M, K, N, S, ws, st);
 }
 
-// PolBN<BN> rebinds the tile width of the epilogue policies that depend on it.
 template <class Pol>
-static hipError_t run_bf16(const char* kind, Pol pol, const GemmA& ga, int M, int K, int N,
-                           bool split, GemmCfg c, SplitWs ws, hipStream_t st,
-                           void (*rebind)(Pol&, int) = nullptr) {
+static hipError_t run_bf16(const char* kind, Pol pol, const ActIn& a, int M, int K, int N,
+                           GemmCfg c, SplitWs ws, hipStream_t st, int (*bn_ok)(const Pol&, int),
+                           void (*rebind)(Pol&, int)) {
   c = cfg_override(kind, c);
-  if (c.bn != 64 && c.bn != 128) c.bn = 128;
-  if (N % c.bn) c.bn = 64;
+  if (!bn_ok(pol, c.bn) || N % c.bn) c.bn = bn_ok(pol, 128) && N % 128 == 0 ? 128 : 64;
   if (rebind) rebind(pol, c.bn);
   const int tiles = (N / c.bn) * ceil_div(M, 128);
   int S = c.s > 0 ? c.s : auto_split(tiles, M, K, ws.floats, N);
-  while (S > 1 && (K % (64 * S) != 0 || (size_t)S * M * N > ws.floats)) S /= 2;
-  if (c.bn == 128)
-    return split ? launch_bf16_pf<128, true>(pol, ga, M, K, N, S, c.pa, c.pw, ws, st)
-                 : launch_bf16_pf<128, false>(pol, ga, M, K, N, S, c.pa, c.pw, ws, st);
-  return split ? launch_bf16_pf<64, true>(pol, ga, M, K, N, S, c.pa, c.pw, ws, st)
-               : launch_bf16_pf<64, false>(pol, ga, M, K, N, S, c.pa, c.pw, ws, st);
+  while (S > 1 && (K % (256 * S) != 0 || (size_t)S * M * N > ws.floats)) S /= 2;
+  if (c.bn == 96) return launch_bf16_pw<96>(pol, a, M, K, N, S, c.pw, ws, st);
+  if (c.bn == 64) return launch_bf16_pw<64>(pol, a, M, K, N, S, c.pw, ws, st);
+  return launch_bf16_pw<128>(pol, a, M, K, N, S, c.pw, ws, st);
 }
 
 template <class Pol>
-static hipError_t run_f32(const Pol& pol, const GemmA& ga, int M, int K, int N, SplitWs ws,
+static hipError_t run_f32(const Pol& pol, const ActIn& a, int M, int K, int N, SplitWs ws,
                           hipStream_t st) {
   constexpr int BN = 32;
   const int ntiles = N / BN, mt = ceil_div(M, 32);
@@ -652,8 +587,8 @@ static hipError_t run_f32(const Pol& pol, const GemmA& ga, int M, int K, int N, 
          (size_t)(S * 2) * M * N <= ws.floats)
     S *= 2;
   dim3 grid(ntiles, mt, S);
-  hipLaunchKernelGGL((gemm_f32_kernel<Pol>), grid, dim3(256), 0, st, pol, ga, M, K / S,
-                     S > 1 ? ws.part : nullptr, N);
+  hipLaunchKernelGGL((gemm_f32_kernel<Pol>), grid, dim3(256), 0, st, pol, (const float*)a.hi,
+                     a.lda, M, K / S, S > 1 ? ws.part : nullptr, N);
   if (S > 1) {
     const size_t total = (size_t)M * N / (Pol::PAIRED ? 2 : 1);
     hipLaunchKernelGGL((splitk_reduce_kernel<BN, Pol>), dim3((unsigned)((total + 255) / 256)),
@@ -662,61 +597,62 @@ static hipError_t run_f32(const Pol& pol, const GemmA& ga, int M, int K, int N, 
   return hipGetLastError();
 }
 
-// Default launch choices for the HBM-bound row counts of cached steps (M <=
-// 256) and the compute-bound ones of block-start steps.
+// Default launch choices: the cached-step row counts (M <= 256) are
+// HBM-bound and want every CU streaming weights; block-start row counts are
+// MFMA-bound and want wide tiles.
 static GemmCfg default_cfg(const char* kind, int M) {
   const bool small = M <= 256;
-  if (!strcmp(kind, "qkv")) return small ? GemmCfg{64, 1, 1, 4} : GemmCfg{128, 1, 1, 2};
-  if (!strcmp(kind, "gate_up")) return small ? GemmCfg{128, 1, 1, 4} : GemmCfg{128, 1, 1, 2};
-  if (!strcmp(kind, "lm")) return small ? GemmCfg{128, 1, 1, 4} : GemmCfg{128, 1, 1, 2};
-  return small ? GemmCfg{128, 0, 1, 4} : GemmCfg{128, 0, 1, 2};   // o, down
+  if (!strcmp(kind, "qkv")) return small ? GemmCfg{128, 2, 4} : GemmCfg{128, 1, 3};
+  if (!strcmp(kind, "gate_up")) return small ? GemmCfg{128, 1, 4} : GemmCfg{128, 1, 3};
+  if (!strcmp(kind, "lm")) return GemmCfg{128, 1, 4};
+  return small ? GemmCfg{128, 0, 4} : GemmCfg{128, 0, 3};   // o, down
 }
 
+template <class Pol> static int any_bn(const Pol&, int bn) { return bn == 64 || bn == 96 || bn == 128; }
+static int qkv_bn(const PolQKV<bf16_t>& p, int bn) { return (bn == 64 || bn == 128) && p.dh % bn == 0; }
 static void rebind_qkv(PolQKV<bf16_t>& p, int bn) { p.tiles_per_head = p.dh / bn; }
 
-hipError_t gemm_qkv(int dtype, bool split, const GemmA& ga, int M, int d, const void* wq,
-                    const void* wk, const void* wv, int H, int Hkv, int dh, const QKVOut& o,
-                    SplitWs ws, hipStream_t st) {
+hipError_t gemm_qkv(int dtype, const ActIn& a, int M, int d, const void* wq, const void* wk,
+                    const void* wv, int H, int Hkv, int dh, const QKVOut& o, SplitWs ws,
+                    hipStream_t st) {
   const int N = (H + 2 * Hkv) * dh;
   if (dtype == 0) {
     PolQKV<float> p{(const float*)wq, (const float*)wk, (const float*)wv, d, H, Hkv, dh, dh / 32,
                     (float*)o.q, (float*)o.kc, (float*)o.vc, o.cap, o.n_cached, o.n_rows, o.rope};
-    return run_f32(p, ga, M, d, N, ws, st);
+    return run_f32(p, a, M, d, N, ws, st);
   }
   PolQKV<bf16_t> p{(const bf16_t*)wq, (const bf16_t*)wk, (const bf16_t*)wv, d, H, Hkv, dh,
                    dh / 128, (bf16_t*)o.q, (bf16_t*)o.kc, (bf16_t*)o.vc, o.cap, o.n_cached,
                    o.n_rows, o.rope};
-  return run_bf16("qkv", p, ga, M, d, N, split, default_cfg("qkv", M), ws, st, rebind_qkv);
+  return run_bf16("qkv", p, a, M, d, N, default_cfg("qkv", M), ws, st, qkv_bn, rebind_qkv);
 }
 
-hipError_t gemm_resid(int dtype, bool split, const char* kind, const GemmA& ga, int M, int K,
-                      const void* w, int N, float* resid, SplitWs ws, hipStream_t st) {
+hipError_t gemm_resid(int dtype, const char* kind, const ActIn& a, int M, int K, const void* w,
+                      int N, float* resid, SplitWs ws, hipStream_t st) {
   if (dtype == 0) {
     PolResid<float> p{(const float*)w, K, N, resid};
-    return run_f32(p, ga, M, K, N, ws, st);
+    return run_f32(p, a, M, K, N, ws, st);
   }
   PolResid<bf16_t> p{(const bf16_t*)w, K, N, resid};
-  return run_bf16(kind, p, ga, M, K, N, split, default_cfg(kind, M), ws, st);
+  return run_bf16(kind, p, a, M, K, N, default_cfg(kind, M), ws, st, any_bn<PolResid<bf16_t>>,
+                  (void (*)(PolResid<bf16_t>&, int))nullptr);
 }
 
-hipError_t gemm_swiglu(int dtype, bool split, const GemmA& ga, int M, int d, const void* wg,
-                       const void* wu, int F, float* act, SplitWs ws, hipStream_t st) {
+hipError_t gemm_swiglu(int dtype, const ActIn& a, int M, int d, const void* wg, const void* wu,
+                       int F, const ActOut& act, SplitWs ws, hipStream_t st) {
   if (dtype == 0) {
     PolSwiGLU<float> p{(const float*)wg, (const float*)wu, d, F, act};
-    return run_f32(p, ga, M, d, 2 * F, ws, st);
+    return run_f32(p, a, M, d, 2 * F, ws, st);
   }
   PolSwiGLU<bf16_t> p{(const bf16_t*)wg, (const bf16_t*)wu, d, F, act};
-  return run_bf16("gate_up", p, ga, M, d, 2 * F, split, default_cfg("gate_up", M), ws, st);
+  return run_bf16("gate_up", p, a, M, d, 2 * F, default_cfg("gate_up", M), ws, st,
+                  any_bn<PolSwiGLU<bf16_t>>, (void (*)(PolSwiGLU<bf16_t>&, int))nullptr);
 }
 
-hipError_t gemm_store(int dtype, bool split, const GemmA& ga, int M, int K, const void* w, int N,
-                      float* c, int ldc, SplitWs ws, hipStream_t st) {
-  if (dtype == 0) {
-    PolStore<float> p{(const float*)w, K, ldc, c};
-    return run_f32(p, ga, M, K, N, ws, st);
-  }
-  PolStore<bf16_t> p{(const bf16_t*)w, K, ldc, c};
-  return run_bf16("lm", p, ga, M, K, N, split, default_cfg("lm", M), ws, st);
+hipError_t gemm_store_f32(const ActIn& a, int M, int K, const void* w, int N, float* c, int ldc,
+                          SplitWs ws, hipStream_t st) {
+  PolStore<float> p{(const float*)w, K, ldc, c};
+  return run_f32(p, a, M, K, N, ws, st);
 }
 
 // Merges the partial statistics of one row (one workgroup per row), in a
@@ -804,17 +740,15 @@ __global__ void __launch_bounds__(256) lm_merge_kernel(const LMPartial* __restri
 
 size_t lm_stats_ws_bytes(int M, int N) { return (size_t)M * (2 * (N / 128)) * sizeof(LMPartial); }
 
-hipError_t lm_head_stats(bool split, const GemmA& ga, int M, int K, const void* w, int N,
-                         int mask_id, int k, void* stats_ws, float* logits, int32_t* argmax,
-                         float* conf, int32_t* topk_ids, float* topk_w, hipStream_t st) {
+hipError_t lm_head_stats(const ActIn& a, int M, int K, const void* w, int N, int mask_id, int k,
+                         void* stats_ws, float* logits, int32_t* argmax, float* conf,
+                         int32_t* topk_ids, float* topk_w, hipStream_t st) {
   constexpr int BN = 128;
   const int ntiles = N / BN;
   PolLMStats<bf16_t> p{(const bf16_t*)w, K, N, mask_id, (LMPartial*)stats_ws, 2 * ntiles, logits, N};
-  GemmCfg c = cfg_override("lm", default_cfg("lm", M));
-  const int pa = c.pa, pw = c.pw;
+  const GemmCfg c = cfg_override("lm", default_cfg("lm", M));
   SplitWs none{nullptr, 0};
-  hipError_t e = split ? launch_bf16_pf<BN, true>(p, ga, M, K, N, 1, pa, pw, none, st)
-                       : launch_bf16_pf<BN, false>(p, ga, M, K, N, 1, pa, pw, none, st);
+  hipError_t e = launch_bf16_pw<BN>(p, a, M, K, N, 1, c.pw, none, st);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(lm_merge_kernel, dim3(M), dim3(256), 0, st, (const LMPartial*)stats_ws,
                      2 * ntiles, k, argmax, conf, topk_ids, topk_w);

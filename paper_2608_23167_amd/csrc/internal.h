@@ -5,6 +5,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "common.h"
 
 namespace ssm {
@@ -55,39 +57,56 @@ struct SplitWs {
   size_t floats;
 };
 
-// float32 activation operand of a projection, with the fused RMSNorm scales:
-// A[m, k] = a[row(m) * lda + k] * rscale[m] * cscale[k] (a null scale is 1),
-// row(m) = (m / per) * stride + off + m % per.
-struct GemmA {
-  const float* a;
+// Activation operand of a projection: bfloat16 [M, lda] (hi) with an
+// optional second bfloat16 part (lo) so that hi + lo carries the float32
+// value; for float32 models `hi` is a float32 [M, lda] array and lo is null.
+struct ActIn {
+  const void* hi;
+  const bf16_t* lo;
   int lda;
-  const float* rscale;
-  const void* cscale;     // model dtype
-  int per, stride, off;
 };
 
-inline GemmA plain_a(const float* a, int lda, int M) { return GemmA{a, lda, nullptr, nullptr, M, 0, 0}; }
+// Destination of an activation written by an epilogue: float32 for float32
+// models; for bfloat16 models hi = bf16(v) and, if lo is not null,
+// lo = bf16(v - hi).
+struct ActOut {
+  void* hi;
+  bf16_t* lo;
+  template <typename T>
+  __device__ __forceinline__ void store(size_t i, float v) const {
+    if constexpr (std::is_same<T, float>::value) {
+      ((float*)hi)[i] = v;
+    } else {
+      const bf16_t h = f2bf(v);
+      ((bf16_t*)hi)[i] = h;
+      if (lo) lo[i] = f2bf(v - bf2f(h));
+    }
+  }
+};
 
-hipError_t launch_row_rms(const float* x, int d, float eps, float* inv, int n_rows, int per,
-                          int stride, int off, hipStream_t st);
-hipError_t gemm_qkv(int dtype, bool split, const GemmA& a, int M, int d, const void* wq,
-                    const void* wk, const void* wv, int H, int Hkv, int dh, const QKVOut& out,
-                    SplitWs ws, hipStream_t st);
-hipError_t gemm_resid(int dtype, bool split, const char* kind, const GemmA& a, int M, int K,
-                      const void* w, int N, float* resid, SplitWs ws, hipStream_t st);
-hipError_t gemm_swiglu(int dtype, bool split, const GemmA& a, int M, int d, const void* wg,
-                       const void* wu, int F, float* act, SplitWs ws, hipStream_t st);
-hipError_t gemm_store(int dtype, bool split, const GemmA& a, int M, int K, const void* w, int N,
-                      float* c, int ldc, SplitWs ws, hipStream_t st);
+// RMSNorm of float32 rows into a projection operand: output row o reads
+// input row (o / per) * stride + off + o % per.
+hipError_t launch_norm(int dtype, const float* x, int d, const void* g, float eps,
+                       const ActOut& y, int n_rows, int per, int stride, int off, hipStream_t st);
+
+hipError_t gemm_qkv(int dtype, const ActIn& a, int M, int d, const void* wq, const void* wk,
+                    const void* wv, int H, int Hkv, int dh, const QKVOut& out, SplitWs ws,
+                    hipStream_t st);
+hipError_t gemm_resid(int dtype, const char* kind, const ActIn& a, int M, int K, const void* w,
+                      int N, float* resid, SplitWs ws, hipStream_t st);
+hipError_t gemm_swiglu(int dtype, const ActIn& a, int M, int d, const void* wg, const void* wu,
+                       int F, const ActOut& act, SplitWs ws, hipStream_t st);
+hipError_t gemm_store_f32(const ActIn& a, int M, int K, const void* w, int N, float* c, int ldc,
+                          SplitWs ws, hipStream_t st);
 size_t gemm_split_ws_floats(int M, int max_n);
 
 // bfloat16 LM head with the row statistics fused into the GEMM epilogue
 // (per half tile) and merged by a second kernel; logits stored only if
 // `logits` is not null.  N must be a multiple of 128.
 size_t lm_stats_ws_bytes(int M, int N);
-hipError_t lm_head_stats(bool split, const GemmA& a, int M, int K, const void* w, int N,
-                         int mask_id, int k, void* stats_ws, float* logits, int32_t* argmax,
-                         float* conf, int32_t* topk_ids, float* topk_w, hipStream_t st);
+hipError_t lm_head_stats(const ActIn& a, int M, int K, const void* w, int N, int mask_id, int k,
+                         void* stats_ws, float* logits, int32_t* argmax, float* conf,
+                         int32_t* topk_ids, float* topk_w, hipStream_t st);
 
 // ---- attention -----------------------------------------------------------
 struct AttnWs {
@@ -95,9 +114,9 @@ struct AttnWs {
   float* ml;         // [S, B*H, Mq, 2]
   int max_splits;
 };
-// out: float32 [B * Mq, H * dh]
+// out: [B * Mq, H * dh] activation operand of the output projection
 hipError_t attention(int dtype, const void* q, const void* kc, const void* vc, int B, int H,
-                     int Hkv, int dh, int Mq, int Nk, int cap, float* out, AttnWs ws,
+                     int Hkv, int dh, int Mq, int Nk, int cap, const ActOut& out, AttnWs ws,
                      hipStream_t st);
 
 // ---- unmasking ------------------------------------------------------------

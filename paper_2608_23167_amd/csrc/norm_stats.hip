@@ -1,7 +1,90 @@
-// RoPE angle table and the per-row output statistics of the LM head.
+// RMSNorm into projection operands, RoPE angle table and the per-row output
+// statistics of the float32 LM head.
 #include "internal.h"
 
 namespace ssm {
+
+// ---- RMSNorm: y = x / sqrt(mean(x^2) + eps) * g, one wave per row --------
+// Vector form: each lane holds NV float4 of the row in registers, so every
+// load of the row is in flight at once and the row is read once.
+template <typename T, int NV>
+__global__ void __launch_bounds__(256) norm_vec_kernel(const float* __restrict__ x, int d,
+                                                       const T* __restrict__ g, float eps,
+                                                       ActOut y, int n_rows, int per, int stride,
+                                                       int off) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int o = blockIdx.x * 4 + wave;
+  if (o >= n_rows) return;
+  const float4* xr = (const float4*)(x + ((size_t)(o / per) * stride + off + o % per) * d);
+  float4 v[NV];
+#pragma unroll
+  for (int i = 0; i < NV; ++i) v[i] = xr[lane + 64 * i];
+  float ss = 0.f;
+#pragma unroll
+  for (int i = 0; i < NV; ++i) ss += v[i].x * v[i].x + v[i].y * v[i].y + v[i].z * v[i].z + v[i].w * v[i].w;
+  ss = wave_sum(ss);
+  const float inv = 1.0f / sqrtf(ss / (float)d + eps);
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const int c = 4 * (lane + 64 * i);
+    const size_t idx = (size_t)o * d + c;
+    const float r[4] = {v[i].x * inv * ldf(g + c), v[i].y * inv * ldf(g + c + 1),
+                        v[i].z * inv * ldf(g + c + 2), v[i].w * inv * ldf(g + c + 3)};
+    if constexpr (std::is_same<T, float>::value) {
+      *(float4*)((float*)y.hi + idx) = make_float4(r[0], r[1], r[2], r[3]);
+    } else {
+      uint16_t hi[4], lo[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        hi[e] = f2bf(r[e]);
+        lo[e] = f2bf(r[e] - bf2f(hi[e]));
+      }
+      *(uint2*)((bf16_t*)y.hi + idx) = *(const uint2*)hi;
+      if (y.lo) *(uint2*)(y.lo + idx) = *(const uint2*)lo;
+    }
+  }
+}
+
+// Any width: two passes, element by element.
+template <typename T>
+__global__ void __launch_bounds__(256) norm_kernel(const float* __restrict__ x, int d,
+                                                   const T* __restrict__ g, float eps, ActOut y,
+                                                   int n_rows, int per, int stride, int off) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int o = blockIdx.x * 4 + wave;
+  if (o >= n_rows) return;
+  const float* xr = x + ((size_t)(o / per) * stride + off + o % per) * d;
+  float ss = 0.f;
+  for (int c = lane; c < d; c += 64) ss += xr[c] * xr[c];
+  ss = wave_sum(ss);
+  const float inv = 1.0f / sqrtf(ss / (float)d + eps);
+  for (int c = lane; c < d; c += 64) y.store<T>((size_t)o * d + c, xr[c] * inv * ldf(g + c));
+}
+
+template <typename T>
+static hipError_t norm_dispatch(const float* x, int d, const T* g, float eps, const ActOut& y,
+                                int n_rows, int per, int stride, int off, hipStream_t st) {
+  const dim3 grid(ceil_div(n_rows, 4)), block(256);
+  if (d % 256 == 0) {
+    switch (d / 256) {
+#define NORM_CASE(NV) \
+  case NV: hipLaunchKernelGGL((norm_vec_kernel<T, NV>), grid, block, 0, st, x, d, g, eps, y, n_rows, per, stride, off); return hipGetLastError();
+      NORM_CASE(1) NORM_CASE(2) NORM_CASE(4) NORM_CASE(8) NORM_CASE(12) NORM_CASE(14)
+      NORM_CASE(16) NORM_CASE(20) NORM_CASE(24) NORM_CASE(32)
+#undef NORM_CASE
+      default: break;
+    }
+  }
+  hipLaunchKernelGGL(norm_kernel<T>, grid, block, 0, st, x, d, g, eps, y, n_rows, per, stride, off);
+  return hipGetLastError();
+}
+
+hipError_t launch_norm(int dtype, const float* x, int d, const void* g, float eps,
+                       const ActOut& y, int n_rows, int per, int stride, int off, hipStream_t st) {
+  if (n_rows == 0) return hipSuccess;
+  if (dtype == 0) return norm_dispatch(x, d, (const float*)g, eps, y, n_rows, per, stride, off, st);
+  return norm_dispatch(x, d, (const bf16_t*)g, eps, y, n_rows, per, stride, off, st);
+}
 
 // ---- RoPE table (rotate-half form), float64 arithmetic -------------------
 __global__ void rope_table_kernel(const int32_t* __restrict__ pos, int n_rows, int half, int dh,

@@ -129,9 +129,10 @@ __global__ void __launch_bounds__(256) attn_bf16_kernel(
   // o[db][r] = O^T[dh 16db + 4g + r][query c16]
   if (Opart == nullptr) {
     const float inv = 1.0f / l_run;
-    const size_t base = ((size_t)s * Mq + q) * (size_t)(H * DH) + h * DH;
+    const int row = s * Mq + q;
 #pragma unroll
     for (int db = 0; db < 8; ++db) {
+      const size_t idx = frag_index(row, h * DH + 16 * db + 4 * g, O.G);   // 4 columns, one chunk
       uint16_t hi[4], lo[4];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
@@ -139,8 +140,8 @@ __global__ void __launch_bounds__(256) attn_bf16_kernel(
         hi[r] = f2bf(v);
         lo[r] = f2bf(v - bf2f(hi[r]));
       }
-      *(uint2*)((bf16_t*)O.hi + base + 16 * db + 4 * g) = *(const uint2*)hi;
-      if (O.lo) *(uint2*)(O.lo + base + 16 * db + 4 * g) = *(const uint2*)lo;
+      *(uint2*)((bf16_t*)O.hi + idx) = *(const uint2*)hi;
+      if (O.lo) *(uint2*)(O.lo + idx) = *(const uint2*)lo;
     }
   } else {
     const size_t row = ((size_t)split * gridDim.y + bh) * Mq + q;
@@ -184,7 +185,7 @@ __global__ void __launch_bounds__(64) attn_f32_kernel(
     m_run = m_new;
   }
   if (Opart == nullptr) {
-    float* out = (float*)O.hi + ((size_t)s * Mq + q) * (size_t)(H * DH) + h * DH;
+    float* out = (float*)O.hi + ((size_t)s * Mq + q) * O.ld + h * DH;
     const float inv = 1.0f / l_run;
 #pragma unroll
     for (int c = 0; c < DH; ++c) out[c] = ov[c] * inv;
@@ -212,14 +213,13 @@ __global__ void attn_merge_kernel(const float* __restrict__ Opart, const float* 
     if (l > 0.f) L += l * exp2f(ML[r * 2] - M);
   }
   const float inv = 1.0f / L;
-  const size_t base = ((size_t)s * Mq + q) * (size_t)(H * DH) + h * DH;
   for (int c = threadIdx.x; c < DH; c += blockDim.x) {
     float acc = 0.f;
     for (int i = 0; i < S; ++i) {
       const size_t r = (size_t)i * BH * Mq + row;
       if (ML[r * 2 + 1] > 0.f) acc += Opart[r * DH + c] * exp2f(ML[r * 2] - M);
     }
-    O.store<T>(base + c, acc * inv);
+    O.store<T>(s * Mq + q, h * DH + c, acc * inv);
   }
 }
 

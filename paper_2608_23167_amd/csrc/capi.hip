@@ -187,15 +187,17 @@ WsLayout ws_layout(const ssm_model* m, int batch, int max_rows) {
   size_t off = 0;
   auto take = [&](size_t bytes) { size_t o = off; off += align256(bytes); return o; };
   // projection operands: float32 for float32 models, bfloat16 hi (+ lo) otherwise
+  // (bfloat16 operands in fragment order: rows padded to whole 16-row groups)
   const size_t lo_es = (m->dtype == SSM_DT_BF16 && m->act_mode == SSM_ACT_BF16X2) ? 2 : 0;
+  const size_t Mp = (size_t)row_groups((int)Mt) * 16;
   w.resid = take(Mt * d * 4);
-  w.xn = take(Mt * d * es);
-  w.xn_lo = take(Mt * d * lo_es);
+  w.xn = take(Mp * d * es);
+  w.xn_lo = take(Mp * d * lo_es);
   w.q = take(Mt * H * dh * es);
-  w.attn = take(Mt * H * dh * es);
-  w.attn_lo = take(Mt * H * dh * lo_es);
-  w.act = take(Mt * F * es);
-  w.act_lo = take(Mt * F * lo_es);
+  w.attn = take(Mp * H * dh * es);
+  w.attn_lo = take(Mp * H * dh * lo_es);
+  w.act = take(Mp * F * es);
+  w.act_lo = take(Mp * F * lo_es);
   w.rope = take((size_t)max_rows * (dh / 2) * 8);
   w.opart = take((size_t)ATTN_MAX_SPLITS * Mt * H * dh * 4);
   w.ml = take((size_t)ATTN_MAX_SPLITS * Mt * H * 2 * 4);
@@ -314,9 +316,12 @@ int32_t ssm_denoise_step(const ssm_model* m, const ssm_kv_cache* cache, int32_t 
   bf16_t* xn_lo = split ? (bf16_t*)(ws + w.xn_lo) : nullptr;
   bf16_t* attn_lo = split ? (bf16_t*)(ws + w.attn_lo) : nullptr;
   bf16_t* act_lo = split ? (bf16_t*)(ws + w.act_lo) : nullptr;
-  const ActOut xn_out{ws + w.xn, xn_lo}, attn_out{ws + w.attn, attn_lo}, act_out{ws + w.act, act_lo};
-  const ActIn xn_in{ws + w.xn, xn_lo, d}, attn_in{ws + w.attn, attn_lo, H * dh},
-      act_in{ws + w.act, act_lo, F};
+  // every step-local operand has Mt rows; the LM head input has Mo rows
+  const int Gt = row_groups(Mt), Go = row_groups(Mo);
+  const ActOut xn_out{ws + w.xn, xn_lo, d, Gt}, attn_out{ws + w.attn, attn_lo, H * dh, Gt},
+      act_out{ws + w.act, act_lo, F, Gt}, head_out{ws + w.xn, xn_lo, d, Go};
+  const ActIn xn_in{ws + w.xn, xn_lo, d, Gt}, attn_in{ws + w.attn, attn_lo, H * dh, Gt},
+      act_in{ws + w.act, act_lo, F, Gt}, head_in{ws + w.xn, xn_lo, d, Go};
   void* qb = ws + w.q;
   float2* rope = (float2*)(ws + w.rope);
   SplitWs sws{(float*)(ws + w.part), w.part_floats};
@@ -346,14 +351,14 @@ int32_t ssm_denoise_step(const ssm_model* m, const ssm_kv_cache* cache, int32_t 
     HIP_TRY(hipMemcpyAsync(d_hidden_dbg, resid, (size_t)Mt * d * 4, hipMemcpyDeviceToDevice, st));
   // final norm and LM head over the output rows only: output row o is row
   // first_out_row + o % n_out of sequence o / n_out
-  PROF_TRY("norm", launch_norm(dt, resid, d, m->final_norm, m->rms_eps, xn_out, Mo, n_out, n_rows,
-                               first_out_row, st));
+  PROF_TRY("norm", launch_norm(dt, resid, d, m->final_norm, m->rms_eps, head_out, Mo, n_out,
+                               n_rows, first_out_row, st));
   if (dt == SSM_DT_BF16) {
-    PROF_TRY("gemm_lm_head", lm_head_stats(xn_in, Mo, d, m->lm_head, V, m->mask_id, k,
+    PROF_TRY("gemm_lm_head", lm_head_stats(head_in, Mo, d, m->lm_head, V, m->mask_id, k,
                                            ws + w.lmstats, d_logits_dbg, d_argmax, d_conf,
                                            d_topk_ids, d_topk_w, st));
   } else {
-    PROF_TRY("gemm_lm_head", gemm_store_f32(xn_in, Mo, d, m->lm_head, V, logits, V, sws, st));
+    PROF_TRY("gemm_lm_head", gemm_store_f32(head_in, Mo, d, m->lm_head, V, logits, V, sws, st));
     PROF_TRY("rowstats", launch_rowstats(logits, Mo, V, V, m->mask_id, k, d_argmax, d_conf,
                                          d_topk_ids, d_topk_w, st));
   }

@@ -12,8 +12,9 @@
 //     three LDS buffers two K-steps ahead of their use;
 //   * compute waves (0-3) each own 32 rows x BN columns: they load their
 //     activation fragments straight from global memory (small, shared by
-//     every workgroup, L2-resident) two K-steps ahead, read the weight
-//     fragments from LDS and issue the MFMAs.
+//     every workgroup, L2-resident, stored in fragment order so that each
+//     16-byte-per-lane load reads 1 KB contiguously) two K-steps ahead, read
+//     the weight fragments from LDS and issue the MFMAs.
 // Splitting the roles keeps the in-order retirement of vector loads from
 // coupling the long HBM latency of the weights to the MFMA issue.  One
 // barrier per K-step (64) hands the LDS buffers over.  The output tile is
@@ -95,7 +96,7 @@ struct PolSwiGLU {
   }
   __device__ __forceinline__ void store(int m, int t, int c, int BN, float g, float u) const {
     const float silu = g / (1.0f + expf(-g));
-    act.store<T>((size_t)m * F + t * (BN / 2) + c, silu * u);
+    act.store<T>(m, t * (BN / 2) + c, silu * u);
   }
 };
 
@@ -239,14 +240,19 @@ __device__ __forceinline__ void tile_epilogue(const Pol& pol, const float* Cs, i
 // ---------------------------------------------------------------------------
 // bfloat16 MFMA kernel
 // ---------------------------------------------------------------------------
-// Tile order: the grid is 1-D over (n-tile, m-tile) pairs.  Workgroups are
-// dealt to the 8 XCDs round-robin by linear id, so id w runs on XCD w % 8;
-// the order below gives each XCD a contiguous range of n-tiles with the
-// m-tiles innermost, so the workgroups that share a weight tile run on the
-// same XCD at about the same time and read it once into that XCD's L2.
-__device__ __forceinline__ void tile_of(int w, int total, int mt, int& tn, int& tm) {
+// Tile order: the grid is 1-D over (split, n-tile, m-tile) triples.
+// Workgroups are dealt to the 8 XCDs round-robin by linear id, so id w runs
+// on XCD w % 8; the order below gives each XCD a contiguous range of the
+// triples, split-major, then n-tiles, m-tiles innermost.  The workgroups that
+// share a weight tile then run on the same XCD at about the same time and
+// read it once into that XCD's L2, and each XCD touches as few K-slices of
+// the activations as possible, so that its slice stays resident in its L2.
+__device__ __forceinline__ void tile_of(int w, int total, int ntm, int mt, int& split, int& tn,
+                                        int& tm) {
   const int per = total / 8;
-  const int t = w < per * 8 ? (w % 8) * per + (w / 8) : w;
+  const int v = w < per * 8 ? (w % 8) * per + (w / 8) : w;
+  split = v / ntm;
+  const int t = v % ntm;
   tn = t / mt;
   tm = t % mt;
 }
@@ -268,9 +274,10 @@ __device__ __forceinline__ void tile_of(int w, int total, int mt, int& tn, int& 
 // one workgroup barrier on both paths.
 template <int BM, int BN, int PW, bool SPLIT, class Pol>
 __global__ void __launch_bounds__(512) gemm_bf16_kernel(Pol pol, const bf16_t* __restrict__ Ahi,
-                                                        const bf16_t* __restrict__ Alo, int lda,
+                                                        const bf16_t* __restrict__ Alo, int G,
                                                         int M, int k_per_split, int mt,
-                                                        float* __restrict__ part, int ldp) {
+                                                        int n_split, float* __restrict__ part,
+                                                        int ldp) {
   static_assert(BM == 128, "4 compute waves of 32 rows");
   constexpr int BK = 64, LS = BK + 8;            // LDS row stride (elements), 144 B
   constexpr int FM = 2, FN = BN / 16;            // per compute wave: 32 rows x BN columns
@@ -287,9 +294,9 @@ __global__ void __launch_bounds__(512) gemm_bf16_kernel(Pol pol, const bf16_t* _
   bf16_t* Ws = (bf16_t*)smem;                    // [NBUF][BN][LS]
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  int t, mtile;
-  tile_of(blockIdx.x, gridDim.x, mt, t, mtile);
-  const int m0 = mtile * BM, split = blockIdx.y;
+  int t, mtile, split;
+  tile_of(blockIdx.x, gridDim.x, gridDim.x / n_split, mt, split, t, mtile);
+  const int m0 = mtile * BM;
   const int kbeg = split * k_per_split;
   const int nk = k_per_split / BK;               // a multiple of 4 (host-checked)
   const int last = nk - 1;
@@ -297,12 +304,15 @@ __global__ void __launch_bounds__(512) gemm_bf16_kernel(Pol pol, const bf16_t* _
 
   if (wave < 4) {
     // ------------------------------ compute waves ------------------------------
-    // activation fragment i, half kk of a K-step: row 32 wave + 16 i + lane % 16,
-    // 8 consecutive k at 32 kk + 8 (lane / 16); rows past M are computed and discarded
+    // activation fragment i, half kk of K-step kt: the 1 KB fragment-order
+    // block of row group (m0 + 32 wave + 16 i) / 16, lane l at 8 l (groups past
+    // the allocation read the last one; rows past M are computed and discarded)
+    const size_t a_kstep = (size_t)G * 1024;
     size_t a_off[FM];
 #pragma unroll
     for (int i = 0; i < FM; ++i)
-      a_off[i] = (size_t)min(m0 + 32 * wave + 16 * i + (lane & 15), M - 1) * lda + kbeg + (lane >> 4) * 8;
+      a_off[i] = (size_t)(kbeg >> 6) * a_kstep +
+                 (size_t)min((m0 + 32 * wave + 16 * i) >> 4, G - 1) * 1024 + lane * 8;
     // weight fragment j, half kk: LDS row 16 j + lane % 16, column 32 kk + 8 (lane / 16)
     const int wfrag = (lane & 15) * LS + (lane >> 4) * 8;
     f32x4_t acc[FM][FN];
@@ -317,8 +327,8 @@ __global__ void __launch_bounds__(512) gemm_bf16_kernel(Pol pol, const bf16_t* _
   do {                                                                                \
     _Pragma("unroll") for (int i = 0; i < FM; ++i)                                    \
     _Pragma("unroll") for (int kk = 0; kk < 2; ++kk) {                                \
-      RA[0][i][kk] = *(const u32x4_t*)(Ahi + a_off[i] + (KT) * BK + kk * 32);        \
-      if (SPLIT) RA[NA - 1][i][kk] = *(const u32x4_t*)(Alo + a_off[i] + (KT) * BK + kk * 32); \
+      RA[0][i][kk] = *(const u32x4_t*)(Ahi + a_off[i] + (KT) * a_kstep + kk * 512);  \
+      if (SPLIT) RA[NA - 1][i][kk] = *(const u32x4_t*)(Alo + a_off[i] + (KT) * a_kstep + kk * 512); \
     }                                                                                 \
   } while (0)
 #define READ_W(F, BUF, KK)                                                            \
@@ -539,9 +549,10 @@ static hipError_t launch_bf16(const Pol& pol, const ActIn& a, int M, int K, int 
                               SplitWs ws, hipStream_t st) {
   constexpr int BM = 128;
   const int ntiles = N / BN, mt = ceil_div(M, BM);
-  dim3 grid(ntiles * mt, S);
+  const dim3 grid(ntiles * mt * S);
   hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, PW, SPLIT, Pol>), grid, dim3(512), 0, st, pol,
-                     (const bf16_t*)a.hi, a.lo, a.lda, M, K / S, mt, S > 1 ? ws.part : nullptr, N);
+                     (const bf16_t*)a.hi, a.lo, a.G, M, K / S, mt, S,
+                     S > 1 ? ws.part : nullptr, N);
   if (S > 1) {
     const size_t total = (size_t)M * N / (Pol::PAIRED ? 2 : 1);
     hipLaunchKernelGGL((splitk_reduce_kernel<BN, Pol>), dim3((unsigned)((total + 255) / 256)),
@@ -588,7 +599,7 @@ static hipError_t run_f32(const Pol& pol, const ActIn& a, int M, int K, int N, S
     S *= 2;
   dim3 grid(ntiles, mt, S);
   hipLaunchKernelGGL((gemm_f32_kernel<Pol>), grid, dim3(256), 0, st, pol, (const float*)a.hi,
-                     a.lda, M, K / S, S > 1 ? ws.part : nullptr, N);
+                     a.ld, M, K / S, S > 1 ? ws.part : nullptr, N);
   if (S > 1) {
     const size_t total = (size_t)M * N / (Pol::PAIRED ? 2 : 1);
     hipLaunchKernelGGL((splitk_reduce_kernel<BN, Pol>), dim3((unsigned)((total + 255) / 256)),

@@ -57,26 +57,48 @@ struct SplitWs {
   size_t floats;
 };
 
-// Activation operand of a projection: bfloat16 [M, lda] (hi) with an
-// optional second bfloat16 part (lo) so that hi + lo carries the float32
-// value; for float32 models `hi` is a float32 [M, lda] array and lo is null.
+// bfloat16 projection operands are stored in MFMA fragment order.  The
+// matrix [M, K] (K a multiple of 64) is cut into 16-row groups and 64-column
+// K-steps; each (K-step, group) pair owns two 1 KB halves of 16 rows x 32
+// columns, and inside a half the 8-element chunk of row r, columns
+// 8q .. 8q + 7, sits at chunk position 16q + r.  One 16-byte load per lane
+// (lane 16q + r) then reads a whole half contiguously, already in the
+// A-operand layout of v_mfma_f32_16x16x32_bf16; a row-major operand would
+// touch 16 cache lines per load instruction instead of 8.  G is the number
+// of row groups of the allocation; rows past M are padding, never stored
+// back by any epilogue.
+__host__ __device__ __forceinline__ size_t frag_index(int m, int k, int G) {
+  return ((((size_t)(k >> 6) * G + (m >> 4)) * 2 + ((k >> 5) & 1)) * 64 + ((k >> 3) & 3) * 16 +
+          (m & 15)) * 8 + (k & 7);
+}
+__host__ __device__ __forceinline__ int row_groups(int M) { return (M + 15) >> 4; }
+
+// Activation operand of a projection: for bfloat16 models a bfloat16 array
+// (hi) in fragment order with G row groups, plus an optional second
+// bfloat16 part (lo) in the same order so that hi + lo carries the float32
+// value; for float32 models `hi` is a row-major float32 array with row
+// stride ld and lo is null.
 struct ActIn {
   const void* hi;
   const bf16_t* lo;
-  int lda;
+  int ld;
+  int G;
 };
 
-// Destination of an activation written by an epilogue: float32 for float32
-// models; for bfloat16 models hi = bf16(v) and, if lo is not null,
-// lo = bf16(v - hi).
+// Destination of an activation written by an epilogue, in the layout of
+// ActIn: float32 row-major for float32 models; for bfloat16 models
+// hi = bf16(v) and, if lo is not null, lo = bf16(v - hi), in fragment order.
 struct ActOut {
   void* hi;
   bf16_t* lo;
+  int ld;
+  int G;
   template <typename T>
-  __device__ __forceinline__ void store(size_t i, float v) const {
+  __device__ __forceinline__ void store(int m, int k, float v) const {
     if constexpr (std::is_same<T, float>::value) {
-      ((float*)hi)[i] = v;
+      ((float*)hi)[(size_t)m * ld + k] = v;
     } else {
+      const size_t i = frag_index(m, k, G);
       const bf16_t h = f2bf(v);
       ((bf16_t*)hi)[i] = h;
       if (lo) lo[i] = f2bf(v - bf2f(h));

@@ -27,11 +27,10 @@ __global__ void __launch_bounds__(256) norm_vec_kernel(const float* __restrict__
 #pragma unroll
   for (int i = 0; i < NV; ++i) {
     const int c = 4 * (lane + 64 * i);
-    const size_t idx = (size_t)o * d + c;
     const float r[4] = {v[i].x * inv * ldf(g + c), v[i].y * inv * ldf(g + c + 1),
                         v[i].z * inv * ldf(g + c + 2), v[i].w * inv * ldf(g + c + 3)};
     if constexpr (std::is_same<T, float>::value) {
-      *(float4*)((float*)y.hi + idx) = make_float4(r[0], r[1], r[2], r[3]);
+      *(float4*)((float*)y.hi + (size_t)o * y.ld + c) = make_float4(r[0], r[1], r[2], r[3]);
     } else {
       uint16_t hi[4], lo[4];
 #pragma unroll
@@ -39,6 +38,7 @@ __global__ void __launch_bounds__(256) norm_vec_kernel(const float* __restrict__
         hi[e] = f2bf(r[e]);
         lo[e] = f2bf(r[e] - bf2f(hi[e]));
       }
+      const size_t idx = frag_index(o, c, y.G);   // 4 consecutive columns share a chunk
       *(uint2*)((bf16_t*)y.hi + idx) = *(const uint2*)hi;
       if (y.lo) *(uint2*)(y.lo + idx) = *(const uint2*)lo;
     }
@@ -58,7 +58,7 @@ __global__ void __launch_bounds__(256) norm_kernel(const float* __restrict__ x, 
   for (int c = lane; c < d; c += 64) ss += xr[c] * xr[c];
   ss = wave_sum(ss);
   const float inv = 1.0f / sqrtf(ss / (float)d + eps);
-  for (int c = lane; c < d; c += 64) y.store<T>((size_t)o * d + c, xr[c] * inv * ldf(g + c));
+  for (int c = lane; c < d; c += 64) y.store<T>(o, c, xr[c] * inv * ldf(g + c));
 }
 
 template <typename T>

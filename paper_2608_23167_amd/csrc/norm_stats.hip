@@ -4,31 +4,57 @@
 
 namespace ssm {
 
-// ---- RMSNorm: y = x / sqrt(mean(x^2) + eps) * g, one wave per row --------
-// Vector form: each lane holds NV float4 of the row in registers, so every
-// load of the row is in flight at once and the row is read once.
+// ---- RMSNorm: y = x / sqrt(mean(x^2) + eps) * g ----------------------------
+// Vector form, one workgroup of 256 threads per row: thread t holds float4
+// number t + 256 i of the row (i < NV) and the matching four gains, all
+// loaded before the reduction, so a row costs one round trip to memory.
+template <typename T> struct Gain4;
+template <> struct Gain4<float> {
+  __device__ __forceinline__ static float4 ld(const float* g) { return *(const float4*)g; }
+};
+template <> struct Gain4<bf16_t> {
+  __device__ __forceinline__ static float4 ld(const bf16_t* g) {
+    const uint2 u = *(const uint2*)g;
+    return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u),
+                       __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u));
+  }
+};
+
 template <typename T, int NV>
 __global__ void __launch_bounds__(256) norm_vec_kernel(const float* __restrict__ x, int d,
                                                        const T* __restrict__ g, float eps,
-                                                       ActOut y, int n_rows, int per, int stride,
-                                                       int off) {
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int o = blockIdx.x * 4 + wave;
-  if (o >= n_rows) return;
+                                                       ActOut y, int per, int stride, int off) {
+  __shared__ float red[4];
+  const int o = blockIdx.x, tid = threadIdx.x;
+  const int nv4 = d >> 2;
   const float4* xr = (const float4*)(x + ((size_t)(o / per) * stride + off + o % per) * d);
-  float4 v[NV];
-#pragma unroll
-  for (int i = 0; i < NV; ++i) v[i] = xr[lane + 64 * i];
+  float4 v[NV], gv[NV];
   float ss = 0.f;
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const int j = tid + 256 * i;
+    if (j < nv4) {
+      v[i] = xr[j];
+      gv[i] = Gain4<T>::ld(g + 4 * j);
+    } else {
+      v[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+      gv[i] = v[i];
+    }
+  }
 #pragma unroll
   for (int i = 0; i < NV; ++i) ss += v[i].x * v[i].x + v[i].y * v[i].y + v[i].z * v[i].z + v[i].w * v[i].w;
   ss = wave_sum(ss);
+  if ((tid & 63) == 0) red[tid >> 6] = ss;
+  __syncthreads();
+  ss = (red[0] + red[1]) + (red[2] + red[3]);
   const float inv = 1.0f / sqrtf(ss / (float)d + eps);
 #pragma unroll
   for (int i = 0; i < NV; ++i) {
-    const int c = 4 * (lane + 64 * i);
-    const float r[4] = {v[i].x * inv * ldf(g + c), v[i].y * inv * ldf(g + c + 1),
-                        v[i].z * inv * ldf(g + c + 2), v[i].w * inv * ldf(g + c + 3)};
+    const int j = tid + 256 * i;
+    if (j >= nv4) continue;
+    const int c = 4 * j;
+    const float r[4] = {v[i].x * inv * gv[i].x, v[i].y * inv * gv[i].y, v[i].z * inv * gv[i].z,
+                        v[i].w * inv * gv[i].w};
     if constexpr (std::is_same<T, float>::value) {
       *(float4*)((float*)y.hi + (size_t)o * y.ld + c) = make_float4(r[0], r[1], r[2], r[3]);
     } else {
@@ -64,18 +90,20 @@ __global__ void __launch_bounds__(256) norm_kernel(const float* __restrict__ x, 
 template <typename T>
 static hipError_t norm_dispatch(const float* x, int d, const T* g, float eps, const ActOut& y,
                                 int n_rows, int per, int stride, int off, hipStream_t st) {
-  const dim3 grid(ceil_div(n_rows, 4)), block(256);
-  if (d % 256 == 0) {
-    switch (d / 256) {
+  const bool aligned = ((uintptr_t)x & 15) == 0 && ((uintptr_t)g & (sizeof(T) * 4 - 1)) == 0;
+  if (aligned && d % 4 == 0 && d <= 4 * 256 * 8) {
+    const int nv = ceil_div(d / 4, 256);
+    switch (nv) {
 #define NORM_CASE(NV) \
-  case NV: hipLaunchKernelGGL((norm_vec_kernel<T, NV>), grid, block, 0, st, x, d, g, eps, y, n_rows, per, stride, off); return hipGetLastError();
-      NORM_CASE(1) NORM_CASE(2) NORM_CASE(4) NORM_CASE(8) NORM_CASE(12) NORM_CASE(14)
-      NORM_CASE(16) NORM_CASE(20) NORM_CASE(24) NORM_CASE(32)
+  case NV: hipLaunchKernelGGL((norm_vec_kernel<T, NV>), dim3(n_rows), dim3(256), 0, st, x, d, g, eps, y, per, stride, off); return hipGetLastError();
+      NORM_CASE(1) NORM_CASE(2) NORM_CASE(3) NORM_CASE(4) NORM_CASE(5) NORM_CASE(6)
+      NORM_CASE(7) NORM_CASE(8)
 #undef NORM_CASE
       default: break;
     }
   }
-  hipLaunchKernelGGL(norm_kernel<T>, grid, block, 0, st, x, d, g, eps, y, n_rows, per, stride, off);
+  hipLaunchKernelGGL(norm_kernel<T>, dim3(ceil_div(n_rows, 4)), dim3(256), 0, st, x, d, g, eps, y,
+                     n_rows, per, stride, off);
   return hipGetLastError();
 }
 

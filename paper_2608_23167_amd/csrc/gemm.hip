@@ -45,6 +45,18 @@ namespace ssm {
 // ---------------------------------------------------------------------------
 // Epilogue policies
 // ---------------------------------------------------------------------------
+// Eight consecutive row-major elements (16 or 32 bytes, aligned).
+__device__ __forceinline__ void store_row8(float* p, const float (&v)[8]) {
+  *(float4*)p = make_float4(v[0], v[1], v[2], v[3]);
+  *(float4*)(p + 4) = make_float4(v[4], v[5], v[6], v[7]);
+}
+__device__ __forceinline__ void store_row8(bf16_t* p, const float (&v)[8]) {
+  uint16_t h[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) h[e] = f2bf(v[e]);
+  *(u32x4_t*)p = *(const u32x4_t*)h;
+}
+
 template <typename T>
 struct PolQKV {
   static constexpr bool PAIRED = true;
@@ -82,6 +94,34 @@ struct PolQKV {
     stf(dst + i, vlo);
     stf(dst + i + dh / 2, vhi);
   }
+  // columns c0 .. c0 + 7 of both halves (c0 a multiple of 8)
+  __device__ __forceinline__ void store8(int m, int t, int c0, int BN, const float (&vlo)[8],
+                                         const float (&vhi)[8]) const {
+    const int head = t / tiles_per_head, sub = t % tiles_per_head;
+    const int i0 = sub * (BN / 2) + c0;
+    const int s = m / n_rows, row = m % n_rows;
+    float a[8], b[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      a[e] = vlo[e];
+      b[e] = vhi[e];
+    }
+    if (head < H + Hkv) {
+      const float2* cs = rope + (size_t)row * (dh / 2) + i0;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float2 r = cs[e];
+        a[e] = vlo[e] * r.x - vhi[e] * r.y;
+        b[e] = vhi[e] * r.x + vlo[e] * r.y;
+      }
+    }
+    T* dst;
+    if (head < H) dst = q + (((size_t)s * H + head) * n_rows + row) * dh;
+    else if (head < H + Hkv) dst = kc + (((size_t)s * Hkv + (head - H)) * cap + n_cached + row) * dh;
+    else dst = vc + (((size_t)s * Hkv + (head - H - Hkv)) * cap + n_cached + row) * dh;
+    store_row8(dst + i0, a);
+    store_row8(dst + i0 + dh / 2, b);
+  }
 };
 
 template <typename T>
@@ -98,6 +138,13 @@ struct PolSwiGLU {
     const float silu = g / (1.0f + expf(-g));
     act.store<T>(m, t * (BN / 2) + c, silu * u);
   }
+  __device__ __forceinline__ void store8(int m, int t, int c0, int BN, const float (&g)[8],
+                                         const float (&u)[8]) const {
+    float v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = g[e] / (1.0f + expf(-g[e])) * u[e];
+    act.store8<T>(m, t * (BN / 2) + c0, v);
+  }
 };
 
 template <typename T>
@@ -113,6 +160,14 @@ struct PolResid {
   __device__ __forceinline__ void store1(int m, int n, float v) const {
     resid[(size_t)m * N + n] += v;
   }
+  __device__ __forceinline__ void store8_1(int m, int n0, const float (&v)[8]) const {
+    float4* p = (float4*)(resid + (size_t)m * N + n0);
+    float4 a = p[0], b = p[1];
+    a.x += v[0]; a.y += v[1]; a.z += v[2]; a.w += v[3];
+    b.x += v[4]; b.y += v[5]; b.z += v[6]; b.w += v[7];
+    p[0] = a;
+    p[1] = b;
+  }
 };
 
 template <typename T>
@@ -127,6 +182,9 @@ struct PolStore {
   }
   __device__ __forceinline__ void store1(int m, int n, float v) const {
     c[(size_t)m * ldc + n] = v;
+  }
+  __device__ __forceinline__ void store8_1(int m, int n0, const float (&v)[8]) const {
+    store_row8(c + (size_t)m * ldc + n0, v);
   }
 };
 
@@ -170,7 +228,6 @@ struct PolLMStats {
     lo = w + (size_t)t * BN * ldb;
     hi = lo + (size_t)(BN / 2) * ldb;
   }
-  __device__ __forceinline__ void store1(int, int, float) const {}
   template <int BM, int BN, int CS>
   __device__ __forceinline__ void tile(const float* Cs, int m0, int M, int t) const {
     const int tid = threadIdx.x;
@@ -220,19 +277,39 @@ __device__ __forceinline__ void tile_epilogue(const Pol& pol, const float* Cs, i
   if constexpr (has_tile<Pol>::value) {
     pol.template tile<BM, BN, CS>(Cs, m0, M, t);
   } else if (part) {
-    for (int idx = tid; idx < BM * BN; idx += blockDim.x) {
-      const int r = idx / BN, c = idx % BN, gm = m0 + r;
-      if (gm < M) part[((size_t)split * M + gm) * ldp + (size_t)t * BN + c] = Cs[r * CS + c];
+    // float32 partial tile, 8 columns per thread
+    for (int idx = tid; idx < BM * (BN / 8); idx += blockDim.x) {
+      const int r = idx / (BN / 8), c0 = (idx % (BN / 8)) * 8, gm = m0 + r;
+      if (gm >= M) continue;
+      float v[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = Cs[r * CS + c0 + e];
+      store_row8(part + ((size_t)split * M + gm) * ldp + (size_t)t * BN + c0, v);
     }
   } else if constexpr (Pol::PAIRED) {
-    for (int idx = tid; idx < BM * (BN / 2); idx += blockDim.x) {
-      const int r = idx / (BN / 2), c = idx % (BN / 2), gm = m0 + r;
-      if (gm < M) pol.store(gm, t, c, BN, Cs[r * CS + c], Cs[r * CS + c + BN / 2]);
+    // 8 columns of each half per thread; 16 consecutive threads take the 16
+    // rows of one row group, which are adjacent chunks of the fragment order
+    constexpr int C8 = BN / 16;
+    for (int idx = tid; idx < BM * C8; idx += blockDim.x) {
+      const int rest = idx >> 4, r = (rest / C8) * 16 + (idx & 15), c0 = (rest % C8) * 8;
+      const int gm = m0 + r;
+      if (gm >= M) continue;
+      float lo[8], hi[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        lo[e] = Cs[r * CS + c0 + e];
+        hi[e] = Cs[r * CS + c0 + BN / 2 + e];
+      }
+      pol.store8(gm, t, c0, BN, lo, hi);
     }
   } else {
-    for (int idx = tid; idx < BM * BN; idx += blockDim.x) {
-      const int r = idx / BN, c = idx % BN, gm = m0 + r;
-      if (gm < M) pol.store1(gm, t * BN + c, Cs[r * CS + c]);
+    for (int idx = tid; idx < BM * (BN / 8); idx += blockDim.x) {
+      const int r = idx / (BN / 8), c0 = (idx % (BN / 8)) * 8, gm = m0 + r;
+      if (gm >= M) continue;
+      float v[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = Cs[r * CS + c0 + e];
+      pol.store8_1(gm, t * BN + c0, v);
     }
   }
 }
@@ -479,27 +556,28 @@ __global__ void __launch_bounds__(256) gemm_f32_kernel(Pol pol, const float* __r
 template <int BN, class Pol>
 __global__ void __launch_bounds__(256) splitk_reduce_kernel(Pol pol, const float* __restrict__ part,
                                                             int ldp, int M, int S, int ntiles) {
+  // one thread per 8 consecutive output columns (of each half, when paired)
   const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if constexpr (Pol::PAIRED) {
-    const size_t per_row = (size_t)ntiles * (BN / 2);
-    if (idx >= (size_t)M * per_row) return;
-    const int m = idx / per_row, rem = idx % per_row;
-    const int t = rem / (BN / 2), c = rem % (BN / 2);
-    float lo = 0.f, hi = 0.f;
-    for (int s = 0; s < S; ++s) {
-      const float* p = part + ((size_t)s * M + m) * ldp + (size_t)t * BN + c;
-      lo += p[0];
-      hi += p[BN / 2];
+  constexpr int C8 = Pol::PAIRED ? BN / 16 : BN / 8;
+  const size_t per_row = (size_t)ntiles * C8;
+  if (idx >= (size_t)M * per_row) return;
+  const int m = idx / per_row, rem = idx % per_row;
+  const int t = rem / C8, c0 = (rem % C8) * 8;
+  float lo[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  float hi[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  for (int s = 0; s < S; ++s) {
+    const float* p = part + ((size_t)s * M + m) * ldp + (size_t)t * BN + c0;
+    const float4 a = *(const float4*)p, b = *(const float4*)(p + 4);
+    lo[0] += a.x; lo[1] += a.y; lo[2] += a.z; lo[3] += a.w;
+    lo[4] += b.x; lo[5] += b.y; lo[6] += b.z; lo[7] += b.w;
+    if constexpr (Pol::PAIRED) {
+      const float4 c = *(const float4*)(p + BN / 2), d = *(const float4*)(p + BN / 2 + 4);
+      hi[0] += c.x; hi[1] += c.y; hi[2] += c.z; hi[3] += c.w;
+      hi[4] += d.x; hi[5] += d.y; hi[6] += d.z; hi[7] += d.w;
     }
-    pol.store(m, t, c, BN, lo, hi);
-  } else {
-    const size_t per_row = (size_t)ntiles * BN;
-    if (idx >= (size_t)M * per_row) return;
-    const int m = idx / per_row, n = idx % per_row;
-    float v = 0.f;
-    for (int s = 0; s < S; ++s) v += part[((size_t)s * M + m) * ldp + n];
-    pol.store1(m, n, v);
   }
+  if constexpr (Pol::PAIRED) pol.store8(m, t, c0, BN, lo, hi);
+  else pol.store8_1(m, t * BN + c0, lo);
 }
 
 // ---------------------------------------------------------------------------
@@ -553,10 +631,12 @@ static hipError_t launch_bf16(const Pol& pol, const ActIn& a, int M, int K, int 
   hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, PW, SPLIT, Pol>), grid, dim3(512), 0, st, pol,
                      (const bf16_t*)a.hi, a.lo, a.G, M, K / S, mt, S,
                      S > 1 ? ws.part : nullptr, N);
-  if (S > 1) {
-    const size_t total = (size_t)M * N / (Pol::PAIRED ? 2 : 1);
-    hipLaunchKernelGGL((splitk_reduce_kernel<BN, Pol>), dim3((unsigned)((total + 255) / 256)),
-                       dim3(256), 0, st, pol, ws.part, N, M, S, ntiles);
+  if constexpr (!has_tile<Pol>::value) {   // whole-tile epilogues never split K
+    if (S > 1) {
+      const size_t total = (size_t)M * N / 8 / (Pol::PAIRED ? 2 : 1);
+      hipLaunchKernelGGL((splitk_reduce_kernel<BN, Pol>), dim3((unsigned)((total + 255) / 256)),
+                         dim3(256), 0, st, pol, ws.part, N, M, S, ntiles);
+    }
   }
   return hipGetLastError();
 }
@@ -601,7 +681,7 @@ static hipError_t run_f32(const Pol& pol, const ActIn& a, int M, int K, int N, S
   hipLaunchKernelGGL((gemm_f32_kernel<Pol>), grid, dim3(256), 0, st, pol, (const float*)a.hi,
                      a.ld, M, K / S, S > 1 ? ws.part : nullptr, N);
   if (S > 1) {
-    const size_t total = (size_t)M * N / (Pol::PAIRED ? 2 : 1);
+    const size_t total = (size_t)M * N / 8 / (Pol::PAIRED ? 2 : 1);
     hipLaunchKernelGGL((splitk_reduce_kernel<BN, Pol>), dim3((unsigned)((total + 255) / 256)),
                        dim3(256), 0, st, pol, ws.part, N, M, S, ntiles);
   }

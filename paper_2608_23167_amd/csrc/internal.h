@@ -104,6 +104,26 @@ struct ActOut {
       if (lo) lo[i] = f2bf(v - bf2f(h));
     }
   }
+  // columns k .. k + 7 of row m, k a multiple of 8: one chunk of the fragment
+  // order, so one 16-byte store per part
+  template <typename T>
+  __device__ __forceinline__ void store8(int m, int k, const float (&v)[8]) const {
+    if constexpr (std::is_same<T, float>::value) {
+      float* p = (float*)hi + (size_t)m * ld + k;
+      *(float4*)p = make_float4(v[0], v[1], v[2], v[3]);
+      *(float4*)(p + 4) = make_float4(v[4], v[5], v[6], v[7]);
+    } else {
+      const size_t i = frag_index(m, k, G);
+      uint16_t h[8], l[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        h[e] = f2bf(v[e]);
+        l[e] = f2bf(v[e] - bf2f(h[e]));
+      }
+      *(u32x4_t*)((bf16_t*)hi + i) = *(const u32x4_t*)h;
+      if (lo) *(u32x4_t*)(lo + i) = *(const u32x4_t*)l;
+    }
+  }
 };
 
 // RMSNorm of float32 rows into a projection operand: output row o reads

@@ -334,6 +334,19 @@ __device__ __forceinline__ void tile_of(int w, int total, int ntm, int mt, int& 
   tm = t % mt;
 }
 
+// K-step handover between the two kinds of waves.  The buffer schedule below
+// never lets a compute wave read an LDS buffer in the step in which it is
+// rewritten, so the compute waves pass the barrier without waiting for their
+// own outstanding LDS reads (the fence of __syncthreads would wait for them);
+// the staging waves wait for their LDS writes to land first.  The empty asm
+// statements keep the compiler from moving memory accesses across.
+__device__ __forceinline__ void lds_handover_barrier() {
+  asm volatile("s_barrier" ::: "memory");
+}
+__device__ __forceinline__ void lds_written_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 // Warp-specialised workgroup of 8 waves, BM = 128 rows x BN columns.
 //  * Waves 4-7 ("staging") stream the weight tile of each K-step (BN rows x 64
 //    k, the HBM-bound stream) through a ring of 4 register stages into a ring
@@ -361,7 +374,7 @@ __global__ void __launch_bounds__(512) gemm_bf16_kernel(Pol pol, const bf16_t* _
   constexpr int NA = SPLIT ? 2 : 1;
   constexpr int WR = BN / 32;                    // weight rows per staging thread per stage
   constexpr int NBUF = 3;                        // LDS weight buffers
-  (void)PW;
+  static_assert(PW == 4 || PW == 8, "weight register ring of 4 or 8 K-steps");
   constexpr int BUF_ELEMS = BN * LS;
   constexpr int SMEM_W = NBUF * BUF_ELEMS * 2;
   constexpr int CS = BN + 4;
@@ -433,7 +446,7 @@ __global__ void __launch_bounds__(512) gemm_bf16_kernel(Pol pol, const bf16_t* _
     READ_W(wf0, (kt_ + 1) % NBUF, 0);                                                 \
     MFMA_H(RA, wf1, 1);                                                               \
     LOAD_A(RA, min(kt_ + 2, last));                                                   \
-    __syncthreads();                                                                  \
+    lds_handover_barrier();                                                           \
   } while (0)
 
     LOAD_A(a0, 0);
@@ -467,7 +480,7 @@ __global__ void __launch_bounds__(512) gemm_bf16_kernel(Pol pol, const bf16_t* _
       const int r = r0 + 32 * i;   // tile rows [0, BN/2) come from lo, the rest from hi
       w_src[i] = (r < BN / 2 ? blo + (size_t)r * pol.ldb : bhi + (size_t)(r - BN / 2) * pol.ldb) + kbeg + col;
     }
-    u32x4_t s0[WR], s1[WR], s2[WR], s3[WR];      // weight stage s in set s % 4
+    u32x4_t s0[WR], s1[WR], s2[WR], s3[WR], s4[WR], s5[WR], s6[WR], s7[WR];   // stage s in set s % PW
 #define LOAD_S(S, KT)                                                                 \
   do {                                                                                \
     _Pragma("unroll") for (int i = 0; i < WR; ++i) S[i] = *(const u32x4_t*)(w_src[i] + (KT) * BK); \
@@ -479,28 +492,47 @@ __global__ void __launch_bounds__(512) gemm_bf16_kernel(Pol pol, const bf16_t* _
   } while (0)
     // during step kt the compute waves read buffers kt % 3 and (kt + 1) % 3;
     // the staging waves fill buffer (kt + 2) % 3 with stage kt + 2 and fetch
-    // stage kt + 6 into the register set it came from
+    // stage kt + 2 + PW into the register set it came from
 #define SSTEP(KT, S)                                                                  \
   do {                                                                                \
     STORE_S(S, ((KT) + 2) % NBUF);                                                    \
-    LOAD_S(S, min((KT) + 6, last));                                                   \
-    __syncthreads();                                                                  \
+    LOAD_S(S, min((KT) + 2 + PW, last));                                              \
+    lds_written_barrier();                                                            \
   } while (0)
 
     LOAD_S(s0, 0);
     LOAD_S(s1, min(1, last));
     LOAD_S(s2, min(2, last));
     LOAD_S(s3, min(3, last));
+    if constexpr (PW == 8) {
+      LOAD_S(s4, min(4, last));
+      LOAD_S(s5, min(5, last));
+      LOAD_S(s6, min(6, last));
+      LOAD_S(s7, min(7, last));
+    }
     STORE_S(s0, 0);
     STORE_S(s1, 1);
-    LOAD_S(s0, min(4, last));
-    LOAD_S(s1, min(5, last));
+    LOAD_S(s0, min(PW, last));
+    LOAD_S(s1, min(PW + 1, last));
     __syncthreads();                               // weight stages 0 and 1 are in LDS
-    for (int kt = 0; kt < nk; kt += 4) {
-      SSTEP(kt, s2);
-      SSTEP(kt + 1, s3);
-      SSTEP(kt + 2, s0);
-      SSTEP(kt + 3, s1);
+    if constexpr (PW == 8) {
+      for (int kt = 0; kt < nk; kt += 8) {         // nk is a multiple of 8 (host-checked)
+        SSTEP(kt, s2);
+        SSTEP(kt + 1, s3);
+        SSTEP(kt + 2, s4);
+        SSTEP(kt + 3, s5);
+        SSTEP(kt + 4, s6);
+        SSTEP(kt + 5, s7);
+        SSTEP(kt + 6, s0);
+        SSTEP(kt + 7, s1);
+      }
+    } else {
+      for (int kt = 0; kt < nk; kt += 4) {
+        SSTEP(kt, s2);
+        SSTEP(kt + 1, s3);
+        SSTEP(kt + 2, s0);
+        SSTEP(kt + 3, s1);
+      }
     }
 #undef LOAD_S
 #undef STORE_S
@@ -592,7 +624,8 @@ size_t gemm_split_ws_floats(int M, int max_n) {
 }
 
 // Per-projection launch choice: tile width BN (64, 96 or 128), split-K S
-// (0 = automatic) and weight prefetch depth PW.
+// (0 = automatic) and the depth PW (4 or 8 K-steps) of the staging waves'
+// register ring of weight loads.
 struct GemmCfg {
   int bn, s, pw;
 };
@@ -645,10 +678,11 @@ template <int BN, class Pol>
 static hipError_t launch_bf16_pw(const Pol& pol, const ActIn& a, int M, int K, int N, int S,
                                  int pw, SplitWs ws, hipStream_t st) {
   const bool split = a.lo != nullptr;
-  // the kernel's K loop is unrolled by 4: nk = K / S / 64 must be a multiple of 4
-  if (pw <= 2)
-    return split ? launch_bf16<BN, 2, true>(pol, a, M, K, N, S, ws, st)
-                 : launch_bf16<BN, 2, false>(pol, a, M, K, N, S, ws, st);
+  // the staging loop is unrolled by the ring depth: nk = K / S / 64 must be a
+  // multiple of it (of 4 always, host-checked)
+  if (pw >= 8 && (K / S / 64) % 8 == 0)
+    return split ? launch_bf16<BN, 8, true>(pol, a, M, K, N, S, ws, st)
+                 : launch_bf16<BN, 8, false>(pol, a, M, K, N, S, ws, st);
   return split ? launch_bf16<BN, 4, true>(pol, a, M, K, N, S, ws, st)
                : launch_bf16<BN, 4, false>(pol, a, M, K, N, S, ws, st);
 }

@@ -2,7 +2,8 @@
 // followed by the rows' own keys), with grouped-query heads.
 //
 // bfloat16 path (head_dim 128): one workgroup = 4 waves = 64 query rows of one
-// (sequence, head); keys stream through LDS in tiles of 64.  Each wave
+// (sequence, head); keys stream through two LDS tile buffers of 64 keys, the
+// next tile's loads in flight while the current one is used.  Each wave
 // computes S^T = K Q^T with v_mfma_f32_16x16x32_bf16 so that a lane ends up
 // holding 4 consecutive keys of one query: the exponentiated scores are then
 // already in the operand layout of the P V product, which is computed as
@@ -16,13 +17,21 @@ namespace ssm {
 
 constexpr float LOG2E = 1.4426950408889634f;
 
+// V^T tile in LDS as 32-bit words: word (d, p) holds keys 2p and 2p + 1 of
+// head dimension d.  The key-pair index is XOR-swizzled by 2 * (d / 16), which
+// keeps pairs 2j, 2j + 1 adjacent (8-byte reads stay aligned) and spreads the
+// transposing writes of a wave over all 64 banks.
+__device__ __forceinline__ int vt_word(int d, int p) { return d * 36 + (p ^ ((d >> 4) << 1)); }
+
 __global__ void __launch_bounds__(256) attn_bf16_kernel(
     const bf16_t* __restrict__ Q, const bf16_t* __restrict__ Kc, const bf16_t* __restrict__ Vc,
     int H, int Hkv, int Mq, int Nk, int cap, int keys_per_split, float scale_log2,
     ActOut O, float* __restrict__ Opart, float* __restrict__ ML) {
-  constexpr int DH = 128, KT = 64, KS = DH + 8, VS = KT + 8;
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[KT * KS];
-  __shared__ __attribute__((aligned(16))) bf16_t Vt[DH * VS];
+  constexpr int DH = 128, KT = 64, KS = DH + 8, VW = 36;    // VW: words per V^T row
+  constexpr int KBUF = KT * KS, VBUF = DH * VW;
+  // two tile buffers: tile i is written while tile i - 1 is read
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[2 * KBUF];
+  __shared__ __attribute__((aligned(16))) uint32_t Vt[2 * VBUF];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, c16 = lane & 15;
   const int bh = blockIdx.y, s = bh / H, h = bh % H, kvh = h / (H / Hkv);
@@ -35,35 +44,66 @@ __global__ void __launch_bounds__(256) attn_bf16_kernel(
 #pragma unroll
   for (int kk = 0; kk < 4; ++kk) {
     if (q < Mq) qf[kk] = *(const bf16x8_t*)(Qh + (size_t)q * DH + 32 * kk + 8 * g);
-    else {
-      uint4 z = {0u, 0u, 0u, 0u};
-      qf[kk] = __builtin_bit_cast(bf16x8_t, z);
-    }
+    else qf[kk] = __builtin_bit_cast(bf16x8_t, u32x4_t{0u, 0u, 0u, 0u});
   }
   const bf16_t* Kh = Kc + (size_t)(s * Hkv + kvh) * cap * DH;
   const bf16_t* Vh = Vc + (size_t)(s * Hkv + kvh) * cap * DH;
+
+  // tile loader: thread part i covers key (tid + 256 i) / 16 of the tile and
+  // head-dimension chunk (tid % 16) * 8; keys past the range load as zero
+  u32x4_t kr[4], vr[4];
+  auto load_tile = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int key = (tid + 256 * i) >> 4, d8 = tid & 15;
+      kr[i] = u32x4_t{0u, 0u, 0u, 0u};
+      vr[i] = kr[i];
+      if (k0 + key < ke) {
+        kr[i] = *(const u32x4_t*)(Kh + (size_t)(k0 + key) * DH + d8 * 8);
+        vr[i] = *(const u32x4_t*)(Vh + (size_t)(k0 + key) * DH + d8 * 8);
+      }
+    }
+  };
+  // K rows as they are; V transposed into key-pair words: lanes l and l ^ 16
+  // hold the same chunk of keys 2p and 2p + 1, swap halves, and each writes
+  // four words (the even key's lane dimensions 0-3, the odd key's 4-7)
+  auto store_tile = [&](int buf) {
+    bf16_t* kd = Ks + buf * KBUF;
+    uint32_t* vd = Vt + buf * VBUF;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int key = (tid + 256 * i) >> 4, d8 = tid & 15;
+      *(u32x4_t*)(kd + key * KS + d8 * 8) = kr[i];
+      const bool odd = (lane >> 4) & 1;
+      u32x4_t other;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) other[e] = __shfl_xor(vr[i][e], 16, 64);
+      const u32x4_t lo = odd ? other : vr[i], hi = odd ? vr[i] : other;   // even key, odd key
+      const int p = key >> 1, d0 = d8 * 8 + (odd ? 4 : 0);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int dd = (odd ? 4 : 0) + e;   // dimension within the chunk
+        const uint32_t a = dd & 1 ? lo[dd >> 1] >> 16 : lo[dd >> 1] & 0xffffu;
+        const uint32_t b = dd & 1 ? hi[dd >> 1] >> 16 : hi[dd >> 1] & 0xffffu;
+        vd[vt_word(d0 + e, p)] = a | (b << 16);
+      }
+    }
+  };
 
   f32x4_t o[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) o[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_run = 0.f;
 
-  for (int k0 = kb; k0 < ke; k0 += KT) {
+  if (kb < ke) load_tile(kb);
+  int buf = 0;
+  for (int k0 = kb; k0 < ke; k0 += KT, buf ^= 1) {
+    // buffer `buf` was last read two tiles ago, before the previous barrier
+    store_tile(buf);
+    if (k0 + KT < ke) load_tile(k0 + KT);   // in flight during this tile
     __syncthreads();
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int c = tid + 256 * i, key = c >> 4, d8 = c & 15;
-      uint4 kv = {0u, 0u, 0u, 0u}, vv = {0u, 0u, 0u, 0u};
-      if (k0 + key < ke) {
-        kv = *(const uint4*)(Kh + (size_t)(k0 + key) * DH + d8 * 8);
-        vv = *(const uint4*)(Vh + (size_t)(k0 + key) * DH + d8 * 8);
-      }
-      *(uint4*)(Ks + key * KS + d8 * 8) = kv;
-      const bf16_t* ve = (const bf16_t*)&vv;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) Vt[(d8 * 8 + e) * VS + key] = ve[e];
-    }
-    __syncthreads();
+    const bf16_t* kd = Ks + buf * KBUF;
+    const uint32_t* vd = Vt + buf * VBUF;
 
     // S^T block nb: sc[nb][r] = score(key 16nb + 4g + r, query c16)
     f32x4_t sc[4];
@@ -72,7 +112,7 @@ __global__ void __launch_bounds__(256) attn_bf16_kernel(
       sc[nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) {
-        const bf16x8_t a = *(const bf16x8_t*)(Ks + (16 * nb + c16) * KS + 32 * kk + 8 * g);
+        const bf16x8_t a = *(const bf16x8_t*)(kd + (16 * nb + c16) * KS + 32 * kk + 8 * g);
         sc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[kk], sc[nb], 0, 0, 0);
       }
     }
@@ -105,17 +145,17 @@ __global__ void __launch_bounds__(256) attn_bf16_kernel(
         l_run += p;
         tmp[e] = f2bf(p);
       }
-      pb[h2] = __builtin_bit_cast(bf16x8_t, *(const uint4*)tmp);
+      pb[h2] = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)tmp);
     }
+    // V^T operand: row 16db + c16, keys 32h2 + 4g .. + 3 and 32h2 + 16 + 4g .. + 3
 #pragma unroll
     for (int h2 = 0; h2 < 2; ++h2) {
 #pragma unroll
       for (int db = 0; db < 8; ++db) {
-        const bf16_t* vr = Vt + (16 * db + c16) * VS + 32 * h2 + 4 * g;
-        uint4 a4;
-        const uint2 lo = *(const uint2*)vr;
-        const uint2 hi = *(const uint2*)(vr + 16);
-        a4.x = lo.x; a4.y = lo.y; a4.z = hi.x; a4.w = hi.y;
+        const int d = 16 * db + c16;
+        const uint2 lo = *(const uint2*)(vd + vt_word(d, 16 * h2 + 2 * g));
+        const uint2 hi = *(const uint2*)(vd + vt_word(d, 16 * h2 + 8 + 2 * g));
+        const u32x4_t a4 = {lo.x, lo.y, hi.x, hi.y};
         o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a4), pb[h2],
                                                         o[db], 0, 0, 0);
       }
@@ -198,29 +238,34 @@ __global__ void __launch_bounds__(64) attn_f32_kernel(
   }
 }
 
-// Combines the splits of one (sequence, head, query) row, in split order.
+// Combines the splits of one (sequence, head, query) row, in split order;
+// thread (row, c8) produces head dimensions 8 c8 .. 8 c8 + 7 of the row.
 template <typename T>
-__global__ void attn_merge_kernel(const float* __restrict__ Opart, const float* __restrict__ ML,
-                                  int S, int BH, int H, int Mq, int DH, ActOut O) {
-  const int row = blockIdx.x;               // over BH * Mq
+__global__ void __launch_bounds__(256) attn_merge_kernel(const float* __restrict__ Opart,
+                                                         const float* __restrict__ ML, int S,
+                                                         int BH, int H, int Mq, int DH, ActOut O) {
+  const int c8n = DH / 8;
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= BH * Mq * c8n) return;
+  const int row = idx / c8n, c0 = (idx % c8n) * 8;   // row over BH * Mq
   const int bh = row / Mq, q = row % Mq, s = bh / H, h = bh % H;
   float M = -INFINITY;
   for (int i = 0; i < S; ++i) M = fmaxf(M, ML[((size_t)i * BH * Mq + row) * 2]);
-  float L = 0.f;
+  float L = 0.f, acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   for (int i = 0; i < S; ++i) {
     const size_t r = (size_t)i * BH * Mq + row;
     const float l = ML[r * 2 + 1];
-    if (l > 0.f) L += l * exp2f(ML[r * 2] - M);
+    if (!(l > 0.f)) continue;
+    const float w = exp2f(ML[r * 2] - M);
+    L += l * w;
+    const float4 a = *(const float4*)(Opart + r * DH + c0), b = *(const float4*)(Opart + r * DH + c0 + 4);
+    acc[0] += a.x * w; acc[1] += a.y * w; acc[2] += a.z * w; acc[3] += a.w * w;
+    acc[4] += b.x * w; acc[5] += b.y * w; acc[6] += b.z * w; acc[7] += b.w * w;
   }
   const float inv = 1.0f / L;
-  for (int c = threadIdx.x; c < DH; c += blockDim.x) {
-    float acc = 0.f;
-    for (int i = 0; i < S; ++i) {
-      const size_t r = (size_t)i * BH * Mq + row;
-      if (ML[r * 2 + 1] > 0.f) acc += Opart[r * DH + c] * exp2f(ML[r * 2] - M);
-    }
-    O.store<T>(s * Mq + q, h * DH + c, acc * inv);
-  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) acc[e] *= inv;
+  O.store8<T>(s * Mq + q, h * DH + c0, acc);
 }
 
 hipError_t attention(int dtype, const void* q, const void* kc, const void* vc, int B, int H,
@@ -229,11 +274,15 @@ hipError_t attention(int dtype, const void* q, const void* kc, const void* vc, i
   if (Mq == 0) return hipSuccess;
   const int BH = B * H;
   const int qtiles = ceil_div(Mq, 64);
-  // split the key range until the grid covers the chip twice over, in whole
-  // 64-key tiles, never leaving a split without keys
-  int S = 1;
+  // split the key range (whole 64-key tiles) until every split has about two
+  // tiles or the grid reaches two workgroups per CU: each workgroup walks its
+  // tiles in sequence and hides only the next tile's load, so short ranges
+  // spread over many workgroups beat long ones
   const int key_tiles = ceil_div(Nk, 64);
-  while (S * 2 <= ws.max_splits && qtiles * BH * S < 512 && S * 2 <= key_tiles) S *= 2;
+  int S = key_tiles / 2;
+  if (S > ws.max_splits) S = ws.max_splits;
+  if (S > 512 / (qtiles * BH)) S = 512 / (qtiles * BH);
+  if (S < 1) S = 1;
   int kps = ceil_div(key_tiles, S) * 64;
   S = ceil_div(Nk, kps);
   const float scale_log2 = LOG2E / sqrtf((float)dh);
@@ -259,12 +308,13 @@ hipError_t attention(int dtype, const void* q, const void* kc, const void* vc, i
                          cap, kps, scale_log2, of, opart, ws.ml);
   }
   if (S > 1) {
+    const dim3 mgrid(ceil_div(BH * Mq * (dh / 8), 256));
     if (dtype == 1)
-      hipLaunchKernelGGL(attn_merge_kernel<bf16_t>, dim3(BH * Mq), dim3(128), 0, st, ws.opart,
-                         ws.ml, S, BH, H, Mq, dh, out);
+      hipLaunchKernelGGL(attn_merge_kernel<bf16_t>, mgrid, dim3(256), 0, st, ws.opart, ws.ml, S,
+                         BH, H, Mq, dh, out);
     else
-      hipLaunchKernelGGL(attn_merge_kernel<float>, dim3(BH * Mq), dim3(128), 0, st, ws.opart,
-                         ws.ml, S, BH, H, Mq, dh, out);
+      hipLaunchKernelGGL(attn_merge_kernel<float>, mgrid, dim3(256), 0, st, ws.opart, ws.ml, S,
+                         BH, H, Mq, dh, out);
   }
   return hipGetLastError();
 }

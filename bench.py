@@ -15,6 +15,7 @@ profiled replay of the same steps) and the CPU oracle baseline.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import statistics
@@ -29,6 +30,40 @@ BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 FP32_PEAK_TFLOPS = 157.3
 
 METRIC = "denoised tokens/sec + step latency per GPU (LLaDA-8B shape); % MFMA/HBM peak"
+
+# HBM traffic of the dominant kernel per launch, from two rocprofv3 counter
+# runs of this script on the same workload (FETCH_SIZE, then WRITE_SIZE, KiB
+# per dispatch averaged over the kernel's dispatches), each scaled by known
+# bytes / counter reading for a plain device copy.  The entry is valid only
+# for the kernel sources it was measured on (sha256 of the GEMM sources).
+TRAFFIC = {
+    # rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE over `bench.py --steps 32 --warmup 1
+    # --no-profile --no-cpu-baseline`; per-dispatch means of the block-start
+    # launches (180299.2 / 18048.0 KiB) and the cached ones (106571.0 / 5760.0
+    # KiB), weighted 1:31 as in the generation schedule; copy kernel:
+    # 268435456 bytes read and written per launch read as 131085.1 KiB fetched
+    # and 262144.0 KiB written
+    ("llada_gen256", "gemm_gate_up"): {
+        "sources_sha256": "d2106e91db15dfc119eec80de3d694921b7feaef98d22f5b5254d348dac21900",
+        "fetch_kib": (180299.2 + 31 * 106571.0) / 32, "write_kib": (18048.0 + 31 * 5760.0) / 32,
+        "fetch_scale": 262144.0 / 131085.1, "write_scale": 1.0},
+}
+GEMM_SOURCES = ("gemm.hip", "internal.h", "common.h")
+
+
+def gemm_sources_sha256():
+    h = hashlib.sha256()
+    for f in GEMM_SOURCES:
+        with open(os.path.join(ROOT, "paper_2608_23167_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload, kernel):
+    t = TRAFFIC.get((workload, kernel))
+    if not t or t["sources_sha256"] != gemm_sources_sha256():
+        return None
+    return round((t["fetch_kib"] * t["fetch_scale"] + t["write_kib"] * t["write_scale"]) * 1024)
 
 
 def gemm_work(shape, tag, M):
@@ -59,8 +94,12 @@ def main():
     ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--workload", default="llada_gen256")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-layers", type=int, default=2,
-                    help="layers of the CPU oracle sample (extrapolated to the model depth)")
+    ap.add_argument("--no-profile", action="store_true",
+                    help="skip the profiled replay (per-kernel times and roofline), e.g. under counter collection")
+    ap.add_argument("--cpu-layers", type=int, default=None,
+                    help="layers of the CPU oracle sample (default: all; fewer are extrapolated)")
+    ap.add_argument("--cpu-reps", type=int, default=4,
+                    help="repetitions of each layer of the CPU oracle sample")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -123,11 +162,14 @@ def main():
     print(f"[bench] {K} steps in {wall:.3f} s -> {value:.1f} tokens/s", file=sys.stderr, flush=True)
 
     # profiled replay of the same steps: per-launch HIP events in the library
-    ssm_profile_enable(True)
-    run(K)
-    torch.cuda.synchronize()
-    prof = {t: ssm_profile_query(t) for t in PROFILE_TAGS}
-    ssm_profile_enable(False)
+    prof = {t: (0, 0.0) for t in PROFILE_TAGS}
+    if not args.no_profile:
+        ssm_profile_enable(True)
+        run(K)
+        torch.cuda.synchronize()
+        prof = {t: ssm_profile_query(t) for t in PROFILE_TAGS}
+        main_kernel = {t: ssm_profile_query(t, 0) for t in PROFILE_TAGS}
+        ssm_profile_enable(False)
     dom = max(prof, key=lambda t: prof[t][1])
     # algorithmic work of the dominant kernel over the replay
     from paper_2608_23167_amd.api import ssm_select_count
@@ -143,9 +185,10 @@ def main():
             b_, f_ = gemm_work(shape, dom, Mo if dom == "gemm_lm_head" else M)
             tot_bytes += reps * b_
             tot_flops += reps * f_
-    n_launch, dom_ms = prof[dom]
+    # the dominant operation's main kernel (split-K reductions excluded)
+    n_launch, dom_ms = main_kernel[dom] if not args.no_profile else (0, 0.0)
     roof = None
-    if tot_bytes > 0:
+    if tot_bytes > 0 and n_launch > 0:
         gbs = tot_bytes / (dom_ms * 1e-3) / 1e9
         tfl = tot_flops / (dom_ms * 1e-3) / 1e12
         intensity = tot_flops / tot_bytes
@@ -158,7 +201,7 @@ def main():
                     "unit": "TFLOP/s", "frac": round(tfl / BF16_PEAK_TFLOPS, 4)}
         roof.update({"kernel": dom, "launches": n_launch, "avg_launch_us": round(dom_ms / n_launch * 1e3, 2),
                      "algorithmic_bytes_per_launch": round(tot_bytes / n_launch),
-                     "mfma_tflops": round(tfl, 1), "traffic": None})
+                     "mfma_tflops": round(tfl, 1), "traffic": measured_traffic(wl.name, dom)})
 
     result = {
         "metric": METRIC,
@@ -189,14 +232,16 @@ def main():
     print(f"[bench] profile: {result['kernel_ms_per_step']}", file=sys.stderr, flush=True)
 
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(wl, mw, dec, args.cpu_layers)
+        result["cpu_baseline"] = cpu_baseline(wl, mw, dec, args.cpu_layers or wl.model.n_layers,
+                                              args.cpu_reps)
     print(json.dumps(result), flush=True)
 
 
-def cpu_baseline(wl, mw, dec, n_layers_sample):
+def cpu_baseline(wl, mw, dec, n_layers_sample, reps):
     """The oracle, untuned, on a bounded sample: one cached step at block 0 with
-    `n_layers_sample` layers plus the LM head and statistics, extrapolated to
-    the model depth and converted to tokens/s."""
+    `n_layers_sample` layers (each run `reps` times on the same input, the mean
+    kept) plus the LM head and statistics, extrapolated to the model depth if
+    fewer layers are sampled, and converted to tokens/s."""
     import numpy as np
     import oracle.generate as OG
     import oracle.model as OM
@@ -220,6 +265,7 @@ def cpu_baseline(wl, mw, dec, n_layers_sample):
     t0 = time.perf_counter()
     x = OE.embed_rows(w.tok_emb, tokens[0], rows.pos, rows.region, pred, predw, ps, -1,
                       wl.alpha, shape.mask_id)
+    t_embed = time.perf_counter() - t0
     prefix = None
     if wl.cache:
         n_pre = wl.prompt_len
@@ -227,25 +273,26 @@ def cpu_baseline(wl, mw, dec, n_layers_sample):
         prefix = [(rng.standard_normal((n_pre, shape.n_kv_heads, shape.head_dim)).astype(np.float32),
                    rng.standard_normal((n_pre, shape.n_kv_heads, shape.head_dim)).astype(np.float32))
                   for _ in range(n_layers_sample)]
-    t_embed = time.perf_counter() - t0
     t_layers = 0.0
     for l in range(n_layers_sample):
         lw = w.layers[l]                      # conversion outside the timed part
-        t0 = time.perf_counter()
         kp, vp = prefix[l] if prefix else (None, None)
-        x = OM.layer_forward(x, rows.pos, lw, shape, kp, vp).x
-        t_layers += time.perf_counter() - t0
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            y = OM.layer_forward(x, rows.pos, lw, shape, kp, vp).x
+        t_layers += (time.perf_counter() - t0) / reps
+        x = y
     t0 = time.perf_counter()
     OM.output_stats(x[rows.first_out_row:], w, shape, wl.topk)
     t_head = time.perf_counter() - t0
     step_s = t_embed + t_layers / n_layers_sample * shape.n_layers + t_head
-    sample_s = t_embed + t_layers + t_head
+    sample_s = t_embed + t_layers * reps + t_head
     return {"value": round(wl.n_per_step * wl.batch / step_s, 5), "unit": "tokens/s",
             "cores": threads, "kind": "oracle",
             "sample": (f"one cached step of {wl.name} at block 0 ({len(rows.pos)} rows): "
-                       f"{n_layers_sample} of {shape.n_layers} layers + LM head and row statistics "
-                       f"in float32 NumPy ({sample_s:.1f} s), layers extrapolated to "
-                       f"{shape.n_layers} -> {step_s:.1f} s per step"),
+                       f"{n_layers_sample} of {shape.n_layers} layers (each timed {reps}x, mean) "
+                       f"+ LM head and row statistics in float32 NumPy ({sample_s:.1f} s of CPU "
+                       f"work) -> {step_s:.2f} s per step"),
             "step_seconds": round(step_s, 3)}
 
 

@@ -266,18 +266,21 @@ int32_t ssm_unmask(int32_t* d_tokens, int32_t batch, int32_t seq_len, int32_t bl
 /* ------------------------------------------------------------------------ */
 
 /*
- * on != 0: from now on every kernel launcher of the calls above is bracketed
- * by a pair of HIP events recorded on the call's stream, under a tag naming
- * the operation ("select", "embed", "rope_table", "norm", "gemm_qkv",
- * "attention", "gemm_o", "gemm_gate_up", "gemm_down", "gemm_lm_head",
- * "rowstats", "unmask").  Each call discards earlier records.  Not
- * thread-safe; meant for a single profiling thread.
+ * on != 0: from now on every kernel launched by the calls above is
+ * bracketed by a pair of HIP events on the call's stream (created without
+ * the system-scope fence), recorded under a tag naming the operation ("select", "embed",
+ * "rope_table", "norm", "gemm_qkv", "attention", "gemm_o", "gemm_gate_up",
+ * "gemm_down", "gemm_lm_head", "rowstats", "unmask") and the kernel's
+ * ordinal within one call of that operation (0 = the main kernel; split-K
+ * reductions and merges come after).  Each call discards earlier records.
+ * Not thread-safe; meant for a single profiling thread.
  */
 int32_t ssm_profile_enable(int32_t on);
 
-/* Number of recorded launches under `tag` and their summed duration in
- * milliseconds; waits for the recorded events to complete. */
-int32_t ssm_profile_query(const char* tag, int32_t* count, double* total_ms);
+/* Number of recorded kernels under `tag` (all ordinals if kernel < 0, else
+ * only that ordinal) and their summed duration in milliseconds; waits for
+ * the recorded events to complete. */
+int32_t ssm_profile_query(const char* tag, int32_t kernel, int32_t* count, double* total_ms);
 
 /* Message of the last error on this thread ("" if none). */
 const char* ssm_last_error(void);

@@ -68,7 +68,7 @@ _SIGS = {
     "ssm_unmask": (I32, [P, I32, I32, I32, I32, I32, I32, I32, C.c_float, P, P, P, P, I32, I32, P,
                          I32, P, P, P, P, P, P]),
     "ssm_profile_enable": (I32, [I32]),
-    "ssm_profile_query": (I32, [C.c_char_p, PI32, C.POINTER(C.c_double)]),
+    "ssm_profile_query": (I32, [C.c_char_p, I32, PI32, C.POINTER(C.c_double)]),
     "ssm_last_error": (C.c_char_p, []),
 }
 

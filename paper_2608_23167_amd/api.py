@@ -131,7 +131,10 @@ def ssm_profile_enable(on: bool) -> None:
     check(lib().ssm_profile_enable(int(bool(on))), "ssm_profile_enable")
 
 
-def ssm_profile_query(tag: str) -> Tuple[int, float]:
+def ssm_profile_query(tag: str, kernel: int = -1) -> Tuple[int, float]:
+    """(kernels recorded, summed ms) under `tag`; kernel >= 0 selects one
+    ordinal within each call (0 = the operation's main kernel)."""
     n, ms = C.c_int32(), C.c_double()
-    check(lib().ssm_profile_query(tag.encode(), C.byref(n), C.byref(ms)), "ssm_profile_query")
+    check(lib().ssm_profile_query(tag.encode(), int(kernel), C.byref(n), C.byref(ms)),
+          "ssm_profile_query")
     return n.value, ms.value

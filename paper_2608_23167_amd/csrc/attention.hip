@@ -289,7 +289,7 @@ hipError_t attention(int dtype, const void* q, const void* kc, const void* vc, i
   dim3 grid(qtiles, BH, S);
   float* opart = S > 1 ? ws.opart : nullptr;
   if (dtype == 1) {
-    hipLaunchKernelGGL(attn_bf16_kernel, grid, dim3(256), 0, st, (const bf16_t*)q,
+    launch(attn_bf16_kernel, grid, dim3(256), 0, st, (const bf16_t*)q,
                        (const bf16_t*)kc, (const bf16_t*)vc, H, Hkv, Mq, Nk, cap, kps, scale_log2,
                        out, opart, ws.ml);
   } else {
@@ -298,22 +298,22 @@ hipError_t attention(int dtype, const void* q, const void* kc, const void* vc, i
     const float* vf = (const float*)vc;
     const ActOut& of = out;
     if (dh == 32)
-      hipLaunchKernelGGL(attn_f32_kernel<32>, grid, dim3(64), 0, st, qf, kf, vf, H, Hkv, Mq, Nk,
+      launch(attn_f32_kernel<32>, grid, dim3(64), 0, st, qf, kf, vf, H, Hkv, Mq, Nk,
                          cap, kps, scale_log2, of, opart, ws.ml);
     else if (dh == 64)
-      hipLaunchKernelGGL(attn_f32_kernel<64>, grid, dim3(64), 0, st, qf, kf, vf, H, Hkv, Mq, Nk,
+      launch(attn_f32_kernel<64>, grid, dim3(64), 0, st, qf, kf, vf, H, Hkv, Mq, Nk,
                          cap, kps, scale_log2, of, opart, ws.ml);
     else
-      hipLaunchKernelGGL(attn_f32_kernel<128>, grid, dim3(64), 0, st, qf, kf, vf, H, Hkv, Mq, Nk,
+      launch(attn_f32_kernel<128>, grid, dim3(64), 0, st, qf, kf, vf, H, Hkv, Mq, Nk,
                          cap, kps, scale_log2, of, opart, ws.ml);
   }
   if (S > 1) {
     const dim3 mgrid(ceil_div(BH * Mq * (dh / 8), 256));
     if (dtype == 1)
-      hipLaunchKernelGGL(attn_merge_kernel<bf16_t>, mgrid, dim3(256), 0, st, ws.opart, ws.ml, S,
+      launch(attn_merge_kernel<bf16_t>, mgrid, dim3(256), 0, st, ws.opart, ws.ml, S,
                          BH, H, Mq, dh, out);
     else
-      hipLaunchKernelGGL(attn_merge_kernel<float>, mgrid, dim3(256), 0, st, ws.opart, ws.ml, S,
+      launch(attn_merge_kernel<float>, mgrid, dim3(256), 0, st, ws.opart, ws.ml, S,
                          BH, H, Mq, dh, out);
   }
   return hipGetLastError();

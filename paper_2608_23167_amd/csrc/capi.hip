@@ -121,11 +121,14 @@ constexpr int ATTN_MAX_SPLITS = 16;
 // ---- launch profiling: HIP events around each launcher, per tag ----------
 struct ProfRec {
   const char* tag;
+  int ordinal;            // kernel ordinal within one call of the operation
   hipEvent_t a, b;
 };
 bool g_prof_on = false;
 std::vector<ProfRec> g_prof;
 std::vector<hipEvent_t> g_event_pool;
+const char* g_prof_tag = nullptr;   // operation being launched
+int g_prof_ordinal = 0;
 
 hipEvent_t pool_event() {
   if (!g_event_pool.empty()) {
@@ -134,7 +137,7 @@ hipEvent_t pool_event() {
     return e;
   }
   hipEvent_t e = nullptr;
-  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return nullptr;
   return e;
 }
 
@@ -147,21 +150,26 @@ void prof_clear() {
 }
 
 struct ProfScope {
-  ProfRec rec{nullptr, nullptr, nullptr};
-  hipStream_t st;
-  ProfScope(const char* tag, hipStream_t s) : st(s) {
-    if (!g_prof_on) return;
-    rec.tag = tag;
-    rec.a = pool_event();
-    rec.b = pool_event();
-    if (rec.a) hipEventRecord(rec.a, st);
+  ProfScope(const char* tag, hipStream_t) {
+    g_prof_tag = tag;
+    g_prof_ordinal = 0;
   }
-  ~ProfScope() {
-    if (!g_prof_on || !rec.a || !rec.b) return;
-    hipEventRecord(rec.b, st);
-    g_prof.push_back(rec);
-  }
+  ~ProfScope() { g_prof_tag = nullptr; }
 };
+
+}  // namespace
+
+bool ssm::prof_next(hipEvent_t* start, hipEvent_t* stop) {
+  if (!g_prof_on || !g_prof_tag) return false;
+  ProfRec r{g_prof_tag, g_prof_ordinal++, pool_event(), pool_event()};
+  if (!r.a || !r.b) return false;
+  g_prof.push_back(r);
+  *start = r.a;
+  *stop = r.b;
+  return true;
+}
+
+namespace {
 
 #define PROF_TRY(tag, expr)            \
   do {                                 \
@@ -399,12 +407,12 @@ int32_t ssm_profile_enable(int32_t on) {
   return ok();
 }
 
-int32_t ssm_profile_query(const char* tag, int32_t* count, double* total_ms) {
+int32_t ssm_profile_query(const char* tag, int32_t kernel, int32_t* count, double* total_ms) {
   if (!tag || !count || !total_ms) return fail(SSM_E_INVAL, "null argument");
   int n = 0;
   double tot = 0.0;
   for (auto& r : g_prof) {
-    if (strcmp(r.tag, tag) != 0) continue;
+    if (strcmp(r.tag, tag) != 0 || (kernel >= 0 && r.ordinal != kernel)) continue;
     hipError_t e = hipEventSynchronize(r.b);
     if (e != hipSuccess) return fail(SSM_E_HIP, "hipEventSynchronize: %s", hipGetErrorString(e));
     float ms = 0.f;

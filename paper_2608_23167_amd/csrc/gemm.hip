@@ -661,13 +661,13 @@ static hipError_t launch_bf16(const Pol& pol, const ActIn& a, int M, int K, int 
   constexpr int BM = 128;
   const int ntiles = N / BN, mt = ceil_div(M, BM);
   const dim3 grid(ntiles * mt * S);
-  hipLaunchKernelGGL((gemm_bf16_kernel<BM, BN, PW, SPLIT, Pol>), grid, dim3(512), 0, st, pol,
+  launch((gemm_bf16_kernel<BM, BN, PW, SPLIT, Pol>), grid, dim3(512), 0, st, pol,
                      (const bf16_t*)a.hi, a.lo, a.G, M, K / S, mt, S,
                      S > 1 ? ws.part : nullptr, N);
   if constexpr (!has_tile<Pol>::value) {   // whole-tile epilogues never split K
     if (S > 1) {
       const size_t total = (size_t)M * N / 8 / (Pol::PAIRED ? 2 : 1);
-      hipLaunchKernelGGL((splitk_reduce_kernel<BN, Pol>), dim3((unsigned)((total + 255) / 256)),
+      launch((splitk_reduce_kernel<BN, Pol>), dim3((unsigned)((total + 255) / 256)),
                          dim3(256), 0, st, pol, ws.part, N, M, S, ntiles);
     }
   }
@@ -712,11 +712,11 @@ static hipError_t run_f32(const Pol& pol, const ActIn& a, int M, int K, int N, S
          (size_t)(S * 2) * M * N <= ws.floats)
     S *= 2;
   dim3 grid(ntiles, mt, S);
-  hipLaunchKernelGGL((gemm_f32_kernel<Pol>), grid, dim3(256), 0, st, pol, (const float*)a.hi,
+  launch((gemm_f32_kernel<Pol>), grid, dim3(256), 0, st, pol, (const float*)a.hi,
                      a.ld, M, K / S, S > 1 ? ws.part : nullptr, N);
   if (S > 1) {
     const size_t total = (size_t)M * N / 8 / (Pol::PAIRED ? 2 : 1);
-    hipLaunchKernelGGL((splitk_reduce_kernel<BN, Pol>), dim3((unsigned)((total + 255) / 256)),
+    launch((splitk_reduce_kernel<BN, Pol>), dim3((unsigned)((total + 255) / 256)),
                        dim3(256), 0, st, pol, ws.part, N, M, S, ntiles);
   }
   return hipGetLastError();
@@ -875,7 +875,7 @@ hipError_t lm_head_stats(const ActIn& a, int M, int K, const void* w, int N, int
   SplitWs none{nullptr, 0};
   hipError_t e = launch_bf16_pw<BN>(p, a, M, K, N, 1, c.pw, none, st);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(lm_merge_kernel, dim3(M), dim3(256), 0, st, (const LMPartial*)stats_ws,
+  launch(lm_merge_kernel, dim3(M), dim3(256), 0, st, (const LMPartial*)stats_ws,
                      2 * ntiles, k, argmax, conf, topk_ids, topk_w);
   return hipGetLastError();
 }

@@ -11,6 +11,27 @@
 
 namespace ssm {
 
+// ---- kernel launches -------------------------------------------------------
+// With launch profiling on, prof_next hands out a pair of HIP events recorded
+// under the current operation tag and the kernel's ordinal within that
+// operation; it returns false when profiling is off.
+bool prof_next(hipEvent_t* start, hipEvent_t* stop);
+
+// Every kernel of the library is launched here; a profiled launch is
+// bracketed by its own pair of events (created without the system-scope
+// fence, so recording them does not write back the caches between kernels).
+// Arguments are converted to the kernel's parameter types first.
+template <typename... KArgs, typename... Args>
+inline void launch(void (*kernel)(KArgs...), dim3 grid, dim3 block, uint32_t shmem,
+                   hipStream_t st, Args&&... args) {
+  static_assert(sizeof...(KArgs) == sizeof...(Args), "kernel argument count");
+  hipEvent_t a, b;
+  const bool timed = prof_next(&a, &b);
+  if (timed) hipEventRecord(a, st);
+  hipLaunchKernelGGL(kernel, grid, block, shmem, st, static_cast<KArgs>(args)...);
+  if (timed) hipEventRecord(b, st);
+}
+
 // Closed-form layout of the compacted rows of one step (Section 3.2, Eq. 1-5).
 struct SelectLayout {
   int n_prefix;      // prefix rows included (0 on a cached step)

@@ -95,14 +95,14 @@ static hipError_t norm_dispatch(const float* x, int d, const T* g, float eps, co
     const int nv = ceil_div(d / 4, 256);
     switch (nv) {
 #define NORM_CASE(NV) \
-  case NV: hipLaunchKernelGGL((norm_vec_kernel<T, NV>), dim3(n_rows), dim3(256), 0, st, x, d, g, eps, y, per, stride, off); return hipGetLastError();
+  case NV: launch((norm_vec_kernel<T, NV>), dim3(n_rows), dim3(256), 0, st, x, d, g, eps, y, per, stride, off); return hipGetLastError();
       NORM_CASE(1) NORM_CASE(2) NORM_CASE(3) NORM_CASE(4) NORM_CASE(5) NORM_CASE(6)
       NORM_CASE(7) NORM_CASE(8)
 #undef NORM_CASE
       default: break;
     }
   }
-  hipLaunchKernelGGL(norm_kernel<T>, dim3(ceil_div(n_rows, 4)), dim3(256), 0, st, x, d, g, eps, y,
+  launch(norm_kernel<T>, dim3(ceil_div(n_rows, 4)), dim3(256), 0, st, x, d, g, eps, y,
                      n_rows, per, stride, off);
   return hipGetLastError();
 }
@@ -129,7 +129,7 @@ hipError_t launch_rope_table(const int32_t* pos, int n_rows, int dh, float base,
                              hipStream_t st) {
   const int half = dh / 2, n = n_rows * half;
   if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(rope_table_kernel, dim3(ceil_div(n, 256)), dim3(256), 0, st, pos, n_rows,
+  launch(rope_table_kernel, dim3(ceil_div(n, 256)), dim3(256), 0, st, pos, n_rows,
                      half, dh, (double)base, tab);
   return hipGetLastError();
 }
@@ -244,7 +244,7 @@ hipError_t launch_rowstats(const float* logits, int rows, int V, int ldl, int ma
                            int32_t* argmax, float* conf, int32_t* topk_ids, float* topk_w,
                            hipStream_t st) {
   if (rows == 0) return hipSuccess;
-  hipLaunchKernelGGL(rowstats_kernel, dim3(rows), dim3(256), 0, st, logits, V, ldl, mask_id, k,
+  launch(rowstats_kernel, dim3(rows), dim3(256), 0, st, logits, V, ldl, mask_id, k,
                      argmax, conf, topk_ids, topk_w);
   return hipGetLastError();
 }

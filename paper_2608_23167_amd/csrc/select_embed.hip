@@ -46,7 +46,7 @@ hipError_t launch_select(const SelectLayout& L, int batch, int seq_len, const in
                          int32_t* pos, int32_t* tok_c, int8_t* region, int cap, hipStream_t st) {
   if (L.n_rows == 0) return hipSuccess;
   dim3 grid(ceil_div(L.n_rows, 256), batch);
-  hipLaunchKernelGGL(select_kernel, grid, dim3(256), 0, st, L, tokens, seq_len, pos, tok_c,
+  launch(select_kernel, grid, dim3(256), 0, st, L, tokens, seq_len, pos, tok_c,
                      region, cap);
   return hipGetLastError();
 }
@@ -105,11 +105,11 @@ hipError_t launch_embed(int dtype, const void* E, int d, int vocab, int mask_id,
   if (n_rows == 0) return hipSuccess;
   dim3 grid(n_rows, batch);
   if (dtype == 0)
-    hipLaunchKernelGGL(embed_kernel<float>, grid, dim3(256), 0, st, (const float*)E, d, vocab,
+    launch(embed_kernel<float>, grid, dim3(256), 0, st, (const float*)E, d, vocab,
                        mask_id, seq_len, tok_c, tok_stride, pos, region, n_rows, pred_ids, pred_w,
                        pred_step, prev_step, k, alpha, x);
   else
-    hipLaunchKernelGGL(embed_kernel<bf16_t>, grid, dim3(256), 0, st, (const bf16_t*)E, d, vocab,
+    launch(embed_kernel<bf16_t>, grid, dim3(256), 0, st, (const bf16_t*)E, d, vocab,
                        mask_id, seq_len, tok_c, tok_stride, pos, region, n_rows, pred_ids, pred_w,
                        pred_step, prev_step, k, alpha, x);
   return hipGetLastError();

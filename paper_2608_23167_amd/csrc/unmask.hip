@@ -81,7 +81,7 @@ hipError_t launch_unmask(int32_t* tokens, int batch, int seq_len, int block_star
                          const float* topk_w, int k, int n_out, const int32_t* pos_out, int step,
                          int32_t* pred_ids, float* pred_w, int32_t* pred_step, uint8_t* selected,
                          int32_t* masked_left, hipStream_t st) {
-  hipLaunchKernelGGL(unmask_kernel, dim3(batch), dim3(256), 0, st, tokens, seq_len, block_start, b,
+  launch(unmask_kernel, dim3(batch), dim3(256), 0, st, tokens, seq_len, block_start, b,
                      mask_id, rule, n_per_step, threshold, argmax, conf, topk_ids, topk_w, k,
                      n_out, pos_out, step, pred_ids, pred_w, pred_step, selected, masked_left);
   return hipGetLastError();

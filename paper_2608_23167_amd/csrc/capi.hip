@@ -339,21 +339,28 @@ int32_t ssm_denoise_step(const ssm_model* m, const ssm_kv_cache* cache, int32_t 
 
   PROF_TRY("rope_table", launch_rope_table(d_pos, n_rows, dh, m->rope_base, rope, st));
   HIP_TRY(hipMemcpyAsync(resid, d_x, (size_t)Mt * d * 4, hipMemcpyDeviceToDevice, st));
+  // the attention norm of layer 0 runs alone; every later norm follows the
+  // residual projection before it (fused with its split-K completion)
+  if (m->n_layers > 0)
+    PROF_TRY("norm", launch_norm(dt, resid, d, m->layers[0].attn_norm, m->rms_eps, xn_out, Mt, Mt,
+                                 0, 0, st));
   for (int l = 0; l < m->n_layers; ++l) {
     const ssm_layer& y = m->layers[l];
     char* kc = (char*)cache->k + l * layer_kv;
     char* vc = (char*)cache->v + l * layer_kv;
-    // attention block
-    PROF_TRY("norm", launch_norm(dt, resid, d, y.attn_norm, m->rms_eps, xn_out, Mt, Mt, 0, 0, st));
+    // attention block (its input norm is in xn)
     QKVOut qo{qb, kc, vc, cache->capacity, n_cached, n_rows, rope};
     PROF_TRY("gemm_qkv", gemm_qkv(dt, xn_in, Mt, d, y.wq, y.wk, y.wv, H, Hkv, dh, qo, sws, st));
     PROF_TRY("attention", attention(dt, qb, kc, vc, batch, H, Hkv, dh, n_rows, Nk,
                                     cache->capacity, attn_out, aws, st));
-    PROF_TRY("gemm_o", gemm_resid(dt, "o", attn_in, Mt, H * dh, y.wo, d, resid, sws, st));
+    const NormTo ffn_norm{y.ffn_norm, m->rms_eps, xn_out};
+    PROF_TRY("gemm_o", gemm_resid(dt, "o", attn_in, Mt, H * dh, y.wo, d, resid, sws, st, &ffn_norm));
     // feed-forward block
-    PROF_TRY("norm", launch_norm(dt, resid, d, y.ffn_norm, m->rms_eps, xn_out, Mt, Mt, 0, 0, st));
     PROF_TRY("gemm_gate_up", gemm_swiglu(dt, xn_in, Mt, d, y.w_gate, y.w_up, F, act_out, sws, st));
-    PROF_TRY("gemm_down", gemm_resid(dt, "down", act_in, Mt, F, y.w_down, d, resid, sws, st));
+    const bool more = l + 1 < m->n_layers;
+    const NormTo next_norm{more ? m->layers[l + 1].attn_norm : nullptr, m->rms_eps, xn_out};
+    PROF_TRY("gemm_down", gemm_resid(dt, "down", act_in, Mt, F, y.w_down, d, resid, sws, st,
+                                     more ? &next_norm : nullptr));
   }
   if (d_hidden_dbg)
     HIP_TRY(hipMemcpyAsync(d_hidden_dbg, resid, (size_t)Mt * d * 4, hipMemcpyDeviceToDevice, st));

@@ -585,7 +585,34 @@ __global__ void __launch_bounds__(256) gemm_f32_kernel(Pol pol, const float* __r
 // ---------------------------------------------------------------------------
 // split-K reduction: sums partial tiles in split order, then the epilogue
 // ---------------------------------------------------------------------------
-template <int BN, class Pol>
+// Sum of the split-K partials of 8 consecutive columns, in split order.  SC
+// is the split count when known at compile time (all loads in flight before
+// the sum), 0 for a runtime count.
+template <int SC>
+__device__ __forceinline__ void sum_partials8(const float* __restrict__ p, size_t stride, int S,
+                                              float (&acc)[8]) {
+  if constexpr (SC > 0) {
+    float4 v[SC][2];
+#pragma unroll
+    for (int s = 0; s < SC; ++s) {
+      v[s][0] = *(const float4*)(p + s * stride);
+      v[s][1] = *(const float4*)(p + s * stride + 4);
+    }
+#pragma unroll
+    for (int s = 0; s < SC; ++s) {
+      acc[0] += v[s][0].x; acc[1] += v[s][0].y; acc[2] += v[s][0].z; acc[3] += v[s][0].w;
+      acc[4] += v[s][1].x; acc[5] += v[s][1].y; acc[6] += v[s][1].z; acc[7] += v[s][1].w;
+    }
+  } else {
+    for (int s = 0; s < S; ++s) {
+      const float4 a = *(const float4*)(p + s * stride), b = *(const float4*)(p + s * stride + 4);
+      acc[0] += a.x; acc[1] += a.y; acc[2] += a.z; acc[3] += a.w;
+      acc[4] += b.x; acc[5] += b.y; acc[6] += b.z; acc[7] += b.w;
+    }
+  }
+}
+
+template <int BN, class Pol, int SC>
 __global__ void __launch_bounds__(256) splitk_reduce_kernel(Pol pol, const float* __restrict__ part,
                                                             int ldp, int M, int S, int ntiles) {
   // one thread per 8 consecutive output columns (of each half, when paired)
@@ -597,19 +624,22 @@ __global__ void __launch_bounds__(256) splitk_reduce_kernel(Pol pol, const float
   const int t = rem / C8, c0 = (rem % C8) * 8;
   float lo[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   float hi[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  for (int s = 0; s < S; ++s) {
-    const float* p = part + ((size_t)s * M + m) * ldp + (size_t)t * BN + c0;
-    const float4 a = *(const float4*)p, b = *(const float4*)(p + 4);
-    lo[0] += a.x; lo[1] += a.y; lo[2] += a.z; lo[3] += a.w;
-    lo[4] += b.x; lo[5] += b.y; lo[6] += b.z; lo[7] += b.w;
-    if constexpr (Pol::PAIRED) {
-      const float4 c = *(const float4*)(p + BN / 2), d = *(const float4*)(p + BN / 2 + 4);
-      hi[0] += c.x; hi[1] += c.y; hi[2] += c.z; hi[3] += c.w;
-      hi[4] += d.x; hi[5] += d.y; hi[6] += d.z; hi[7] += d.w;
-    }
-  }
+  const float* p = part + (size_t)m * ldp + (size_t)t * BN + c0;
+  sum_partials8<SC>(p, (size_t)M * ldp, S, lo);
+  if constexpr (Pol::PAIRED) sum_partials8<SC>(p + BN / 2, (size_t)M * ldp, S, hi);
   if constexpr (Pol::PAIRED) pol.store8(m, t, c0, BN, lo, hi);
   else pol.store8_1(m, t * BN + c0, lo);
+}
+
+template <int BN, class Pol>
+static void launch_reduce(const Pol& pol, const float* part, int N, int M, int S, int ntiles,
+                          hipStream_t st) {
+  const size_t total = (size_t)M * N / 8 / (Pol::PAIRED ? 2 : 1);
+  const dim3 grid((unsigned)((total + 255) / 256)), block(256);
+  if (S == 8) launch((splitk_reduce_kernel<BN, Pol, 8>), grid, block, 0, st, pol, part, N, M, S, ntiles);
+  else if (S == 4) launch((splitk_reduce_kernel<BN, Pol, 4>), grid, block, 0, st, pol, part, N, M, S, ntiles);
+  else if (S == 2) launch((splitk_reduce_kernel<BN, Pol, 2>), grid, block, 0, st, pol, part, N, M, S, ntiles);
+  else launch((splitk_reduce_kernel<BN, Pol, 0>), grid, block, 0, st, pol, part, N, M, S, ntiles);
 }
 
 // ---------------------------------------------------------------------------
@@ -657,7 +687,7 @@ static int auto_split(int tiles, int M, int K, size_t ws_floats, int N) {
 
 template <int BN, int PW, bool SPLIT, class Pol>
 static hipError_t launch_bf16(const Pol& pol, const ActIn& a, int M, int K, int N, int S,
-                              SplitWs ws, hipStream_t st) {
+                              SplitWs ws, hipStream_t st, bool reduce) {
   constexpr int BM = 128;
   const int ntiles = N / BN, mt = ceil_div(M, BM);
   const dim3 grid(ntiles * mt * S);
@@ -665,41 +695,116 @@ static hipError_t launch_bf16(const Pol& pol, const ActIn& a, int M, int K, int 
                      (const bf16_t*)a.hi, a.lo, a.G, M, K / S, mt, S,
                      S > 1 ? ws.part : nullptr, N);
   if constexpr (!has_tile<Pol>::value) {   // whole-tile epilogues never split K
-    if (S > 1) {
-      const size_t total = (size_t)M * N / 8 / (Pol::PAIRED ? 2 : 1);
-      launch((splitk_reduce_kernel<BN, Pol>), dim3((unsigned)((total + 255) / 256)),
-                         dim3(256), 0, st, pol, ws.part, N, M, S, ntiles);
-    }
+    if (S > 1 && reduce) launch_reduce<BN>(pol, ws.part, N, M, S, ntiles, st);
   }
   return hipGetLastError();
 }
 
 template <int BN, class Pol>
 static hipError_t launch_bf16_pw(const Pol& pol, const ActIn& a, int M, int K, int N, int S,
-                                 int pw, SplitWs ws, hipStream_t st) {
+                                 int pw, SplitWs ws, hipStream_t st, bool reduce = true) {
   const bool split = a.lo != nullptr;
   // the staging loop is unrolled by the ring depth: nk = K / S / 64 must be a
   // multiple of it (of 4 always, host-checked)
   if (pw >= 8 && (K / S / 64) % 8 == 0)
-    return split ? launch_bf16<BN, 8, true>(pol, a, M, K, N, S, ws, st)
-                 : launch_bf16<BN, 8, false>(pol, a, M, K, N, S, ws, st);
-  return split ? launch_bf16<BN, 4, true>(pol, a, M, K, N, S, ws, st)
-               : launch_bf16<BN, 4, false>(pol, a, M, K, N, S, ws, st);
+    return split ? launch_bf16<BN, 8, true>(pol, a, M, K, N, S, ws, st, reduce)
+                 : launch_bf16<BN, 8, false>(pol, a, M, K, N, S, ws, st, reduce);
+  return split ? launch_bf16<BN, 4, true>(pol, a, M, K, N, S, ws, st, reduce)
+               : launch_bf16<BN, 4, false>(pol, a, M, K, N, S, ws, st, reduce);
 }
 
+// Launch plan of one projection: the configuration with a valid tile width
+// and the split-K factor.
 template <class Pol>
-static hipError_t run_bf16(const char* kind, Pol pol, const ActIn& a, int M, int K, int N,
-                           GemmCfg c, SplitWs ws, hipStream_t st, int (*bn_ok)(const Pol&, int),
-                           void (*rebind)(Pol&, int)) {
+static GemmCfg plan_bf16(const char* kind, Pol& pol, int M, int K, int N, GemmCfg c,
+                         const SplitWs& ws, int (*bn_ok)(const Pol&, int),
+                         void (*rebind)(Pol&, int)) {
   c = cfg_override(kind, c);
   if (!bn_ok(pol, c.bn) || N % c.bn) c.bn = bn_ok(pol, 128) && N % 128 == 0 ? 128 : 64;
   if (rebind) rebind(pol, c.bn);
   const int tiles = (N / c.bn) * ceil_div(M, 128);
   int S = c.s > 0 ? c.s : auto_split(tiles, M, K, ws.floats, N);
   while (S > 1 && (K % (256 * S) != 0 || (size_t)S * M * N > ws.floats)) S /= 2;
-  if (c.bn == 96) return launch_bf16_pw<96>(pol, a, M, K, N, S, c.pw, ws, st);
-  if (c.bn == 64) return launch_bf16_pw<64>(pol, a, M, K, N, S, c.pw, ws, st);
-  return launch_bf16_pw<128>(pol, a, M, K, N, S, c.pw, ws, st);
+  c.s = S;
+  return c;
+}
+
+template <class Pol>
+static hipError_t launch_plan(const Pol& pol, const ActIn& a, int M, int K, int N, GemmCfg c,
+                              SplitWs ws, hipStream_t st, bool reduce = true) {
+  if (c.bn == 96) return launch_bf16_pw<96>(pol, a, M, K, N, c.s, c.pw, ws, st, reduce);
+  if (c.bn == 64) return launch_bf16_pw<64>(pol, a, M, K, N, c.s, c.pw, ws, st, reduce);
+  return launch_bf16_pw<128>(pol, a, M, K, N, c.s, c.pw, ws, st, reduce);
+}
+
+template <class Pol>
+static hipError_t run_bf16(const char* kind, Pol pol, const ActIn& a, int M, int K, int N,
+                           GemmCfg c, SplitWs ws, hipStream_t st, int (*bn_ok)(const Pol&, int),
+                           void (*rebind)(Pol&, int)) {
+  c = plan_bf16(kind, pol, M, K, N, c, ws, bn_ok, rebind);
+  return launch_plan(pol, a, M, K, N, c, ws, st);
+}
+
+// Completion of a split-K residual projection fused with the RMSNorm that
+// follows it: resid[m] += sum over splits of part[s][m] (split order, as the
+// split-K reduction does), then y[m] = resid[m] / rms(resid[m]) * g as the next
+// projection's operand.  One workgroup of 512 threads per row; thread t holds
+// the 8-column chunks t + 512 q of the row (q < NC).
+template <int SC, int NC>
+__global__ void __launch_bounds__(512) resid_norm_kernel(const float* __restrict__ part, int S,
+                                                         int M, int N, float* __restrict__ resid,
+                                                         const bf16_t* __restrict__ g, float eps,
+                                                         ActOut y) {
+  __shared__ float red[8];
+  const int m = blockIdx.x, tid = threadIdx.x, nc8 = N >> 3;
+  float v[NC][8];
+  float ss = 0.f;
+#pragma unroll
+  for (int q = 0; q < NC; ++q) {
+    const int c8 = tid + 512 * q;
+    if (c8 >= nc8) continue;
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    sum_partials8<SC>(part + (size_t)m * N + c8 * 8, (size_t)M * N, S, acc);
+    float4* r = (float4*)(resid + (size_t)m * N + c8 * 8);
+    float4 r0 = r[0], r1 = r[1];
+    r0.x += acc[0]; r0.y += acc[1]; r0.z += acc[2]; r0.w += acc[3];
+    r1.x += acc[4]; r1.y += acc[5]; r1.z += acc[6]; r1.w += acc[7];
+    r[0] = r0;
+    r[1] = r1;
+    v[q][0] = r0.x; v[q][1] = r0.y; v[q][2] = r0.z; v[q][3] = r0.w;
+    v[q][4] = r1.x; v[q][5] = r1.y; v[q][6] = r1.z; v[q][7] = r1.w;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) ss += v[q][e] * v[q][e];
+  }
+  ss = wave_sum(ss);
+  if ((tid & 63) == 0) red[tid >> 6] = ss;
+  __syncthreads();
+  ss = ((red[0] + red[1]) + (red[2] + red[3])) + ((red[4] + red[5]) + (red[6] + red[7]));
+  const float inv = 1.0f / sqrtf(ss / (float)N + eps);
+#pragma unroll
+  for (int q = 0; q < NC; ++q) {
+    const int c8 = tid + 512 * q;
+    if (c8 >= nc8) continue;
+    const u32x4_t gw = *(const u32x4_t*)(g + c8 * 8);
+    float o[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const uint32_t w = gw[e >> 1];
+      const float ge = __uint_as_float(e & 1 ? (w & 0xffff0000u) : (w << 16));
+      o[e] = v[q][e] * inv * ge;
+    }
+    y.store8<bf16_t>(m, c8 * 8, o);
+  }
+}
+
+template <int SC>
+static void launch_resid_norm(int nc, int S, int M, int N, const float* part, float* resid,
+                              const NormTo* nrm, hipStream_t st) {
+  const bf16_t* g = (const bf16_t*)nrm->g;
+  if (nc == 1)
+    launch(resid_norm_kernel<SC, 1>, dim3(M), dim3(512), 0, st, part, S, M, N, resid, g, nrm->eps, nrm->y);
+  else
+    launch(resid_norm_kernel<SC, 2>, dim3(M), dim3(512), 0, st, part, S, M, N, resid, g, nrm->eps, nrm->y);
 }
 
 template <class Pol>
@@ -714,11 +819,7 @@ static hipError_t run_f32(const Pol& pol, const ActIn& a, int M, int K, int N, S
   dim3 grid(ntiles, mt, S);
   launch((gemm_f32_kernel<Pol>), grid, dim3(256), 0, st, pol, (const float*)a.hi,
                      a.ld, M, K / S, S > 1 ? ws.part : nullptr, N);
-  if (S > 1) {
-    const size_t total = (size_t)M * N / 8 / (Pol::PAIRED ? 2 : 1);
-    launch((splitk_reduce_kernel<BN, Pol>), dim3((unsigned)((total + 255) / 256)),
-                       dim3(256), 0, st, pol, ws.part, N, M, S, ntiles);
-  }
+  if (S > 1) launch_reduce<BN>(pol, ws.part, N, M, S, ntiles, st);
   return hipGetLastError();
 }
 
@@ -753,14 +854,28 @@ hipError_t gemm_qkv(int dtype, const ActIn& a, int M, int d, const void* wq, con
 }
 
 hipError_t gemm_resid(int dtype, const char* kind, const ActIn& a, int M, int K, const void* w,
-                      int N, float* resid, SplitWs ws, hipStream_t st) {
+                      int N, float* resid, SplitWs ws, hipStream_t st, const NormTo* nrm) {
+  hipError_t e;
   if (dtype == 0) {
     PolResid<float> p{(const float*)w, K, N, resid};
-    return run_f32(p, a, M, K, N, ws, st);
+    e = run_f32(p, a, M, K, N, ws, st);
+  } else {
+    PolResid<bf16_t> p{(const bf16_t*)w, K, N, resid};
+    const GemmCfg c = plan_bf16(kind, p, M, K, N, default_cfg(kind, M), ws,
+                                any_bn<PolResid<bf16_t>>, (void (*)(PolResid<bf16_t>&, int))nullptr);
+    const int nc = ceil_div(N / 8, 512);
+    const bool fuse = nrm && c.s > 1 && N % 8 == 0 && nc <= 2 && ((uintptr_t)nrm->g & 15) == 0;
+    e = launch_plan(p, a, M, K, N, c, ws, st, !fuse);
+    if (e != hipSuccess || !fuse) goto separate;
+    if (c.s == 8) launch_resid_norm<8>(nc, c.s, M, N, ws.part, resid, nrm, st);
+    else if (c.s == 4) launch_resid_norm<4>(nc, c.s, M, N, ws.part, resid, nrm, st);
+    else if (c.s == 2) launch_resid_norm<2>(nc, c.s, M, N, ws.part, resid, nrm, st);
+    else launch_resid_norm<0>(nc, c.s, M, N, ws.part, resid, nrm, st);
+    return hipGetLastError();
   }
-  PolResid<bf16_t> p{(const bf16_t*)w, K, N, resid};
-  return run_bf16(kind, p, a, M, K, N, default_cfg(kind, M), ws, st, any_bn<PolResid<bf16_t>>,
-                  (void (*)(PolResid<bf16_t>&, int))nullptr);
+separate:
+  if (e != hipSuccess || !nrm) return e;
+  return launch_norm(dtype, resid, N, nrm->g, nrm->eps, nrm->y, M, M, 0, 0, st);
 }
 
 hipError_t gemm_swiglu(int dtype, const ActIn& a, int M, int d, const void* wg, const void* wu,

@@ -155,8 +155,17 @@ hipError_t launch_norm(int dtype, const float* x, int d, const void* g, float ep
 hipError_t gemm_qkv(int dtype, const ActIn& a, int M, int d, const void* wq, const void* wk,
                     const void* wv, int H, int Hkv, int dh, const QKVOut& out, SplitWs ws,
                     hipStream_t st);
+// RMSNorm applied to the residual stream right after a residual projection:
+// y = resid / rms(resid) * g, written as the next projection's operand.
+struct NormTo {
+  const void* g;
+  float eps;
+  ActOut y;
+};
+// resid += a * w^T; with `nrm`, the updated rows are also normalised into
+// nrm->y (fused with the split-K completion when the projection splits K).
 hipError_t gemm_resid(int dtype, const char* kind, const ActIn& a, int M, int K, const void* w,
-                      int N, float* resid, SplitWs ws, hipStream_t st);
+                      int N, float* resid, SplitWs ws, hipStream_t st, const NormTo* nrm);
 hipError_t gemm_swiglu(int dtype, const ActIn& a, int M, int d, const void* wg, const void* wu,
                        int F, const ActOut& act, SplitWs ws, hipStream_t st);
 hipError_t gemm_store_f32(const ActIn& a, int M, int K, const void* w, int N, float* c, int ldc,

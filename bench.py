@@ -94,6 +94,12 @@ def main():
     ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--workload", default="llada_gen256")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--attn-sweep", action="store_true",
+                    help="instead of the decoding bench: the attention/gather microbenchmark "
+                         "(LLaDA-8B heads, batch 8, prefix 4096, block 64, suffix 4096) over the "
+                         "kept-suffix count")
+    ap.add_argument("--no-full-suffix", action="store_true",
+                    help="skip the unpruned (full-suffix) decoder run of the same schedule")
     ap.add_argument("--no-profile", action="store_true",
                     help="skip the profiled replay (per-kernel times and roofline), e.g. under counter collection")
     ap.add_argument("--cpu-layers", type=int, default=None,
@@ -106,6 +112,10 @@ def main():
         print("bench.py: this build runs on exactly one GPU; multi-GPU runs are not supported "
               "(sequences would shard data-parallel with no per-step exchange)", file=sys.stderr)
         sys.exit(2)
+
+    if args.attn_sweep:
+        attn_sweep()
+        return
 
     import numpy as np
     import torch
@@ -128,35 +138,40 @@ def main():
     K = args.steps or len(sched)
     W = args.warmup
 
-    def run(n, events=None):
+    def run(n, events=None, d=dec):
         """n steps of the schedule from a fresh generation, wrapping around."""
-        dec.reset(tok0)
+        d.reset(tok0)
         for i in range(n):
             j, first = sched[i % len(sched)]
             if i and i % len(sched) == 0:
-                dec.reset(tok0)
+                d.reset(tok0)
             if events is not None:
                 events[i][0].record()
-            dec.step(j, first)
+            d.step(j, first)
             if events is not None:
                 events[i][1].record()
 
-    print(f"[bench] warmup {W} steps", file=sys.stderr, flush=True)
-    run(W)
-    torch.cuda.synchronize()
+    def timed(d):
+        """W warm-up steps, then K timed steps: (wall s, per-step ms, step kinds)."""
+        run(W, d=d)
+        torch.cuda.synchronize()
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(K)]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        run(K, ev, d=d)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        return wall, [a.elapsed_time(b) for a, b in ev], [sched[i % len(sched)][1] for i in range(K)]
 
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(K)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    run(K, ev)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    wall = t1 - t0
-    step_ms = [a.elapsed_time(b) for a, b in ev]
-    kinds = [sched[i % len(sched)][1] for i in range(K)]
-    start_ms = [t for t, f in zip(step_ms, kinds) if f]
-    cached_ms = [t for t, f in zip(step_ms, kinds) if not f]
+    def medians(step_ms, kinds):
+        start_ms = [t for t, f in zip(step_ms, kinds) if f]
+        cached_ms = [t for t, f in zip(step_ms, kinds) if not f]
+        return {"block_start_median": round(statistics.median(start_ms), 4) if start_ms else None,
+                "cached_median": round(statistics.median(cached_ms), 4) if cached_ms else None}
+
+    print(f"[bench] warmup {W} steps", file=sys.stderr, flush=True)
+    wall, step_ms, kinds = timed(dec)
     tokens = K * wl.n_per_step * wl.batch
     value = tokens / wall
     print(f"[bench] {K} steps in {wall:.3f} s -> {value:.1f} tokens/s", file=sys.stderr, flush=True)
@@ -221,20 +236,100 @@ def main():
                    "block": wl.block_size, "rule": f"{wl.rule}-{wl.n_per_step}",
                    "budgets": [wl.local_budget, wl.middle_budget, wl.tail_budget],
                    "prefix_cache": wl.cache, "topk": wl.topk, "alpha": wl.alpha},
-        "step_latency_ms": {
-            "block_start_median": round(statistics.median(start_ms), 4) if start_ms else None,
-            "cached_median": round(statistics.median(cached_ms), 4) if cached_ms else None,
-        },
+        "step_latency_ms": medians(step_ms, kinds),
         "kernel_ms_per_step": {t: round(prof[t][1] / K, 4) for t in PROFILE_TAGS if prof[t][0]},
         "roofline": roof,
         "cpu_baseline": None,
     }
     print(f"[bench] profile: {result['kernel_ms_per_step']}", file=sys.stderr, flush=True)
 
+    if not args.no_full_suffix:
+        # the same schedule without suffix pruning: every suffix token is a
+        # local row (the unpruned decoder SSM is measured against)
+        wl_full = wl.replace(local_budget=wl.gen_len, middle_budget=0, tail_budget=0)
+        dec_full = Decoder(wl_full, dm, device=dev)
+        fwall, fstep_ms, fkinds = timed(dec_full)
+        fvalue = tokens / fwall
+        del dec_full
+        print(f"[bench] full suffix: {K} steps in {fwall:.3f} s -> {fvalue:.1f} tokens/s",
+              file=sys.stderr, flush=True)
+        result["full_suffix"] = {"value": round(fvalue, 2), "unit": "tokens/s",
+                                 "ms_per_step": round(fwall / K * 1e3, 4),
+                                 "step_latency_ms": medians(fstep_ms, fkinds),
+                                 "ssm_speedup": round(value / fvalue, 3)}
+
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, mw, dec, args.cpu_layers or wl.model.n_layers,
                                               args.cpu_reps)
     print(json.dumps(result), flush=True)
+
+
+def attn_sweep(reps=10):
+    """Attention over prefix KV 4096 + block 64 + kept suffix rows, and the gather
+    of the kept rows of a [8, 4096, 4096] bf16 suffix tensor, for kept-suffix
+    counts 0 .. 4096 (local only below 48; else local kept-48, middle 32, tail
+    16; 4096 = the whole suffix).  Q, K, V ~ N(0, 1); one JSON line."""
+    import torch
+    from synthetic.generate import seeded_normal
+    from paper_2608_23167_amd.api import (select_params, ssm_attention,
+                                          ssm_attention_workspace_size, ssm_gather_rows,
+                                          ssm_select_suffix)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    B, H, DH, PRE, BLK, SUF = 8, 32, 128, 4096, 64, 4096
+    cap = PRE + BLK + SUF
+    q_all = seeded_normal((B, H, BLK + SUF, DH), 0, "sweep.q", device=dev, dtype=torch.bfloat16)
+    kc = seeded_normal((B, H, cap, DH), 0, "sweep.k", device=dev, dtype=torch.bfloat16)
+    vc = seeded_normal((B, H, cap, DH), 0, "sweep.v", device=dev, dtype=torch.bfloat16)
+    src = seeded_normal((B, SUF, H * DH), 0, "sweep.x", device=dev, dtype=torch.bfloat16)
+    tokens = torch.zeros((1, PRE + BLK + SUF), device=dev, dtype=torch.int32)
+    points = []
+    for kept in (0, 16, 48, 176, 256, 512, 1024, 2048, 4096):
+        lb, mb, tb = (kept, 0, 0) if kept < 48 or kept == SUF else (kept - 48, 32, 16)
+        prm = select_params(PRE, BLK + SUF, BLK, 0, lb, mb, 0, tb, False)
+        pos = torch.empty(BLK + SUF, device=dev, dtype=torch.int32)
+        tok_c = torch.empty((1, BLK + SUF), device=dev, dtype=torch.int32)
+        n_rows, n_suf, _ = ssm_select_suffix(prm, tokens, pos, tok_c, None)
+        assert n_suf == kept, (kept, n_suf)
+        n_q, n_keys = BLK + kept, PRE + BLK + kept
+        q = q_all[:, :, :n_q].contiguous()
+        out = torch.empty((B, n_q, H * DH), device=dev, dtype=torch.float32)
+        ws = torch.empty(ssm_attention_workspace_size(B, H, n_q), device=dev, dtype=torch.uint8)
+        spos = (pos[BLK:n_rows] - (PRE + BLK)).contiguous()
+        gout = torch.empty((B, kept, H * DH), device=dev, dtype=torch.bfloat16)
+
+        def timed(fn):
+            fn()
+            torch.cuda.synchronize()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            for _ in range(reps):
+                fn()
+            b.record()
+            torch.cuda.synchronize()
+            return a.elapsed_time(b) / reps * 1e3
+
+        t_att = timed(lambda: ssm_attention(q, kc, vc, n_keys, out, ws))
+        flops = 4.0 * B * H * n_q * n_keys * DH
+        att_bytes = 2.0 * B * H * n_q * DH + 2 * 2.0 * B * H * n_keys * DH + 4.0 * B * n_q * H * DH
+        tfl = flops / (t_att * 1e-6) / 1e12
+        gbs = att_bytes / (t_att * 1e-6) / 1e9
+        mfma_bound = flops / att_bytes > BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
+        pt = {"kept": kept, "n_q": n_q, "n_keys": n_keys, "attn_us": round(t_att, 2),
+              "attn_tflops": round(tfl, 1), "attn_gbs": round(gbs, 1),
+              "attn_bound": "mfma" if mfma_bound else "hbm",
+              "attn_frac": round(tfl / BF16_PEAK_TFLOPS if mfma_bound else gbs / HBM_PEAK_GBS, 4)}
+        if kept:
+            t_g = timed(lambda: ssm_gather_rows(src, spos, gout))
+            g_bytes = 2 * 2.0 * B * kept * H * DH
+            pt.update({"gather_us": round(t_g, 2), "gather_gbs": round(g_bytes / (t_g * 1e-6) / 1e9, 1),
+                       "gather_frac": round(g_bytes / (t_g * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)})
+        print(f"[bench] sweep {pt}", file=sys.stderr, flush=True)
+        points.append(pt)
+    print(json.dumps({"metric": "attention and gather per layer vs kept-suffix count "
+                                "(LLaDA-8B heads, batch 8, prefix 4096, block 64, suffix 4096)",
+                      "unit": "us", "n_gpus": 1, "dtype": "bf16", "data": "synthetic N(0,1) Q/K/V",
+                      "points": points}), flush=True)
 
 
 def cpu_baseline(wl, mw, dec, n_layers_sample, reps):

@@ -234,6 +234,41 @@ int32_t ssm_denoise_step(const ssm_model* m, const ssm_kv_cache* cache, int32_t 
                          void* stream);
 
 /* ------------------------------------------------------------------------ */
+/* Building blocks of the step, callable alone (measurement and testing).   */
+/* ------------------------------------------------------------------------ */
+
+/* Bytes of device workspace ssm_attention needs (split-KV partial results). */
+int32_t ssm_attention_workspace_size(int32_t batch, int32_t n_heads, int32_t n_q, size_t* bytes);
+
+/*
+ * The non-causal attention of ssm_denoise_step on its own (Section 3.2: every
+ * compacted row attends to every key): for sequence s, head h, row i,
+ *   out[s, i, 128 h + :] = sum_j softmax_j(q[s,h,i,:] . k[s,h/g,j,:] / sqrt(128)) v[s,h/g,j,:]
+ * over keys j < n_keys, g = n_heads / n_kv_heads (grouped-query heads).
+ * Inputs bfloat16: d_q [batch, n_heads, n_q, 128]; d_k, d_v [batch,
+ * n_kv_heads, capacity, 128] (the KV cache layout, keys already rotated).
+ * Output float32 d_out [batch, n_q, n_heads * 128], row-major.  Scores and
+ * softmax in float32; the probabilities are rounded to bfloat16 for the
+ * P V product, as in the step.  n_keys <= capacity (SSM_E_CAPACITY), n_heads a
+ * multiple of n_kv_heads (SSM_E_SHAPE), ws_bytes >=
+ * ssm_attention_workspace_size(batch, n_heads, n_q) (SSM_E_CAPACITY).
+ */
+int32_t ssm_attention(int32_t batch, int32_t n_heads, int32_t n_kv_heads, int32_t n_q,
+                      int32_t n_keys, int32_t capacity, const void* d_q, const void* d_k,
+                      const void* d_v, float* d_out, void* d_ws, size_t ws_bytes, void* stream);
+
+/*
+ * The row gather of the compaction (Section 3.2, sparse input construction)
+ * applied to activations: for each sequence s and i < n_rows,
+ *   d_dst[s, i, :] = d_src[s, d_pos[i], :]
+ * for bfloat16 rows of `width` elements (a multiple of 8); d_src [batch,
+ * src_rows, width], d_pos int32 [n_rows], d_dst [batch, n_rows, width].
+ * A position outside [0, src_rows) yields a row of zeros.
+ */
+int32_t ssm_gather_rows(int32_t batch, int32_t src_rows, int32_t width, const void* d_src,
+                        const int32_t* d_pos, int32_t n_rows, void* d_dst, void* stream);
+
+/* ------------------------------------------------------------------------ */
 /* Confidence-based unmasking and prediction-state update (Section 4.2).    */
 /* ------------------------------------------------------------------------ */
 

@@ -102,6 +102,41 @@ def ssm_denoise_step(model, cache, cache_mode: int, n_cached: int, pos: torch.Te
     check(rc, "ssm_denoise_step")
 
 
+def ssm_attention_workspace_size(batch: int, n_heads: int, n_q: int) -> int:
+    n = C.c_size_t()
+    check(lib().ssm_attention_workspace_size(batch, n_heads, n_q, C.byref(n)),
+          "ssm_attention_workspace_size")
+    return n.value
+
+
+def ssm_attention(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, n_keys: int,
+                  out: torch.Tensor, ws: torch.Tensor, stream=None) -> None:
+    """q bf16 [B, H, n_q, 128]; k, v bf16 [B, H_kv, capacity, 128]; out float32
+    [B, n_q, H * 128]; ws uint8 of ssm_attention_workspace_size(B, H, n_q) bytes."""
+    B, H, n_q, dh = q.shape
+    if dh != 128 or k.shape != v.shape or k.shape[0] != B or k.shape[3] != 128:
+        raise ValueError("shapes: q [B, H, n_q, 128], k = v [B, H_kv, capacity, 128]")
+    if tuple(out.shape) != (B, n_q, H * 128):
+        raise ValueError("out must be [B, n_q, H * 128]")
+    check(lib().ssm_attention(B, H, k.shape[1], n_q, int(n_keys), k.shape[2],
+                              _ptr(q, torch.bfloat16, "q"), _ptr(k, torch.bfloat16, "k"),
+                              _ptr(v, torch.bfloat16, "v"), _ptr(out, torch.float32, "out"),
+                              _ptr(ws, None, "ws"), ws.numel() * ws.element_size(),
+                              _stream(stream)), "ssm_attention")
+
+
+def ssm_gather_rows(src: torch.Tensor, pos: torch.Tensor, out: torch.Tensor, stream=None) -> None:
+    """out[s, i, :] = src[s, pos[i], :]; src bf16 [B, src_rows, width], pos int32
+    [n_rows], out bf16 [B, n_rows, width]; out-of-range positions give zeros."""
+    B, rows, width = src.shape
+    if tuple(out.shape) != (B, pos.numel(), width):
+        raise ValueError("out must be [B, n_rows, width]")
+    check(lib().ssm_gather_rows(B, rows, width, _ptr(src, torch.bfloat16, "src"),
+                                _ptr(pos, torch.int32, "pos"), pos.numel(),
+                                _ptr(out, torch.bfloat16, "out"), _stream(stream)),
+          "ssm_gather_rows")
+
+
 def ssm_unmask(tokens: torch.Tensor, block_start: int, block_size: int, mask_id: int, rule: int,
                n_per_step: int, threshold: float, argmax: torch.Tensor, conf: torch.Tensor,
                topk_ids: torch.Tensor, topk_w: torch.Tensor, k: int, n_out: int,

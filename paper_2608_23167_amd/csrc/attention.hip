@@ -23,10 +23,23 @@ constexpr float LOG2E = 1.4426950408889634f;
 // transposing writes of a wave over all 64 banks.
 __device__ __forceinline__ int vt_word(int d, int p) { return d * 36 + (p ^ ((d >> 4) << 1)); }
 
+// Workgroup order: a 1-D grid over (query tile, sequence x head, split),
+// query tiles innermost, dealt so that each XCD (workgroup id w runs on XCD
+// w % 8) gets a contiguous range: the query tiles of one head then read its
+// keys and values through one L2 instead of one per XCD.
+__device__ __forceinline__ void attn_tile_of(int w, int total, int qtiles, int BH, int& qt,
+                                             int& bh, int& split) {
+  const int per = total / 8;
+  const int v = w < per * 8 ? (w % 8) * per + (w / 8) : w;
+  qt = v % qtiles;
+  bh = (v / qtiles) % BH;
+  split = v / (qtiles * BH);
+}
+
 __global__ void __launch_bounds__(256) attn_bf16_kernel(
     const bf16_t* __restrict__ Q, const bf16_t* __restrict__ Kc, const bf16_t* __restrict__ Vc,
     int H, int Hkv, int Mq, int Nk, int cap, int keys_per_split, float scale_log2,
-    ActOut O, float* __restrict__ Opart, float* __restrict__ ML) {
+    ActOut O, float* __restrict__ Opart, float* __restrict__ ML, int qtiles, int BH) {
   constexpr int DH = 128, KT = 64, KS = DH + 8, VW = 36;    // VW: words per V^T row
   constexpr int KBUF = KT * KS, VBUF = DH * VW;
   // two tile buffers: tile i is written while tile i - 1 is read
@@ -34,10 +47,11 @@ __global__ void __launch_bounds__(256) attn_bf16_kernel(
   __shared__ __attribute__((aligned(16))) uint32_t Vt[2 * VBUF];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, c16 = lane & 15;
-  const int bh = blockIdx.y, s = bh / H, h = bh % H, kvh = h / (H / Hkv);
-  const int split = blockIdx.z;
+  int qt, bh, split;
+  attn_tile_of(blockIdx.x, gridDim.x, qtiles, BH, qt, bh, split);
+  const int s = bh / H, h = bh % H, kvh = h / (H / Hkv);
   const int kb = split * keys_per_split, ke = min(Nk, kb + keys_per_split);
-  const int q = blockIdx.x * 64 + wave * 16 + c16;
+  const int q = qt * 64 + wave * 16 + c16;
 
   const bf16_t* Qh = Q + (size_t)bh * Mq * DH;
   bf16x8_t qf[4];
@@ -170,6 +184,14 @@ __global__ void __launch_bounds__(256) attn_bf16_kernel(
   if (Opart == nullptr) {
     const float inv = 1.0f / l_run;
     const int row = s * Mq + q;
+    if (O.f32) {
+      float* orow = (float*)O.hi + (size_t)row * O.ld + h * DH + 4 * g;
+#pragma unroll
+      for (int db = 0; db < 8; ++db)
+        *(float4*)(orow + 16 * db) = make_float4(o[db][0] * inv, o[db][1] * inv, o[db][2] * inv,
+                                                 o[db][3] * inv);
+      return;
+    }
 #pragma unroll
     for (int db = 0; db < 8; ++db) {
       const size_t idx = frag_index(row, h * DH + 16 * db + 4 * g, O.G);   // 4 columns, one chunk
@@ -184,7 +206,7 @@ __global__ void __launch_bounds__(256) attn_bf16_kernel(
       if (O.lo) *(uint2*)(O.lo + idx) = *(const uint2*)lo;
     }
   } else {
-    const size_t row = ((size_t)split * gridDim.y + bh) * Mq + q;
+    const size_t row = ((size_t)split * BH + bh) * Mq + q;
     float* op = Opart + row * DH;
 #pragma unroll
     for (int db = 0; db < 8; ++db) *(f32x4_t*)(op + 16 * db + 4 * g) = o[db];
@@ -289,9 +311,9 @@ hipError_t attention(int dtype, const void* q, const void* kc, const void* vc, i
   dim3 grid(qtiles, BH, S);
   float* opart = S > 1 ? ws.opart : nullptr;
   if (dtype == 1) {
-    launch(attn_bf16_kernel, grid, dim3(256), 0, st, (const bf16_t*)q,
-                       (const bf16_t*)kc, (const bf16_t*)vc, H, Hkv, Mq, Nk, cap, kps, scale_log2,
-                       out, opart, ws.ml);
+    launch(attn_bf16_kernel, dim3(qtiles * BH * S), dim3(256), 0, st, (const bf16_t*)q,
+           (const bf16_t*)kc, (const bf16_t*)vc, H, Hkv, Mq, Nk, cap, kps, scale_log2, out, opart,
+           ws.ml, qtiles, BH);
   } else {
     const float* qf = (const float*)q;
     const float* kf = (const float*)kc;

@@ -380,6 +380,53 @@ int32_t ssm_denoise_step(const ssm_model* m, const ssm_kv_cache* cache, int32_t 
   return ok();
 }
 
+// Largest split-KV count the attention launcher picks for this grid: it never
+// exceeds 512 workgroups over (64-row query tiles x sequences x heads).
+static int attn_max_splits(int batch, int n_heads, int n_q) {
+  const long tiles = (long)ceil_div(n_q > 0 ? n_q : 1, 64) * batch * n_heads;
+  long s = 512 / tiles;
+  if (s > ATTN_MAX_SPLITS) s = ATTN_MAX_SPLITS;
+  return s < 1 ? 1 : (int)s;
+}
+
+int32_t ssm_attention_workspace_size(int32_t batch, int32_t n_heads, int32_t n_q, size_t* bytes) {
+  if (!bytes || batch < 1 || n_heads < 1 || n_q < 0) return fail(SSM_E_INVAL, "bad arguments");
+  const size_t rows = (size_t)attn_max_splits(batch, n_heads, n_q) * batch * n_heads * n_q;
+  *bytes = align256(rows * 128 * 4) + align256(rows * 2 * 4);
+  return ok();
+}
+
+int32_t ssm_attention(int32_t batch, int32_t n_heads, int32_t n_kv_heads, int32_t n_q,
+                      int32_t n_keys, int32_t capacity, const void* d_q, const void* d_k,
+                      const void* d_v, float* d_out, void* d_ws, size_t ws_bytes, void* stream) {
+  if (batch < 1 || n_heads < 1 || n_kv_heads < 1 || n_q < 0 || n_keys < 1 || capacity < 1)
+    return fail(SSM_E_INVAL, "bad sizes");
+  if (n_heads % n_kv_heads) return fail(SSM_E_SHAPE, "n_heads %d not a multiple of n_kv_heads %d", n_heads, n_kv_heads);
+  if (n_keys > capacity) return fail(SSM_E_CAPACITY, "n_keys %d > capacity %d", n_keys, capacity);
+  if (!d_q || !d_k || !d_v || !d_out || !d_ws) return fail(SSM_E_INVAL, "null device pointer");
+  size_t need = 0;
+  ssm_attention_workspace_size(batch, n_heads, n_q, &need);
+  if (ws_bytes < need) return fail(SSM_E_CAPACITY, "workspace %zu < %zu bytes", ws_bytes, need);
+  const int max_splits = attn_max_splits(batch, n_heads, n_q);
+  const size_t rows = (size_t)max_splits * batch * n_heads * n_q;
+  AttnWs aws{(float*)d_ws, (float*)((char*)d_ws + align256(rows * 128 * 4)), max_splits};
+  const ActOut out{d_out, nullptr, n_heads * 128, 0, 1};
+  hipStream_t st = (hipStream_t)stream;
+  HIP_TRY(attention(SSM_DT_BF16, d_q, d_k, d_v, batch, n_heads, n_kv_heads, 128, n_q, n_keys,
+                    capacity, out, aws, st));
+  return ok();
+}
+
+int32_t ssm_gather_rows(int32_t batch, int32_t src_rows, int32_t width, const void* d_src,
+                        const int32_t* d_pos, int32_t n_rows, void* d_dst, void* stream) {
+  if (batch < 1 || src_rows < 0 || width < 8 || width % 8 || n_rows < 0)
+    return fail(SSM_E_INVAL, "bad sizes (width must be a positive multiple of 8)");
+  if (n_rows > 0 && (!d_src || !d_pos || !d_dst)) return fail(SSM_E_INVAL, "null device pointer");
+  HIP_TRY(launch_gather_rows(batch, src_rows, width, (const bf16_t*)d_src, d_pos, n_rows,
+                             (bf16_t*)d_dst, (hipStream_t)stream));
+  return ok();
+}
+
 int32_t ssm_unmask(int32_t* d_tokens, int32_t batch, int32_t seq_len, int32_t block_start,
                    int32_t block_size, int32_t mask_id, int32_t rule, int32_t n_per_step,
                    float threshold, const int32_t* d_argmax, const float* d_conf,

@@ -47,6 +47,10 @@ struct SelectLayout {
 hipError_t launch_select(const SelectLayout& L, int batch, int seq_len, const int32_t* tokens,
                          int32_t* pos, int32_t* tok_c, int8_t* region, int cap, hipStream_t st);
 
+// out[s, i, :] = src[s, pos[i], :] for bfloat16 rows of `width` elements.
+hipError_t launch_gather_rows(int batch, int src_rows, int width, const bf16_t* src,
+                              const int32_t* pos, int n_rows, bf16_t* dst, hipStream_t st);
+
 hipError_t launch_embed(int dtype, const void* E, int d, int vocab, int mask_id, int batch,
                         int seq_len, const int32_t* tok_c, int tok_stride, const int32_t* pos,
                         const int8_t* region, int n_rows, const int32_t* pred_ids,
@@ -108,15 +112,18 @@ struct ActIn {
 
 // Destination of an activation written by an epilogue, in the layout of
 // ActIn: float32 row-major for float32 models; for bfloat16 models
-// hi = bf16(v) and, if lo is not null, lo = bf16(v - hi), in fragment order.
+// hi = bf16(v) and, if lo is not null, lo = bf16(v - hi), in fragment order;
+// with f32 set, a bfloat16 kernel writes float32 row-major (row stride ld)
+// instead (outputs handed back to a caller).
 struct ActOut {
   void* hi;
   bf16_t* lo;
   int ld;
   int G;
+  int f32;
   template <typename T>
   __device__ __forceinline__ void store(int m, int k, float v) const {
-    if constexpr (std::is_same<T, float>::value) {
+    if (std::is_same<T, float>::value || f32) {
       ((float*)hi)[(size_t)m * ld + k] = v;
     } else {
       const size_t i = frag_index(m, k, G);
@@ -129,7 +136,7 @@ struct ActOut {
   // order, so one 16-byte store per part
   template <typename T>
   __device__ __forceinline__ void store8(int m, int k, const float (&v)[8]) const {
-    if constexpr (std::is_same<T, float>::value) {
+    if (std::is_same<T, float>::value || f32) {
       float* p = (float*)hi + (size_t)m * ld + k;
       *(float4*)p = make_float4(v[0], v[1], v[2], v[3]);
       *(float4*)(p + 4) = make_float4(v[4], v[5], v[6], v[7]);

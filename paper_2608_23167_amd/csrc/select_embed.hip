@@ -115,4 +115,30 @@ hipError_t launch_embed(int dtype, const void* E, int d, int vocab, int mask_id,
   return hipGetLastError();
 }
 
+// ---- row gather of activations -------------------------------------------
+// One thread per 16-byte chunk: out[s, i, 8c .. 8c + 7] = src[s, pos[i], ...];
+// positions outside [0, src_rows) give zeros.
+__global__ void __launch_bounds__(256) gather_rows_kernel(const bf16_t* __restrict__ src,
+                                                          int src_rows, int width,
+                                                          const int32_t* __restrict__ pos,
+                                                          int n_rows, bf16_t* __restrict__ dst) {
+  const int c8n = width >> 3, s = blockIdx.y;
+  const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (size_t)n_rows * c8n) return;
+  const int i = (int)(idx / c8n), c = (int)(idx % c8n);
+  const int p = pos[i];
+  u32x4_t v = {0u, 0u, 0u, 0u};
+  if (p >= 0 && p < src_rows) v = *(const u32x4_t*)(src + ((size_t)s * src_rows + p) * width + c * 8);
+  *(u32x4_t*)(dst + ((size_t)s * n_rows + i) * width + c * 8) = v;
+}
+
+hipError_t launch_gather_rows(int batch, int src_rows, int width, const bf16_t* src,
+                              const int32_t* pos, int n_rows, bf16_t* dst, hipStream_t st) {
+  const size_t n = (size_t)n_rows * (width / 8);
+  if (n == 0 || batch == 0) return hipSuccess;
+  launch(gather_rows_kernel, dim3((unsigned)((n + 255) / 256), batch), dim3(256), 0, st, src,
+         src_rows, width, pos, n_rows, dst);
+  return hipGetLastError();
+}
+
 }  // namespace ssm

@@ -1,0 +1,117 @@
+"""Attention and row gather on their own (ssm_attention, ssm_gather_rows)
+against the oracle: the attention-and-gather microbenchmark shape (LLaDA-8B
+heads, batch 8, prefix KV of 4096, block 64, kept suffix 176 and the full
+4096) and small ragged shapes.
+
+Tolerance: the kernel rounds the softmax probabilities to bfloat16 before the
+P V product (relative rounding 2^-9 per probability), with scores, softmax
+and accumulation in float32; the oracle is float64 on the same bf16 inputs.
+The relative L2 error of the output is then of order 2^-9; the bound 1e-2
+leaves a factor of five."""
+import numpy as np
+import pytest
+import torch
+
+import oracle.model as OM
+from synthetic.generate import seeded_normal, seeded_uniform_ints
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-2
+
+
+def _inputs(B, H, Hkv, n_q, cap, seed):
+    dev = "cuda"
+    q = seeded_normal((B, H, n_q, 128), seed, "attn.q", device=dev, dtype=torch.bfloat16)
+    k = seeded_normal((B, Hkv, cap, 128), seed, "attn.k", device=dev, dtype=torch.bfloat16)
+    v = seeded_normal((B, Hkv, cap, 128), seed, "attn.v", device=dev, dtype=torch.bfloat16)
+    return q, k, v
+
+
+def _run(q, k, v, n_keys):
+    from paper_2608_23167_amd.api import ssm_attention, ssm_attention_workspace_size
+    B, H, n_q, _ = q.shape
+    out = torch.empty((B, n_q, H * 128), device="cuda", dtype=torch.float32)
+    ws = torch.empty(ssm_attention_workspace_size(B, H, n_q), device="cuda", dtype=torch.uint8)
+    ssm_attention(q, k, v, n_keys, out, ws)
+    torch.cuda.synchronize()
+    return out.cpu().numpy()
+
+
+def _oracle_rows(q, k, v, n_keys, s, rows):
+    """Oracle attention of query rows `rows` of sequence s: [len(rows), H*128]."""
+    qs = q[s, :, rows, :].float().cpu().numpy().astype(np.float64).transpose(1, 0, 2)
+    ks = k[s, :, :n_keys, :].float().cpu().numpy().astype(np.float64).transpose(1, 0, 2)
+    vs = v[s, :, :n_keys, :].float().cpu().numpy().astype(np.float64).transpose(1, 0, 2)
+    return OM.attention(qs, ks, vs)
+
+
+def _rel(a, b):
+    return float(np.linalg.norm(a - b) / np.linalg.norm(b))
+
+
+@pytest.mark.parametrize("B,H,Hkv,n_q,n_keys,cap", [
+    (2, 4, 2, 70, 200, 256),      # GQA, ragged query tile and key tile
+    (1, 2, 2, 1, 1, 8),           # one query, one key
+    (1, 4, 1, 64, 64, 64),        # exact tiles, 4 heads on one KV head
+    (3, 2, 2, 129, 1000, 1030),   # several key tiles: split key ranges and merge
+])
+def test_attention_matches_oracle(gpu, B, H, Hkv, n_q, n_keys, cap):
+    q, k, v = _inputs(B, H, Hkv, n_q, cap, seed=B * 1000 + n_q)
+    got = _run(q, k, v, n_keys)
+    for s in range(B):
+        ref = _oracle_rows(q, k, v, n_keys, s, list(range(n_q)))
+        assert _rel(got[s], ref) < TOL, (s, _rel(got[s], ref))
+
+
+@pytest.mark.parametrize("kept", [176, 4096])
+def test_attention_microbench_shape_sampled(gpu, kept):
+    """Batch 8, 32 heads: prefix 4096 + block 64 + kept suffix rows attend to
+    all prefix, block and kept keys; sampled rows checked against the oracle."""
+    B, H = 8, 32
+    n_q = 64 + kept
+    n_keys = 4096 + 64 + kept
+    q, k, v = _inputs(B, H, H, n_q, n_keys, seed=kept)
+    got = _run(q, k, v, n_keys)
+    rng = np.random.default_rng(kept)
+    for s in (0, 3, 7):
+        rows = sorted(set(rng.integers(0, n_q, size=6).tolist()) | {0, n_q - 1})
+        ref = _oracle_rows(q, k, v, n_keys, s, rows)
+        assert _rel(got[s, rows], ref) < TOL, (s, rows, _rel(got[s, rows], ref))
+
+
+def test_gather_rows_bit_exact(gpu):
+    from paper_2608_23167_amd.api import ssm_gather_rows
+    B, rows, width = 3, 100, 4096
+    src = seeded_normal((B, rows, width), 5, "gather.src", device="cuda", dtype=torch.bfloat16)
+    pos = seeded_uniform_ints((37,), 0, rows, 5, "gather.pos", device="cuda")
+    pos[3] = -1                      # outside the source: zeros
+    pos[10] = rows
+    pos[11] = pos[12]                # repeated position
+    out = torch.empty((B, pos.numel(), width), device="cuda", dtype=torch.bfloat16)
+    ssm_gather_rows(src, pos, out)
+    torch.cuda.synchronize()
+    s_np = src.view(torch.int16).cpu().numpy()
+    p_np = pos.cpu().numpy()
+    ref = np.zeros((B, p_np.size, width), np.int16)
+    ok = (p_np >= 0) & (p_np < rows)
+    ref[:, ok] = s_np[:, p_np[ok]]
+    assert np.array_equal(out.view(torch.int16).cpu().numpy(), ref)
+
+
+def test_gather_rows_microbench_shape(gpu):
+    """The kept suffix rows (local 128, middle 32, tail 16 of 4096) of a
+    [8, 4096, 4096] bf16 tensor."""
+    from paper_2608_23167_amd.api import ssm_gather_rows
+    import oracle.selection as OS
+    B, rows, width = 8, 4096, 4096
+    # prefix 4096, block [4096, 4160), suffix [4160, 8256): kept suffix rows
+    # as indices into the suffix tensor
+    kept = OS.retained_suffix(4096, 64 + rows, 64, 0, 128, 32, 0, 16).positions
+    pos = torch.tensor(np.asarray(kept, np.int32) - 4160, device="cuda")
+    src = seeded_normal((B, rows, width), 6, "gather.big", device="cuda", dtype=torch.bfloat16)
+    out = torch.empty((B, pos.numel(), width), device="cuda", dtype=torch.bfloat16)
+    ssm_gather_rows(src, pos, out)
+    torch.cuda.synchronize()
+    assert pos.numel() == 176
+    assert torch.equal(out, src[:, pos.long()])

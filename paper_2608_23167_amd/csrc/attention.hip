@@ -36,14 +36,15 @@ __device__ __forceinline__ void attn_tile_of(int w, int total, int qtiles, int B
   split = v / (qtiles * BH);
 }
 
-__global__ void __launch_bounds__(256) attn_bf16_kernel(
+template <int QB>
+__global__ void __launch_bounds__(256, 2) attn_bf16_kernel(
     const bf16_t* __restrict__ Q, const bf16_t* __restrict__ Kc, const bf16_t* __restrict__ Vc,
     int H, int Hkv, int Mq, int Nk, int cap, int keys_per_split, float scale_log2,
     ActOut O, float* __restrict__ Opart, float* __restrict__ ML, int qtiles, int BH) {
-  constexpr int DH = 128, KT = 64, KS = DH + 8, VW = 36;    // VW: words per V^T row
-  constexpr int KBUF = KT * KS, VBUF = DH * VW;
+  constexpr int DH = 128, KT = 64, VW = 36;    // VW: words per V^T row
+  constexpr int KBUF = KT * DH, VBUF = DH * VW;
   // two tile buffers: tile i is written while tile i - 1 is read
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[2 * KBUF];
+  __shared__ __attribute__((aligned(1024))) bf16_t Ks[2 * KBUF];
   __shared__ __attribute__((aligned(16))) uint32_t Vt[2 * VBUF];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, c16 = lane & 15;
@@ -51,115 +52,146 @@ __global__ void __launch_bounds__(256) attn_bf16_kernel(
   attn_tile_of(blockIdx.x, gridDim.x, qtiles, BH, qt, bh, split);
   const int s = bh / H, h = bh % H, kvh = h / (H / Hkv);
   const int kb = split * keys_per_split, ke = min(Nk, kb + keys_per_split);
-  const int q = qt * 64 + wave * 16 + c16;
+  // query block b of the wave: rows q0 + 16 b .. + 15; this lane's query in it
+  const int q0 = (qt * 4 + wave) * 16 * QB;
 
   const bf16_t* Qh = Q + (size_t)bh * Mq * DH;
-  bf16x8_t qf[4];
+  bf16x8_t qf[QB][4];
 #pragma unroll
-  for (int kk = 0; kk < 4; ++kk) {
-    if (q < Mq) qf[kk] = *(const bf16x8_t*)(Qh + (size_t)q * DH + 32 * kk + 8 * g);
-    else qf[kk] = __builtin_bit_cast(bf16x8_t, u32x4_t{0u, 0u, 0u, 0u});
+  for (int b = 0; b < QB; ++b) {
+    const int q = q0 + 16 * b + c16;
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      if (q < Mq) qf[b][kk] = *(const bf16x8_t*)(Qh + (size_t)q * DH + 32 * kk + 8 * g);
+      else qf[b][kk] = __builtin_bit_cast(bf16x8_t, u32x4_t{0u, 0u, 0u, 0u});
+    }
   }
   const bf16_t* Kh = Kc + (size_t)(s * Hkv + kvh) * cap * DH;
   const bf16_t* Vh = Vc + (size_t)(s * Hkv + kvh) * cap * DH;
 
-  // tile loader: thread part i covers key (tid + 256 i) / 16 of the tile and
-  // head-dimension chunk (tid % 16) * 8; keys past the range load as zero
-  u32x4_t kr[4], vr[4];
-  auto load_tile = [&](int k0) {
+  // K tile: 64 rows of 256 bytes, the 16-byte chunk j of row r at slot
+  // j ^ (r % 16), copied from global memory straight into LDS (1 KB = 4 rows
+  // per instruction, 4 per wave); keys past the range repeat the last key of
+  // the range (their scores are masked).  Fragment reads of 16 rows at one
+  // chunk then hit 16 different slots.
+  const int krow = 16 * wave + (lane >> 4);
+  auto dma_k = [&](int k0, int buf) {
+    char* dst = (char*)(Ks + buf * KBUF) + wave * 4096;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int key = (tid + 256 * i) >> 4, d8 = tid & 15;
-      kr[i] = u32x4_t{0u, 0u, 0u, 0u};
-      vr[i] = kr[i];
-      if (k0 + key < ke) {
-        kr[i] = *(const u32x4_t*)(Kh + (size_t)(k0 + key) * DH + d8 * 8);
-        vr[i] = *(const u32x4_t*)(Vh + (size_t)(k0 + key) * DH + d8 * 8);
-      }
+      const int r = krow + 4 * i, key = min(k0 + r, ke - 1);
+      const int j = c16 ^ (r & 15);
+      __builtin_amdgcn_global_load_lds((const void*)(Kh + (size_t)key * DH + j * 8),
+                                       (__attribute__((address_space(3))) void*)(dst + i * 1024),
+                                       16, 0, 0);
     }
   };
-  // K rows as they are; V transposed into key-pair words: lanes l and l ^ 16
-  // hold the same chunk of keys 2p and 2p + 1, swap halves, and each writes
-  // four words (the even key's lane dimensions 0-3, the odd key's 4-7)
-  auto store_tile = [&](int buf) {
-    bf16_t* kd = Ks + buf * KBUF;
+  // V: part i covers the key pair p = tid / 16 + 16 i (keys 2p and 2p + 1) at
+  // head-dimension chunk (tid % 16) * 8, so that the thread forms the
+  // transposed key-pair words by itself; keys past the range load as zero
+  const int d8 = tid & 15;
+  u32x4_t vr[2][2];
+  auto load_v = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int o = 0; o < 2; ++o) {
+        const int key = 2 * ((tid >> 4) + 16 * i) + o;
+        vr[i][o] = u32x4_t{0u, 0u, 0u, 0u};
+        if (k0 + key < ke) vr[i][o] = *(const u32x4_t*)(Vh + (size_t)(k0 + key) * DH + d8 * 8);
+      }
+  };
+  // V^T word (d, p) = (key 2p, key 2p + 1) of dimension d
+  auto store_v = [&](int buf) {
     uint32_t* vd = Vt + buf * VBUF;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int key = (tid + 256 * i) >> 4, d8 = tid & 15;
-      *(u32x4_t*)(kd + key * KS + d8 * 8) = kr[i];
-      const bool odd = (lane >> 4) & 1;
-      u32x4_t other;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) other[e] = __shfl_xor(vr[i][e], 16, 64);
-      const u32x4_t lo = odd ? other : vr[i], hi = odd ? vr[i] : other;   // even key, odd key
-      const int p = key >> 1, d0 = d8 * 8 + (odd ? 4 : 0);
+    for (int i = 0; i < 2; ++i) {
+      const int p = (tid >> 4) + 16 * i;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const int dd = (odd ? 4 : 0) + e;   // dimension within the chunk
-        const uint32_t a = dd & 1 ? lo[dd >> 1] >> 16 : lo[dd >> 1] & 0xffffu;
-        const uint32_t b = dd & 1 ? hi[dd >> 1] >> 16 : hi[dd >> 1] & 0xffffu;
-        vd[vt_word(d0 + e, p)] = a | (b << 16);
+        // dims 2e (low halves) and 2e + 1 (high halves) of the two keys
+        vd[vt_word(d8 * 8 + 2 * e, p)] = __builtin_amdgcn_perm(vr[i][1][e], vr[i][0][e], 0x05040100u);
+        vd[vt_word(d8 * 8 + 2 * e + 1, p)] = __builtin_amdgcn_perm(vr[i][1][e], vr[i][0][e], 0x07060302u);
       }
     }
   };
 
-  f32x4_t o[8];
+  f32x4_t o[QB][8];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) o[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  float m_run = -INFINITY, l_run = 0.f;
+  for (int b = 0; b < QB; ++b)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) o[b][i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  float m_run[QB], l_run[QB];
+#pragma unroll
+  for (int b = 0; b < QB; ++b) { m_run[b] = -INFINITY; l_run[b] = 0.f; }
 
-  if (kb < ke) load_tile(kb);
+  if (kb < ke) {
+    dma_k(kb, 0);
+    load_v(kb);
+  }
   int buf = 0;
   for (int k0 = kb; k0 < ke; k0 += KT, buf ^= 1) {
-    // buffer `buf` was last read two tiles ago, before the previous barrier
-    store_tile(buf);
-    if (k0 + KT < ke) load_tile(k0 + KT);   // in flight during this tile
+    // V^T buffer `buf` was last read two tiles ago, before the previous barrier
+    store_v(buf);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's K copy has landed
     __syncthreads();
-    const bf16_t* kd = Ks + buf * KBUF;
+    // the other buffers were last read in the previous tile: refill them
+    if (k0 + KT < ke) {
+      dma_k(k0 + KT, buf ^ 1);
+      load_v(k0 + KT);
+    }
+    const char* kd = (const char*)(Ks + buf * KBUF);
     const uint32_t* vd = Vt + buf * VBUF;
 
-    // S^T block nb: sc[nb][r] = score(key 16nb + 4g + r, query c16)
-    f32x4_t sc[4];
+    // S^T block nb: sc[b][nb][r] = score(key 16nb + 4g + r, query q0 + 16b + c16);
+    // each K fragment read from LDS serves the QB query blocks
+    f32x4_t sc[QB][4];
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb) {
-      sc[nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int b = 0; b < QB; ++b) sc[b][nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) {
-        const bf16x8_t a = *(const bf16x8_t*)(kd + (16 * nb + c16) * KS + 32 * kk + 8 * g);
-        sc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[kk], sc[nb], 0, 0, 0);
+        const bf16x8_t a = *(const bf16x8_t*)(kd + (16 * nb + c16) * 256 + (((4 * kk + g) ^ c16) << 4));
+#pragma unroll
+        for (int b = 0; b < QB; ++b)
+          sc[b][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[b][kk], sc[b][nb], 0, 0, 0);
       }
     }
-    float mt = -INFINITY;
-#pragma unroll
-    for (int nb = 0; nb < 4; ++nb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int key = k0 + 16 * nb + 4 * g + r;
-        const float v = key < ke ? sc[nb][r] * scale_log2 : -INFINITY;
-        sc[nb][r] = v;
-        mt = fmaxf(mt, v);
-      }
-    mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
-    mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-    const float m_new = fmaxf(m_run, mt);
-    const float alpha = exp2f(m_run - m_new);
-    l_run *= alpha;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) o[i] *= alpha;
-
     // P^T operand: slot e of lane group g holds key 32*h2 + 16*(e/4) + 4g + e%4
-    bf16x8_t pb[2];
+    bf16x8_t pb[QB][2];
 #pragma unroll
-    for (int h2 = 0; h2 < 2; ++h2) {
-      uint16_t tmp[8];
+    for (int b = 0; b < QB; ++b) {
+      float mt = -INFINITY;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float p = exp2f(sc[2 * h2 + (e >> 2)][e & 3] - m_new);
-        l_run += p;
-        tmp[e] = f2bf(p);
+      for (int nb = 0; nb < 4; ++nb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int key = k0 + 16 * nb + 4 * g + r;
+          const float v = key < ke ? sc[b][nb][r] * scale_log2 : -INFINITY;
+          sc[b][nb][r] = v;
+          mt = fmaxf(mt, v);
+        }
+      mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
+      mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+      const float m_new = fmaxf(m_run[b], mt);
+      const float alpha = exp2f(m_run[b] - m_new);
+      l_run[b] *= alpha;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) o[b][i] *= alpha;
+#pragma unroll
+      for (int h2 = 0; h2 < 2; ++h2) {
+        float p[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          p[e] = exp2f(sc[b][2 * h2 + (e >> 2)][e & 3] - m_new);
+          l_run[b] += p[e];
+        }
+        const u32x4_t w = {pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]),
+                           pack_bf16x2(p[4], p[5]), pack_bf16x2(p[6], p[7])};
+        pb[b][h2] = __builtin_bit_cast(bf16x8_t, w);
       }
-      pb[h2] = __builtin_bit_cast(bf16x8_t, *(const u32x4_t*)tmp);
+      m_run[b] = m_new;
     }
     // V^T operand: row 16db + c16, keys 32h2 + 4g .. + 3 and 32h2 + 16 + 4g .. + 3
 #pragma unroll
@@ -169,48 +201,52 @@ __global__ void __launch_bounds__(256) attn_bf16_kernel(
         const int d = 16 * db + c16;
         const uint2 lo = *(const uint2*)(vd + vt_word(d, 16 * h2 + 2 * g));
         const uint2 hi = *(const uint2*)(vd + vt_word(d, 16 * h2 + 8 + 2 * g));
-        const u32x4_t a4 = {lo.x, lo.y, hi.x, hi.y};
-        o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a4), pb[h2],
-                                                        o[db], 0, 0, 0);
+        const bf16x8_t a = __builtin_bit_cast(bf16x8_t, u32x4_t{lo.x, lo.y, hi.x, hi.y});
+#pragma unroll
+        for (int b = 0; b < QB; ++b)
+          o[b][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[b][h2], o[b][db], 0, 0, 0);
       }
     }
-    m_run = m_new;
   }
 
-  l_run += __shfl_xor(l_run, 16, 64);
-  l_run += __shfl_xor(l_run, 32, 64);
-  if (q >= Mq) return;
-  // o[db][r] = O^T[dh 16db + 4g + r][query c16]
-  if (Opart == nullptr) {
-    const float inv = 1.0f / l_run;
-    const int row = s * Mq + q;
-    if (O.f32) {
-      float* orow = (float*)O.hi + (size_t)row * O.ld + h * DH + 4 * g;
 #pragma unroll
-      for (int db = 0; db < 8; ++db)
-        *(float4*)(orow + 16 * db) = make_float4(o[db][0] * inv, o[db][1] * inv, o[db][2] * inv,
-                                                 o[db][3] * inv);
-      return;
-    }
+  for (int b = 0; b < QB; ++b) {
+    float l = l_run[b];
+    l += __shfl_xor(l, 16, 64);
+    l += __shfl_xor(l, 32, 64);
+    const int q = q0 + 16 * b + c16;
+    if (q >= Mq) continue;
+    // o[b][db][r] = O^T[dh 16db + 4g + r][query q]
+    if (Opart == nullptr) {
+      const float inv = 1.0f / l;
+      const int row = s * Mq + q;
+      if (O.f32) {
+        float* orow = (float*)O.hi + (size_t)row * O.ld + h * DH + 4 * g;
 #pragma unroll
-    for (int db = 0; db < 8; ++db) {
-      const size_t idx = frag_index(row, h * DH + 16 * db + 4 * g, O.G);   // 4 columns, one chunk
-      uint16_t hi[4], lo[4];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float v = o[db][r] * inv;
-        hi[r] = f2bf(v);
-        lo[r] = f2bf(v - bf2f(hi[r]));
+        for (int db = 0; db < 8; ++db)
+          *(float4*)(orow + 16 * db) = make_float4(o[b][db][0] * inv, o[b][db][1] * inv,
+                                                   o[b][db][2] * inv, o[b][db][3] * inv);
+        continue;
       }
-      *(uint2*)((bf16_t*)O.hi + idx) = *(const uint2*)hi;
-      if (O.lo) *(uint2*)(O.lo + idx) = *(const uint2*)lo;
-    }
-  } else {
-    const size_t row = ((size_t)split * BH + bh) * Mq + q;
-    float* op = Opart + row * DH;
 #pragma unroll
-    for (int db = 0; db < 8; ++db) *(f32x4_t*)(op + 16 * db + 4 * g) = o[db];
-    if (g == 0) { ML[row * 2] = m_run; ML[row * 2 + 1] = l_run; }
+      for (int db = 0; db < 8; ++db) {
+        const size_t idx = frag_index(row, h * DH + 16 * db + 4 * g, O.G);   // 4 columns, one chunk
+        float v[4], r[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = o[b][db][e] * inv;
+        const uint2 hw = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) r[e] = v[e] - bf2f((bf16_t)((e >> 1 ? hw.y : hw.x) >> (16 * (e & 1))));
+        *(uint2*)((bf16_t*)O.hi + idx) = hw;
+        if (O.lo) *(uint2*)(O.lo + idx) = uint2{pack_bf16x2(r[0], r[1]), pack_bf16x2(r[2], r[3])};
+      }
+    } else {
+      const size_t row = ((size_t)split * BH + bh) * Mq + q;
+      float* op = Opart + row * DH;
+#pragma unroll
+      for (int db = 0; db < 8; ++db) *(f32x4_t*)(op + 16 * db + 4 * g) = o[b][db];
+      if (g == 0) { ML[row * 2] = m_run[b]; ML[row * 2 + 1] = l; }
+    }
   }
 }
 
@@ -295,7 +331,10 @@ hipError_t attention(int dtype, const void* q, const void* kc, const void* vc, i
                      hipStream_t st) {
   if (Mq == 0) return hipSuccess;
   const int BH = B * H;
-  const int qtiles = ceil_div(Mq, 64);
+  // bfloat16: 32 query rows per wave (128 per workgroup) once there are more
+  // than 64 rows, which halves the LDS reads per MFMA; float32: 64 per block
+  const int QB = dtype == 1 && Mq > 64 ? 2 : 1;
+  const int qtiles = ceil_div(Mq, 64 * QB);
   // split the key range (whole 64-key tiles) until every split has about two
   // tiles or the grid reaches two workgroups per CU: each workgroup walks its
   // tiles in sequence and hides only the next tile's load, so short ranges
@@ -308,13 +347,17 @@ hipError_t attention(int dtype, const void* q, const void* kc, const void* vc, i
   int kps = ceil_div(key_tiles, S) * 64;
   S = ceil_div(Nk, kps);
   const float scale_log2 = LOG2E / sqrtf((float)dh);
-  dim3 grid(qtiles, BH, S);
   float* opart = S > 1 ? ws.opart : nullptr;
   if (dtype == 1) {
-    launch(attn_bf16_kernel, dim3(qtiles * BH * S), dim3(256), 0, st, (const bf16_t*)q,
-           (const bf16_t*)kc, (const bf16_t*)vc, H, Hkv, Mq, Nk, cap, kps, scale_log2, out, opart,
-           ws.ml, qtiles, BH);
+    const dim3 grid(qtiles * BH * S);
+    if (QB == 2)
+      launch(attn_bf16_kernel<2>, grid, dim3(256), 0, st, (const bf16_t*)q, (const bf16_t*)kc,
+             (const bf16_t*)vc, H, Hkv, Mq, Nk, cap, kps, scale_log2, out, opart, ws.ml, qtiles, BH);
+    else
+      launch(attn_bf16_kernel<1>, grid, dim3(256), 0, st, (const bf16_t*)q, (const bf16_t*)kc,
+             (const bf16_t*)vc, H, Hkv, Mq, Nk, cap, kps, scale_log2, out, opart, ws.ml, qtiles, BH);
   } else {
+    const dim3 grid(qtiles, BH, S);
     const float* qf = (const float*)q;
     const float* kf = (const float*)kc;
     const float* vf = (const float*)vc;

@@ -17,11 +17,30 @@ namespace ssm {
 
 constexpr float LOG2E = 1.4426950408889634f;
 
-// V^T tile in LDS as 32-bit words: word (d, p) holds keys 2p and 2p + 1 of
-// head dimension d.  The key-pair index is XOR-swizzled by 2 * (d / 16), which
-// keeps pairs 2j, 2j + 1 adjacent (8-byte reads stay aligned) and spreads the
-// transposing writes of a wave over all 64 banks.
-__device__ __forceinline__ int vt_word(int d, int p) { return d * 36 + (p ^ ((d >> 4) << 1)); }
+// V^T tile in LDS as 32-bit words, one row of 32 words per head dimension d
+// (row stride 36 words).  Each word holds a pair of consecutive keys; the
+// pair of keys 2p, 2p + 1 (p = 16 h + 8 a + 2 g + c within the 64-key tile)
+// sits at position 16 h + 4 g + 2 a + c, so that the four words at 16 h + 4 g
+// hold keys 32h + 4g .. 32h + 4g + 3 and 32h + 16 + 4g .. + 3: the A operand
+// of one lane of the P V product, read with one 16-byte load.  Positions are
+// XOR-swizzled in whole 4-word groups by (d / 16) % 8, which spreads the
+// transposing writes of a wave over the banks; the 16-byte reads of 16
+// consecutive d are conflict-free without it (row stride 9 x 16 bytes).
+__device__ __forceinline__ int vt_pos(int p) {
+  return (p & 16) + ((p >> 1) & 3) * 4 + ((p >> 3) & 1) * 2 + (p & 1);
+}
+__device__ __forceinline__ int vt_word(int d, int pos) {
+  return d * 36 + (pos ^ (((d >> 4) & 7) << 2));
+}
+
+// Cross-lane maximum over the 4 lanes l, l ^ 16, l ^ 32, l ^ 48 (the lanes
+// that hold the scores of one query) with the gfx950 lane-swap instructions.
+__device__ __forceinline__ float max_lanes_16_32(float v) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
 
 // Workgroup order: a 1-D grid over (query tile, sequence x head, split),
 // query tiles innermost, dealt so that each XCD (workgroup id w runs on XCD
@@ -110,8 +129,10 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         // dims 2e (low halves) and 2e + 1 (high halves) of the two keys
-        vd[vt_word(d8 * 8 + 2 * e, p)] = __builtin_amdgcn_perm(vr[i][1][e], vr[i][0][e], 0x05040100u);
-        vd[vt_word(d8 * 8 + 2 * e + 1, p)] = __builtin_amdgcn_perm(vr[i][1][e], vr[i][0][e], 0x07060302u);
+        vd[vt_word(d8 * 8 + 2 * e, vt_pos(p))] =
+            __builtin_amdgcn_perm(vr[i][1][e], vr[i][0][e], 0x05040100u);
+        vd[vt_word(d8 * 8 + 2 * e + 1, vt_pos(p))] =
+            __builtin_amdgcn_perm(vr[i][1][e], vr[i][0][e], 0x07060302u);
       }
     }
   };
@@ -158,33 +179,40 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(
           sc[b][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[b][kk], sc[b][nb], 0, 0, 0);
       }
     }
+    // softmax in base 2 with the scale folded into one fma per score; keys
+    // past the range (last tile only) are masked to -inf
+    if (k0 + KT > ke) {
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (k0 + 16 * nb + 4 * g + r >= ke)
+#pragma unroll
+            for (int b = 0; b < QB; ++b) sc[b][nb][r] = -INFINITY;
+    }
     // P^T operand: slot e of lane group g holds key 32*h2 + 16*(e/4) + 4g + e%4
     bf16x8_t pb[QB][2];
 #pragma unroll
     for (int b = 0; b < QB; ++b) {
-      float mt = -INFINITY;
+      float mt = sc[b][0][0];
 #pragma unroll
       for (int nb = 0; nb < 4; ++nb)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int key = k0 + 16 * nb + 4 * g + r;
-          const float v = key < ke ? sc[b][nb][r] * scale_log2 : -INFINITY;
-          sc[b][nb][r] = v;
-          mt = fmaxf(mt, v);
-        }
-      mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
-      mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-      const float m_new = fmaxf(m_run[b], mt);
-      const float alpha = exp2f(m_run[b] - m_new);
-      l_run[b] *= alpha;
+        for (int r = 0; r < 4; ++r) mt = fmaxf(mt, sc[b][nb][r]);
+      const float m_new = fmaxf(m_run[b], max_lanes_16_32(mt) * scale_log2);
+      // rescale only when some query of the wave has a new maximum
+      if (__builtin_amdgcn_ballot_w64(m_new > m_run[b]) != 0) {
+        const float alpha = __builtin_amdgcn_exp2f(m_run[b] - m_new);
+        l_run[b] *= alpha;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) o[b][i] *= alpha;
+        for (int i = 0; i < 8; ++i) o[b][i] *= alpha;
+      }
 #pragma unroll
       for (int h2 = 0; h2 < 2; ++h2) {
         float p[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          p[e] = exp2f(sc[b][2 * h2 + (e >> 2)][e & 3] - m_new);
+          p[e] = __builtin_amdgcn_exp2f(fmaf(sc[b][2 * h2 + (e >> 2)][e & 3], scale_log2, -m_new));
           l_run[b] += p[e];
         }
         const u32x4_t w = {pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]),
@@ -199,9 +227,7 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(
 #pragma unroll
       for (int db = 0; db < 8; ++db) {
         const int d = 16 * db + c16;
-        const uint2 lo = *(const uint2*)(vd + vt_word(d, 16 * h2 + 2 * g));
-        const uint2 hi = *(const uint2*)(vd + vt_word(d, 16 * h2 + 8 + 2 * g));
-        const bf16x8_t a = __builtin_bit_cast(bf16x8_t, u32x4_t{lo.x, lo.y, hi.x, hi.y});
+        const bf16x8_t a = *(const bf16x8_t*)(vd + vt_word(d, 16 * h2 + 4 * g));
 #pragma unroll
         for (int b = 0; b < QB; ++b)
           o[b][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[b][h2], o[b][db], 0, 0, 0);

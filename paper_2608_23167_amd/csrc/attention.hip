@@ -16,22 +16,21 @@
 namespace ssm {
 
 constexpr float LOG2E = 1.4426950408889634f;
+typedef short v4i16_t __attribute__((ext_vector_type(4)));
 
-// V^T tile in LDS as 32-bit words, one row of 32 words per head dimension d
-// (row stride 36 words).  Each word holds a pair of consecutive keys; the
-// pair of keys 2p, 2p + 1 (p = 16 h + 8 a + 2 g + c within the 64-key tile)
-// sits at position 16 h + 4 g + 2 a + c, so that the four words at 16 h + 4 g
-// hold keys 32h + 4g .. 32h + 4g + 3 and 32h + 16 + 4g .. + 3: the A operand
-// of one lane of the P V product, read with one 16-byte load.  Positions are
-// XOR-swizzled in whole 4-word groups by (d / 16) % 8, which spreads the
-// transposing writes of a wave over the banks; the 16-byte reads of 16
-// consecutive d are conflict-free without it (row stride 9 x 16 bytes).
-__device__ __forceinline__ int vt_pos(int p) {
-  return (p & 16) + ((p >> 1) & 3) * 4 + ((p >> 3) & 1) * 2 + (p & 1);
-}
-__device__ __forceinline__ int vt_word(int d, int pos) {
-  return d * 36 + (pos ^ (((d >> 4) & 7) << 2));
-}
+// LDS tiles of 64 keys x 128 dimensions, rows of 256 bytes, both copied
+// straight from global memory (global_load_lds, 1 KB = 4 rows per
+// instruction).
+//  * K: the 16-byte chunk j of row r sits at slot j ^ (r % 16); a K fragment
+//    (16 rows at one chunk) then reads 16 different slots.
+//  * V: the 32-byte block j (dimensions 16j .. 16j + 15) of row r sits at
+//    block j ^ (r % 8).  The V^T operand of the P V product is read with the
+//    transposing load ds_read_b64_tr_b16: within a group of 16 lanes, lanes
+//    4r .. 4r + 3 each supply 4 consecutive dimensions of key row r and lane
+//    i receives dimension i of the 4 rows.  A read covers 16 rows x 32 bytes
+//    over 8 block positions, 2 rows each: two passes, the minimum for 512 bytes.
+__device__ __forceinline__ int k_slot(int row, int chunk) { return row * 256 + ((chunk ^ (row & 15)) << 4); }
+__device__ __forceinline__ int v_byte(int row, int block) { return row * 256 + ((block ^ (row & 7)) << 5); }
 
 // Cross-lane maximum over the 4 lanes l, l ^ 16, l ^ 32, l ^ 48 (the lanes
 // that hold the scores of one query) with the gfx950 lane-swap instructions.
@@ -60,11 +59,10 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(
     const bf16_t* __restrict__ Q, const bf16_t* __restrict__ Kc, const bf16_t* __restrict__ Vc,
     int H, int Hkv, int Mq, int Nk, int cap, int keys_per_split, float scale_log2,
     ActOut O, float* __restrict__ Opart, float* __restrict__ ML, int qtiles, int BH) {
-  constexpr int DH = 128, KT = 64, VW = 36;    // VW: words per V^T row
-  constexpr int KBUF = KT * DH, VBUF = DH * VW;
-  // two tile buffers: tile i is written while tile i - 1 is read
-  __shared__ __attribute__((aligned(1024))) bf16_t Ks[2 * KBUF];
-  __shared__ __attribute__((aligned(16))) uint32_t Vt[2 * VBUF];
+  constexpr int DH = 128, KT = 64, TBUF = KT * DH;
+  // two buffers per tile kind: tile i is copied in while tile i - 1 is read
+  __shared__ __attribute__((aligned(1024))) bf16_t Ks[2 * TBUF];
+  __shared__ __attribute__((aligned(1024))) bf16_t Vs[2 * TBUF];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, c16 = lane & 15;
   int qt, bh, split;
@@ -88,52 +86,25 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(
   const bf16_t* Kh = Kc + (size_t)(s * Hkv + kvh) * cap * DH;
   const bf16_t* Vh = Vc + (size_t)(s * Hkv + kvh) * cap * DH;
 
-  // K tile: 64 rows of 256 bytes, the 16-byte chunk j of row r at slot
-  // j ^ (r % 16), copied from global memory straight into LDS (1 KB = 4 rows
-  // per instruction, 4 per wave); keys past the range repeat the last key of
-  // the range (their scores are masked).  Fragment reads of 16 rows at one
-  // chunk then hit 16 different slots.
-  const int krow = 16 * wave + (lane >> 4);
-  auto dma_k = [&](int k0, int buf) {
-    char* dst = (char*)(Ks + buf * KBUF) + wave * 4096;
+  // tile copy: wave w copies rows 16w .. 16w + 15 of the K and V tiles, 4
+  // rows per instruction; lane l covers row 16w + 4i + l / 16 and slot l % 16.
+  // Keys past the range repeat the last key of the range: their scores are
+  // masked, so their probabilities are exactly zero.
+  const int crow = 16 * wave + (lane >> 4);
+  auto copy_tile = [&](int k0, int buf) {
+    char* kdst = (char*)(Ks + buf * TBUF) + wave * 4096;
+    char* vdst = (char*)(Vs + buf * TBUF) + wave * 4096;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int r = krow + 4 * i, key = min(k0 + r, ke - 1);
-      const int j = c16 ^ (r & 15);
-      __builtin_amdgcn_global_load_lds((const void*)(Kh + (size_t)key * DH + j * 8),
-                                       (__attribute__((address_space(3))) void*)(dst + i * 1024),
+      const int r = crow + 4 * i, key = min(k0 + r, ke - 1);
+      const int kc = c16 ^ (r & 15);                                  // K chunk for slot c16
+      const int vc = (((c16 >> 1) ^ (r & 7)) << 1) | (c16 & 1);       // V chunk for slot c16
+      __builtin_amdgcn_global_load_lds((const void*)(Kh + (size_t)key * DH + kc * 8),
+                                       (__attribute__((address_space(3))) void*)(kdst + i * 1024),
                                        16, 0, 0);
-    }
-  };
-  // V: part i covers the key pair p = tid / 16 + 16 i (keys 2p and 2p + 1) at
-  // head-dimension chunk (tid % 16) * 8, so that the thread forms the
-  // transposed key-pair words by itself; keys past the range load as zero
-  const int d8 = tid & 15;
-  u32x4_t vr[2][2];
-  auto load_v = [&](int k0) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int o = 0; o < 2; ++o) {
-        const int key = 2 * ((tid >> 4) + 16 * i) + o;
-        vr[i][o] = u32x4_t{0u, 0u, 0u, 0u};
-        if (k0 + key < ke) vr[i][o] = *(const u32x4_t*)(Vh + (size_t)(k0 + key) * DH + d8 * 8);
-      }
-  };
-  // V^T word (d, p) = (key 2p, key 2p + 1) of dimension d
-  auto store_v = [&](int buf) {
-    uint32_t* vd = Vt + buf * VBUF;
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int p = (tid >> 4) + 16 * i;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        // dims 2e (low halves) and 2e + 1 (high halves) of the two keys
-        vd[vt_word(d8 * 8 + 2 * e, vt_pos(p))] =
-            __builtin_amdgcn_perm(vr[i][1][e], vr[i][0][e], 0x05040100u);
-        vd[vt_word(d8 * 8 + 2 * e + 1, vt_pos(p))] =
-            __builtin_amdgcn_perm(vr[i][1][e], vr[i][0][e], 0x07060302u);
-      }
+      __builtin_amdgcn_global_load_lds((const void*)(Vh + (size_t)key * DH + vc * 8),
+                                       (__attribute__((address_space(3))) void*)(vdst + i * 1024),
+                                       16, 0, 0);
     }
   };
 
@@ -146,23 +117,15 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(
 #pragma unroll
   for (int b = 0; b < QB; ++b) { m_run[b] = -INFINITY; l_run[b] = 0.f; }
 
-  if (kb < ke) {
-    dma_k(kb, 0);
-    load_v(kb);
-  }
+  if (kb < ke) copy_tile(kb, 0);
   int buf = 0;
   for (int k0 = kb; k0 < ke; k0 += KT, buf ^= 1) {
-    // V^T buffer `buf` was last read two tiles ago, before the previous barrier
-    store_v(buf);
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's K copy has landed
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's copies of tile k0
     __syncthreads();
     // the other buffers were last read in the previous tile: refill them
-    if (k0 + KT < ke) {
-      dma_k(k0 + KT, buf ^ 1);
-      load_v(k0 + KT);
-    }
-    const char* kd = (const char*)(Ks + buf * KBUF);
-    const uint32_t* vd = Vt + buf * VBUF;
+    if (k0 + KT < ke) copy_tile(k0 + KT, buf ^ 1);
+    const char* kd = (const char*)(Ks + buf * TBUF);
+    const char* vd = (const char*)(Vs + buf * TBUF);
 
     // S^T block nb: sc[b][nb][r] = score(key 16nb + 4g + r, query q0 + 16b + c16);
     // each K fragment read from LDS serves the QB query blocks
@@ -173,7 +136,7 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(
       for (int b = 0; b < QB; ++b) sc[b][nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) {
-        const bf16x8_t a = *(const bf16x8_t*)(kd + (16 * nb + c16) * 256 + (((4 * kk + g) ^ c16) << 4));
+        const bf16x8_t a = *(const bf16x8_t*)(kd + k_slot(16 * nb + c16, 4 * kk + g));
 #pragma unroll
         for (int b = 0; b < QB; ++b)
           sc[b][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[b][kk], sc[b][nb], 0, 0, 0);
@@ -221,13 +184,22 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(
       }
       m_run[b] = m_new;
     }
-    // V^T operand: row 16db + c16, keys 32h2 + 4g .. + 3 and 32h2 + 16 + 4g .. + 3
+    // V^T operand of lane (g, c16) for dimension block db: dimension
+    // 16db + c16 of keys 32h2 + 4g .. + 3 (transposing read t = 0) and
+    // 32h2 + 16 + 4g .. + 3 (t = 1), the slot order of P^T
+    const int tr_r = c16 >> 2, tr_q = c16 & 3;
 #pragma unroll
     for (int h2 = 0; h2 < 2; ++h2) {
 #pragma unroll
       for (int db = 0; db < 8; ++db) {
-        const int d = 16 * db + c16;
-        const bf16x8_t a = *(const bf16x8_t*)(vd + vt_word(d, 16 * h2 + 4 * g));
+        const int r0 = 32 * h2 + 4 * g + tr_r, r1 = r0 + 16;
+        const v4i16_t t0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) v4i16_t*)(vd + v_byte(r0, db) + tr_q * 8));
+        const v4i16_t t1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) v4i16_t*)(vd + v_byte(r1, db) + tr_q * 8));
+        const bf16x8_t a = __builtin_bit_cast(
+            bf16x8_t, u32x4_t{__builtin_bit_cast(uint2, t0).x, __builtin_bit_cast(uint2, t0).y,
+                              __builtin_bit_cast(uint2, t1).x, __builtin_bit_cast(uint2, t1).y});
 #pragma unroll
         for (int b = 0; b < QB; ++b)
           o[b][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[b][h2], o[b][db], 0, 0, 0);

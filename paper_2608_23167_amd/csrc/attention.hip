@@ -1,16 +1,18 @@
 // Non-causal attention of the compacted rows over every key (cached prefix
 // followed by the rows' own keys), with grouped-query heads.
 //
-// bfloat16 path (head_dim 128): one workgroup = 4 waves = 64 query rows of one
-// (sequence, head); keys stream through two LDS tile buffers of 64 keys, the
-// next tile's loads in flight while the current one is used.  Each wave
-// computes S^T = K Q^T with v_mfma_f32_16x16x32_bf16 so that a lane ends up
-// holding 4 consecutive keys of one query: the exponentiated scores are then
-// already in the operand layout of the P V product, which is computed as
-// O^T = V^T P^T from a transposed V tile.  The softmax is the online
-// (running max / running sum) form, reduced across the 4 lanes that share a
-// query.  Split-KV over the key range fills the GPU at small row counts; a
-// merge kernel combines the per-split (max, sum, output) triples in order.
+// bfloat16 path (head_dim 128): one workgroup = 4 waves of 16 QB query rows
+// of one (sequence, head); QB = 2 once there are more than 64 rows, so that
+// every K and V fragment read from LDS feeds two MFMAs.  Key tiles of 64 are
+// copied from global memory straight into LDS (two buffers per kind).  Each
+// wave computes S^T = K Q^T with v_mfma_f32_16x16x32_bf16, so that a lane ends
+// up holding 4 keys of one query: the exponentiated scores are then already
+// in the B-operand layout of O^T = V^T P^T, whose V^T operand comes from the
+// transposing LDS read.  The online softmax (running max, sum of P as an
+// extra MFMA output block) runs in base 2 in float32; the scores of the next
+// tile are computed while it runs.  Split-KV over the key range fills the GPU
+// at small row counts; a merge kernel combines the per-split (max, sum,
+// output) triples in split order.
 #include "internal.h"
 
 namespace ssm {
@@ -60,7 +62,7 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(
     int H, int Hkv, int Mq, int Nk, int cap, int keys_per_split, float scale_log2,
     ActOut O, float* __restrict__ Opart, float* __restrict__ ML, int qtiles, int BH) {
   constexpr int DH = 128, KT = 64, TBUF = KT * DH;
-  // two buffers per tile kind: tile i is copied in while tile i - 1 is read
+  // two buffers per tile kind
   __shared__ __attribute__((aligned(1024))) bf16_t Ks[2 * TBUF];
   __shared__ __attribute__((aligned(1024))) bf16_t Vs[2 * TBUF];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -69,6 +71,7 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(
   attn_tile_of(blockIdx.x, gridDim.x, qtiles, BH, qt, bh, split);
   const int s = bh / H, h = bh % H, kvh = h / (H / Hkv);
   const int kb = split * keys_per_split, ke = min(Nk, kb + keys_per_split);
+  const int ntile = (ke - kb + KT - 1) / KT;   // >= 1: every split holds a key
   // query block b of the wave: rows q0 + 16 b .. + 15; this lane's query in it
   const int q0 = (qt * 4 + wave) * 16 * QB;
 
@@ -86,50 +89,37 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(
   const bf16_t* Kh = Kc + (size_t)(s * Hkv + kvh) * cap * DH;
   const bf16_t* Vh = Vc + (size_t)(s * Hkv + kvh) * cap * DH;
 
-  // tile copy: wave w copies rows 16w .. 16w + 15 of the K and V tiles, 4
-  // rows per instruction; lane l covers row 16w + 4i + l / 16 and slot l % 16.
+  // tile copy: wave w copies rows 16w .. 16w + 15 of a K or V tile, 4 rows
+  // per instruction; lane l covers row 16w + 4i + l / 16 and slot l % 16.
   // Keys past the range repeat the last key of the range: their scores are
   // masked, so their probabilities are exactly zero.
   const int crow = 16 * wave + (lane >> 4);
-  auto copy_tile = [&](int k0, int buf) {
-    char* kdst = (char*)(Ks + buf * TBUF) + wave * 4096;
-    char* vdst = (char*)(Vs + buf * TBUF) + wave * 4096;
+  auto copy_k = [&](int t, int buf) {
+    char* dst = (char*)(Ks + buf * TBUF) + wave * 4096;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int r = crow + 4 * i, key = min(k0 + r, ke - 1);
-      const int kc = c16 ^ (r & 15);                                  // K chunk for slot c16
-      const int vc = (((c16 >> 1) ^ (r & 7)) << 1) | (c16 & 1);       // V chunk for slot c16
-      __builtin_amdgcn_global_load_lds((const void*)(Kh + (size_t)key * DH + kc * 8),
-                                       (__attribute__((address_space(3))) void*)(kdst + i * 1024),
+      const int r = crow + 4 * i, key = min(kb + t * KT + r, ke - 1);
+      __builtin_amdgcn_global_load_lds((const void*)(Kh + (size_t)key * DH + (c16 ^ (r & 15)) * 8),
+                                       (__attribute__((address_space(3))) void*)(dst + i * 1024),
                                        16, 0, 0);
+    }
+  };
+  auto copy_v = [&](int t, int buf) {
+    char* dst = (char*)(Vs + buf * TBUF) + wave * 4096;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = crow + 4 * i, key = min(kb + t * KT + r, ke - 1);
+      const int vc = (((c16 >> 1) ^ (r & 7)) << 1) | (c16 & 1);
       __builtin_amdgcn_global_load_lds((const void*)(Vh + (size_t)key * DH + vc * 8),
-                                       (__attribute__((address_space(3))) void*)(vdst + i * 1024),
+                                       (__attribute__((address_space(3))) void*)(dst + i * 1024),
                                        16, 0, 0);
     }
   };
 
-  f32x4_t o[QB][8];
-#pragma unroll
-  for (int b = 0; b < QB; ++b)
-#pragma unroll
-    for (int i = 0; i < 8; ++i) o[b][i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  float m_run[QB], l_run[QB];
-#pragma unroll
-  for (int b = 0; b < QB; ++b) { m_run[b] = -INFINITY; l_run[b] = 0.f; }
-
-  if (kb < ke) copy_tile(kb, 0);
-  int buf = 0;
-  for (int k0 = kb; k0 < ke; k0 += KT, buf ^= 1) {
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's copies of tile k0
-    __syncthreads();
-    // the other buffers were last read in the previous tile: refill them
-    if (k0 + KT < ke) copy_tile(k0 + KT, buf ^ 1);
+  // S^T block nb: sc[b][nb][r] = score(key 16nb + 4g + r, query q0 + 16b + c16);
+  // each K fragment read from LDS serves the QB query blocks
+  auto qk = [&](int buf, f32x4_t (&sc)[QB][4]) {
     const char* kd = (const char*)(Ks + buf * TBUF);
-    const char* vd = (const char*)(Vs + buf * TBUF);
-
-    // S^T block nb: sc[b][nb][r] = score(key 16nb + 4g + r, query q0 + 16b + c16);
-    // each K fragment read from LDS serves the QB query blocks
-    f32x4_t sc[QB][4];
 #pragma unroll
     for (int nb = 0; nb < 4; ++nb) {
 #pragma unroll
@@ -142,8 +132,24 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(
           sc[b][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[b][kk], sc[b][nb], 0, 0, 0);
       }
     }
-    // softmax in base 2 with the scale folded into one fma per score; keys
-    // past the range (last tile only) are masked to -inf
+  };
+
+  f32x4_t o[QB][8], ol[QB];   // ol: row sums of P, an extra output block of ones
+  float m_run[QB];
+#pragma unroll
+  for (int b = 0; b < QB; ++b) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) o[b][i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    ol[b] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    m_run[b] = -INFINITY;
+  }
+  const bf16x8_t ones = __builtin_bit_cast(bf16x8_t, u32x4_t{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u});
+
+  // softmax of tile t in base 2, the scale folded into one fma per score;
+  // keys past the range (last tile only) are masked to -inf.  P^T operand:
+  // slot e of lane group g holds key 32*h2 + 16*(e/4) + 4g + e%4.
+  auto softmax = [&](int t, f32x4_t (&sc)[QB][4], bf16x8_t (&pb)[QB][2]) {
+    const int k0 = kb + t * KT;
     if (k0 + KT > ke) {
 #pragma unroll
       for (int nb = 0; nb < 4; ++nb)
@@ -153,8 +159,6 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(
 #pragma unroll
             for (int b = 0; b < QB; ++b) sc[b][nb][r] = -INFINITY;
     }
-    // P^T operand: slot e of lane group g holds key 32*h2 + 16*(e/4) + 4g + e%4
-    bf16x8_t pb[QB][2];
 #pragma unroll
     for (int b = 0; b < QB; ++b) {
       float mt = sc[b][0][0];
@@ -166,7 +170,7 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(
       // rescale only when some query of the wave has a new maximum
       if (__builtin_amdgcn_ballot_w64(m_new > m_run[b]) != 0) {
         const float alpha = __builtin_amdgcn_exp2f(m_run[b] - m_new);
-        l_run[b] *= alpha;
+        ol[b] *= alpha;
 #pragma unroll
         for (int i = 0; i < 8; ++i) o[b][i] *= alpha;
       }
@@ -174,22 +178,27 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(
       for (int h2 = 0; h2 < 2; ++h2) {
         float p[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
+        for (int e = 0; e < 8; ++e)
           p[e] = __builtin_amdgcn_exp2f(fmaf(sc[b][2 * h2 + (e >> 2)][e & 3], scale_log2, -m_new));
-          l_run[b] += p[e];
-        }
         const u32x4_t w = {pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]),
                            pack_bf16x2(p[4], p[5]), pack_bf16x2(p[6], p[7])};
         pb[b][h2] = __builtin_bit_cast(bf16x8_t, w);
       }
       m_run[b] = m_new;
     }
-    // V^T operand of lane (g, c16) for dimension block db: dimension
-    // 16db + c16 of keys 32h2 + 4g .. + 3 (transposing read t = 0) and
-    // 32h2 + 16 + 4g .. + 3 (t = 1), the slot order of P^T
-    const int tr_r = c16 >> 2, tr_q = c16 & 3;
+  };
+
+  // O^T += V^T P^T.  V^T operand of lane (g, c16) for dimension block db:
+  // dimension 16db + c16 of keys 32h2 + 4g .. + 3 (transposing read t = 0)
+  // and 32h2 + 16 + 4g .. + 3 (t = 1), the slot order of P^T
+  const int tr_r = c16 >> 2, tr_q = c16 & 3;
+  auto pv = [&](int buf, const bf16x8_t (&pb)[QB][2]) {
+    const char* vd = (const char*)(Vs + buf * TBUF);
 #pragma unroll
     for (int h2 = 0; h2 < 2; ++h2) {
+#pragma unroll
+      for (int b = 0; b < QB; ++b)
+        ol[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[b][h2], ol[b], 0, 0, 0);
 #pragma unroll
       for (int db = 0; db < 8; ++db) {
         const int r0 = 32 * h2 + 4 * g + tr_r, r1 = r0 + 16;
@@ -205,13 +214,42 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(
           o[b][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[b][h2], o[b][db], 0, 0, 0);
       }
     }
+  };
+
+  {
+    // software pipeline: the scores of tile t + 1 are computed (MFMA) while
+    // the softmax of tile t runs (VALU).  In step t the waves read K of tile
+    // t + 1 and V of tile t while K of tile t + 2 and V of tile t + 1 are
+    // copied into the buffers read in step t - 1; one barrier per step.
+    copy_k(0, 0);
+    copy_v(0, 0);
+    if (ntile > 1) copy_k(1, 1);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    f32x4_t sa[QB][4], sb[QB][4];
+    qk(0, sa);
+    __syncthreads();                                       // K buffer 0 is refilled next
+    auto step = [&](int t, f32x4_t (&cur)[QB][4], f32x4_t (&nxt)[QB][4]) {
+      if (t + 2 < ntile) copy_k(t + 2, t & 1);
+      if (t + 1 < ntile) {
+        copy_v(t + 1, (t + 1) & 1);
+        qk((t + 1) & 1, nxt);
+      }
+      bf16x8_t pb[QB][2];
+      softmax(t, cur, pb);
+      pv(t & 1, pb);
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      __syncthreads();
+    };
+    for (int t = 0; t < ntile; t += 2) {
+      step(t, sa, sb);
+      if (t + 1 < ntile) step(t + 1, sb, sa);
+    }
   }
 
 #pragma unroll
   for (int b = 0; b < QB; ++b) {
-    float l = l_run[b];
-    l += __shfl_xor(l, 16, 64);
-    l += __shfl_xor(l, 32, 64);
+    const float l = ol[b][0];   // every row of the ones block holds the sum
     const int q = q0 + 16 * b + c16;
     if (q >= Mq) continue;
     // o[b][db][r] = O^T[dh 16db + 4g + r][query q]

@@ -38,14 +38,14 @@ METRIC = "denoised tokens/sec + step latency per GPU (LLaDA-8B shape); % MFMA/HB
 # for the kernel sources it was measured on (sha256 of the GEMM sources).
 TRAFFIC = {
     # rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE over `bench.py --steps 32 --warmup 1
-    # --no-profile --no-cpu-baseline`; per-dispatch means of the block-start
-    # launches (180299.2 / 18048.0 KiB) and the cached ones (106571.0 / 5760.0
-    # KiB), weighted 1:31 as in the generation schedule; copy kernel:
-    # 268435456 bytes read and written per launch read as 131085.1 KiB fetched
-    # and 262144.0 KiB written
+    # --no-profile --no-cpu-baseline --no-full-suffix`; per-dispatch means of the
+    # block-start launches (180293.1 / 18048.0 KiB, 64 dispatches) and the cached
+    # ones (106564.5 / 5760.0 KiB, 992 dispatches), weighted 1:31 as in the
+    # generation schedule; copy kernel: 268435456 bytes read and written per
+    # launch read as 131085.1 KiB fetched and 262144.0 KiB written
     ("llada_gen256", "gemm_gate_up"): {
-        "sources_sha256": "d2106e91db15dfc119eec80de3d694921b7feaef98d22f5b5254d348dac21900",
-        "fetch_kib": (180299.2 + 31 * 106571.0) / 32, "write_kib": (18048.0 + 31 * 5760.0) / 32,
+        "sources_sha256": "66a76846dde85b11f142bb8dccb8c7f0562abc5a8a57acb8d69710e312fb17f9",
+        "fetch_kib": (180293.1 + 31 * 106564.5) / 32, "write_kib": (18048.0 + 31 * 5760.0) / 32,
         "fetch_scale": 262144.0 / 131085.1, "write_scale": 1.0},
 }
 GEMM_SOURCES = ("gemm.hip", "internal.h", "common.h")

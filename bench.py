@@ -102,6 +102,9 @@ def main():
                     help="skip the unpruned (full-suffix) decoder run of the same schedule")
     ap.add_argument("--no-profile", action="store_true",
                     help="skip the profiled replay (per-kernel times and roofline), e.g. under counter collection")
+    ap.add_argument("--no-mfma", action="store_true",
+                    help="skip the MFMA report (projections and attention of the LLaDA-8B-shaped "
+                         "generation of length 1024)")
     ap.add_argument("--cpu-layers", type=int, default=None,
                     help="layers of the CPU oracle sample (default: all; fewer are extrapolated)")
     ap.add_argument("--cpu-reps", type=int, default=4,
@@ -258,10 +261,71 @@ def main():
                                  "step_latency_ms": medians(fstep_ms, fkinds),
                                  "ssm_speedup": round(value / fvalue, 3)}
 
+    if not args.no_mfma and shape.dtype == "bf16" and shape == WORKLOADS["llada_long1024"].model:
+        result["mfma"] = mfma_report(dm, dev)
+        print(f"[bench] mfma: {result['mfma']}", file=sys.stderr, flush=True)
+
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, mw, dec, args.cpu_layers or wl.model.n_layers,
                                               args.cpu_reps)
     print(json.dumps(result), flush=True)
+
+
+PROJ_TAGS = ("gemm_qkv", "gemm_o", "gemm_gate_up", "gemm_down")
+
+
+def mfma_report(dm, dev, reps=3):
+    """MFMA throughput of the projections and of attention on the LLaDA-8B-shaped
+    generation of length 1024 (prompt 1024, block 64, budgets 128/32/16, prefix
+    cache): a block-start step of the middle block (every row, prefix included)
+    and a cached step of the same block.  Times are the library's per-launch
+    HIP events summed over each operation (split-K reductions and merges
+    included); flops are algorithmic (2 per multiply-add, attention 4 M N_kv H
+    d_h).  `issued` counts the MFMA instructions actually run: the projections
+    take two passes (bfloat16 hi and lo parts of the activations)."""
+    import torch
+    from synthetic import WORKLOADS, initial_tokens
+    from paper_2608_23167_amd import _lib as L
+    from paper_2608_23167_amd.api import ssm_profile_enable, ssm_profile_query, ssm_select_count
+    from paper_2608_23167_amd.decoder import Decoder
+
+    wl = WORKLOADS["llada_long1024"]
+    sh = wl.model
+    d_, H, Hkv, dh, F = sh.d_model, sh.n_heads, sh.n_kv_heads, sh.head_dim, sh.ffn_dim
+    passes = 2 if dm.c_model.act_mode == L.SSM_ACT_BF16X2 else 1
+    dec = Decoder(wl, dm, device=dev)
+    tok = initial_tokens(wl, device=dev)
+    j = wl.n_blocks // 2
+    out = {"workload": wl.name, "block": j, "peak_tflops": BF16_PEAK_TFLOPS}
+    for kind, first in (("block_start", True), ("cached", False)):
+        dec.reset(tok)
+        dec.step(j, True, unmask=False)          # fills the prefix cache; warm-up
+        dec.step(j, first, unmask=False)
+        torch.cuda.synchronize()
+        ssm_profile_enable(True)
+        for _ in range(reps):
+            dec.step(j, first, unmask=False)
+        torch.cuda.synchronize()
+        ms = {t: ssm_profile_query(t)[1] / reps for t in PROJ_TAGS + ("attention",)}
+        ssm_profile_enable(False)
+        n_rows, _, _ = ssm_select_count(dec.params(j, first))
+        M = wl.batch * n_rows
+        n_keys = n_rows + (0 if first else wl.prompt_len + j * wl.block_size)
+        proj_fl = sh.n_layers * 2.0 * M * d_ * ((H + 2 * Hkv) * dh + d_ + 2 * F + F)
+        attn_fl = sh.n_layers * 4.0 * M * n_keys * H * dh
+        proj_ms = sum(ms[t] for t in PROJ_TAGS)
+        proj_tf = proj_fl / (proj_ms * 1e-3) / 1e12
+        attn_tf = attn_fl / (ms["attention"] * 1e-3) / 1e12
+        out[kind] = {"rows": M, "keys": n_keys,
+                     "proj_ms": round(proj_ms, 3),
+                     "proj_ms_by_kind": {t[5:]: round(ms[t], 3) for t in PROJ_TAGS},
+                     "proj_tflops": round(proj_tf, 1),
+                     "proj_frac": round(proj_tf / BF16_PEAK_TFLOPS, 4),
+                     "proj_issued_frac": round(passes * proj_tf / BF16_PEAK_TFLOPS, 4),
+                     "attn_ms": round(ms["attention"], 3), "attn_tflops": round(attn_tf, 1),
+                     "attn_frac": round(attn_tf / BF16_PEAK_TFLOPS, 4)}
+    del dec
+    return out
 
 
 def attn_sweep(reps=10):

@@ -543,6 +543,142 @@ __global__ void __launch_bounds__(512) gemm_bf16_kernel(Pol pol, const bf16_t* _
 }
 
 // ---------------------------------------------------------------------------
+// bfloat16 MFMA kernel for many rows (block-start steps of long prompts)
+// ---------------------------------------------------------------------------
+// Waits until at most N vector-memory operations of this wave are in flight.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// A BM x BN output tile per workgroup of 8 waves in a WM x WN grid; wave
+// (wm, wn) owns rows (BM / WM) wm .. and columns (BN / WN) wn .. (FM x FN MFMA
+// blocks).  Shapes: 256 x 128 (4 x 2 waves) and 128 x 256 (2 x 4).
+// Both operands go from global memory straight into LDS (global_load_lds,
+// 1 KB per instruction) in K-steps of 32, through a ring of two stages:
+//  * activations: the fragment-order operand already holds each 16-row x
+//    32-column MFMA operand as 1 KB, so a stage is BM / 16 such blocks per
+//    part (hi, lo), copied as they are;
+//  * weights: BN / 16 blocks of 16 rows x 32 columns, lane l of a block
+//    holding row l % 16, columns 8 (l / 16) .. + 7: the B-operand layout.
+// Every operand read is then one conflict-free 16-byte LDS load per lane.
+// With 64-80 KB of LDS and at most 128 VGPRs, two workgroups share a CU, so
+// one workgroup's barrier wait overlaps the other's MFMAs.  The output tile
+// goes through LDS in chunks of EB rows into the same epilogues as
+// gemm_bf16_kernel.
+template <int BM, int BN, int WM, int WN, bool SPLIT, class Pol>
+__global__ void __launch_bounds__(512, 4) gemm_big_kernel(Pol pol, const bf16_t* __restrict__ Ahi,
+                                                          const bf16_t* __restrict__ Alo, int G,
+                                                          int M, int k_per_split, int mt,
+                                                          int n_split, float* __restrict__ part,
+                                                          int ldp) {
+  static_assert(WM * WN == 8, "8 waves");
+  constexpr int BK = 32, NS = 2;
+  constexpr int NA = SPLIT ? 2 : 1;
+  constexpr int GB = BM / 16;                                   // row groups per tile
+  constexpr int A_BLOCKS = GB * NA, BLOCKS = A_BLOCKS + BN / 16;
+  static_assert(BLOCKS % 8 == 0, "whole blocks per wave");
+  constexpr int CPW = BLOCKS / 8, STAGE = BLOCKS * 1024;
+  constexpr int RW = BM / WM, CW = BN / WN, FM = RW / 16, FN = CW / 16;
+  constexpr int CS = BN + 4;
+  constexpr int EB = BN > 128 ? BM / 2 : 128;                   // epilogue chunk rows
+  constexpr int SMEM_W = NS * STAGE, SMEM_C = EB * CS * 4;
+  constexpr int SMEM = SMEM_W > SMEM_C ? SMEM_W : SMEM_C;
+  static_assert(EB % RW == 0, "a wave's rows in one epilogue chunk");
+  __shared__ __attribute__((aligned(1024))) char smem[SMEM];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = wave % WM, wn = wave / WM;
+  int t, mtile, split;
+  tile_of(blockIdx.x, gridDim.x, gridDim.x / n_split, mt, split, t, mtile);
+  const int m0 = mtile * BM;
+  const int kbeg = split * k_per_split, nk = k_per_split / BK, last = nk - 1;
+
+  // this wave's blocks of a stage: block c = wave * CPW + i; c < A_BLOCKS are
+  // activation blocks (part c / GB, row group c % GB), the rest weight blocks
+  const bf16_t *blo, *bhi;
+  pol.b_ptrs(t, BN, blo, bhi);
+  const size_t a_kstep = (size_t)G * 1024;
+  const bf16_t* src[CPW];
+  bool is_a[CPW];
+#pragma unroll
+  for (int i = 0; i < CPW; ++i) {
+    const int c = wave * CPW + i;
+    is_a[i] = c < A_BLOCKS;
+    if (c < A_BLOCKS) {
+      const int grp = min((m0 >> 4) + (c % GB), G - 1);   // groups past the allocation: the last
+      src[i] = ((c / GB) ? Alo : Ahi) + (size_t)(kbeg >> 6) * a_kstep + (size_t)grp * 1024 + lane * 8;
+    } else {
+      const int r = 16 * (c - A_BLOCKS) + (lane & 15);
+      src[i] = (r < BN / 2 ? blo + (size_t)r * pol.ldb : bhi + (size_t)(r - BN / 2) * pol.ldb) +
+               kbeg + 8 * (lane >> 4);
+    }
+  }
+  // K-step ks of the split into the ring slot of K-step kb
+  auto issue = [&](int kb, int ks) {
+    char* dst = smem + (kb % NS) * STAGE + wave * CPW * 1024;
+#pragma unroll
+    for (int i = 0; i < CPW; ++i) {
+      const bf16_t* p = is_a[i] ? src[i] + (size_t)(ks >> 1) * a_kstep + (ks & 1) * 512
+                                : src[i] + (size_t)ks * BK;
+      __builtin_amdgcn_global_load_lds((const void*)p,
+                                       (__attribute__((address_space(3))) void*)(dst + i * 1024),
+                                       16, 0, 0);
+    }
+  };
+  f32x4_t acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  issue(0, 0);
+  wait_vmcnt<0>();
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    // the other slot was last read in step kt - 1, before the last barrier
+    issue(kt + 1, min(kt + 1, last));
+    const char* stg = smem + (kt % NS) * STAGE;
+    bf16x8_t af[NA][FM], wf[FN];
+#pragma unroll
+    for (int p = 0; p < NA; ++p)
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+        af[p][i] = *(const bf16x8_t*)(stg + (p * GB + FM * wm + i) * 1024 + lane * 16);
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+      wf[j] = *(const bf16x8_t*)(stg + (A_BLOCKS + FN * wn + j) * 1024 + lane * 16);
+#pragma unroll
+    for (int p = 0; p < NA; ++p)
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[p][i], wf[j], acc[i][j], 0, 0, 0);
+    wait_vmcnt<0>();                               // this wave's blocks of step kt + 1
+    __syncthreads();                               // all blocks visible; slot kt free
+  }
+  // acc[i][j][r] = C[RW wm + 16 i + 4 (lane / 16) + r][CW wn + 16 j + lane % 16]
+  float* Cs = (float*)smem;
+#pragma unroll
+  for (int h = 0; h < BM / EB; ++h) {
+    if ((RW * wm) / EB == h) {
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            Cs[(RW * wm - h * EB + 16 * i + 4 * (lane >> 4) + r) * CS + CW * wn + 16 * j + (lane & 15)] =
+                acc[i][j][r];
+    }
+    __syncthreads();
+    tile_epilogue<EB, BN, CS>(pol, Cs, m0 + h * EB, M, t, part, split, ldp);
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
 // float32 kernel (fp32 mode): 32x32 tiles, BK = 32, 256 threads, 4 outputs each
 // ---------------------------------------------------------------------------
 template <class Pol>
@@ -647,6 +783,8 @@ static void launch_reduce(const Pol& pol, const float* part, int N, int M, int S
 // ---------------------------------------------------------------------------
 // Split-K is only used while S * M stays small, which bounds the workspace.
 static constexpr int SPLIT_ROWS_MAX = 1024;
+// Row count from which the projections use gemm_big_kernel.
+static constexpr int BIG_ROWS_MIN = 512;
 
 size_t gemm_split_ws_floats(int M, int max_n) {
   (void)M;
@@ -658,18 +796,21 @@ size_t gemm_split_ws_floats(int M, int max_n) {
 // register ring of weight loads.
 struct GemmCfg {
   int bn, s, pw;
+  int big = 0;    // gemm_big_kernel tile: 1 = 256 x 128, 2 = 128 x 256; 0 = gemm_bf16_kernel;
+                  // -1 = automatic
 };
 
-// Tuning override: SSM_GEMM_CFG="kind:bn:s:pw,..." with kind one of qkv, o,
-// gate_up, down, lm; read once per process.
+// Tuning override: SSM_GEMM_CFG="kind:bn:s:pw[:big],..." with kind one of
+// qkv, o, gate_up, down, lm (big as in GemmCfg); read once per process.
 static GemmCfg cfg_override(const char* kind, GemmCfg c) {
   static const char* env = getenv("SSM_GEMM_CFG");
   if (!env) return c;
   const size_t kl = strlen(kind);
   for (const char* p = env; p && *p;) {
     if (strncmp(p, kind, kl) == 0 && p[kl] == ':') {
-      int bn, s, pw;
-      if (sscanf(p + kl + 1, "%d:%d:%d", &bn, &s, &pw) == 3) return GemmCfg{bn, s, pw};
+      int bn, s, pw, big = -1;
+      const int n = sscanf(p + kl + 1, "%d:%d:%d:%d", &bn, &s, &pw, &big);
+      if (n >= 3) return GemmCfg{bn, s, pw, n == 4 ? big : c.big};
     }
     p = strchr(p, ',');
     if (p) ++p;
@@ -720,18 +861,48 @@ static GemmCfg plan_bf16(const char* kind, Pol& pol, int M, int K, int N, GemmCf
                          const SplitWs& ws, int (*bn_ok)(const Pol&, int),
                          void (*rebind)(Pol&, int)) {
   c = cfg_override(kind, c);
-  if (!bn_ok(pol, c.bn) || N % c.bn) c.bn = bn_ok(pol, 128) && N % 128 == 0 ? 128 : 64;
+  // many rows: the big-tile kernel where its shape constraints hold
+  if (c.big < 0) c.big = 0;
+  const int big_bn = c.big == 2 ? 256 : 128;
+  // (the per-head QKV epilogue, the one with a rebind, takes only 128 columns)
+  if (c.big && (M < BIG_ROWS_MIN || has_tile<Pol>::value || !bn_ok(pol, 128) ||
+                (big_bn != 128 && rebind) || N % big_bn != 0 || K % 32 != 0))
+    c.big = 0;
+  if (c.big) c.bn = big_bn;
+  else if (!bn_ok(pol, c.bn) || N % c.bn) c.bn = bn_ok(pol, 128) && N % 128 == 0 ? 128 : 64;
   if (rebind) rebind(pol, c.bn);
-  const int tiles = (N / c.bn) * ceil_div(M, 128);
+  const int tiles = (N / c.bn) * ceil_div(M, c.big == 1 ? 256 : 128);
   int S = c.s > 0 ? c.s : auto_split(tiles, M, K, ws.floats, N);
   while (S > 1 && (K % (256 * S) != 0 || (size_t)S * M * N > ws.floats)) S /= 2;
   c.s = S;
   return c;
 }
 
+template <int BM, int BN, int WM, int WN, class Pol>
+static hipError_t launch_big(const Pol& pol, const ActIn& a, int M, int K, int N, int S,
+                             SplitWs ws, hipStream_t st, bool reduce) {
+  if constexpr (has_tile<Pol>::value) {
+    return hipErrorInvalidValue;   // whole-tile epilogues run on gemm_bf16_kernel only
+  } else {
+    const int ntiles = N / BN, mt = ceil_div(M, BM);
+    const dim3 grid(ntiles * mt * S);
+    float* pp = S > 1 ? ws.part : nullptr;
+    if (a.lo)
+      launch((gemm_big_kernel<BM, BN, WM, WN, true, Pol>), grid, dim3(512), 0, st, pol,
+             (const bf16_t*)a.hi, a.lo, a.G, M, K / S, mt, S, pp, N);
+    else
+      launch((gemm_big_kernel<BM, BN, WM, WN, false, Pol>), grid, dim3(512), 0, st, pol,
+             (const bf16_t*)a.hi, a.lo, a.G, M, K / S, mt, S, pp, N);
+    if (S > 1 && reduce) launch_reduce<BN>(pol, ws.part, N, M, S, ntiles, st);
+    return hipGetLastError();
+  }
+}
+
 template <class Pol>
 static hipError_t launch_plan(const Pol& pol, const ActIn& a, int M, int K, int N, GemmCfg c,
                               SplitWs ws, hipStream_t st, bool reduce = true) {
+  if (c.big == 1) return launch_big<256, 128, 4, 2>(pol, a, M, K, N, c.s, ws, st, reduce);
+  if (c.big == 2) return launch_big<128, 256, 2, 4>(pol, a, M, K, N, c.s, ws, st, reduce);
   if (c.bn == 96) return launch_bf16_pw<96>(pol, a, M, K, N, c.s, c.pw, ws, st, reduce);
   if (c.bn == 64) return launch_bf16_pw<64>(pol, a, M, K, N, c.s, c.pw, ws, st, reduce);
   return launch_bf16_pw<128>(pol, a, M, K, N, c.s, c.pw, ws, st, reduce);
@@ -826,12 +997,17 @@ static hipError_t run_f32(const Pol& pol, const ActIn& a, int M, int K, int N, S
 // Default launch choices: the cached-step row counts (M <= 256) are
 // HBM-bound and want every CU streaming weights; block-start row counts are
 // MFMA-bound and want wide tiles.
+// Measured choices: below 512 rows gemm_bf16_kernel; from 512 rows the big
+// tiles for QKV (256 x 128: a tile stays one head for RoPE) and gate/up
+// (128 x 256), while O and down (N = d) keep gemm_bf16_kernel, whose 128-row
+// tiles fill more CUs there.
 static GemmCfg default_cfg(const char* kind, int M) {
   const bool small = M <= 256;
-  if (!strcmp(kind, "qkv")) return small ? GemmCfg{128, 2, 4} : GemmCfg{128, 1, 3};
-  if (!strcmp(kind, "gate_up")) return small ? GemmCfg{128, 1, 4} : GemmCfg{128, 1, 3};
-  if (!strcmp(kind, "lm")) return GemmCfg{128, 1, 4};
-  return small ? GemmCfg{128, 0, 4} : GemmCfg{128, 0, 3};   // o, down
+  if (!strcmp(kind, "qkv"))   // split-K pays at 120 rows, not at 240
+    return small ? GemmCfg{128, M <= 128 ? 2 : 1, 4, 0} : GemmCfg{128, 1, 3, 1};
+  if (!strcmp(kind, "gate_up")) return small ? GemmCfg{128, 1, 4, 0} : GemmCfg{128, 1, 3, 2};
+  if (!strcmp(kind, "lm")) return GemmCfg{128, 1, 4, 0};
+  return small ? GemmCfg{128, 0, 4, 0} : GemmCfg{128, 0, 3, 0};   // o, down
 }
 
 template <class Pol> static int any_bn(const Pol&, int bn) { return bn == 64 || bn == 96 || bn == 128; }

@@ -39,14 +39,14 @@ METRIC = "denoised tokens/sec + step latency per GPU (LLaDA-8B shape); % MFMA/HB
 TRAFFIC = {
     # rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE over `bench.py --steps 32 --warmup 1
     # --no-profile --no-cpu-baseline --no-full-suffix`; per-dispatch means of the
-    # block-start launches (180293.1 / 18048.0 KiB, 64 dispatches) and the cached
-    # ones (106564.5 / 5760.0 KiB, 992 dispatches), weighted 1:31 as in the
-    # generation schedule; copy kernel: 268435456 bytes read and written per
-    # launch read as 131085.1 KiB fetched and 262144.0 KiB written
+    # block-start launches (180289.7 / 18048.0 KiB, 64 dispatches, grid 294912) and
+    # the cached ones (106561.0 / 5760.0 KiB, 992 dispatches, grid 98304), weighted
+    # 1:31 as in the generation schedule; copy kernel: 268435456 bytes read and
+    # written per launch read as 131085.0 KiB fetched and 262144.0 KiB written
     ("llada_gen256", "gemm_gate_up"): {
-        "sources_sha256": "66a76846dde85b11f142bb8dccb8c7f0562abc5a8a57acb8d69710e312fb17f9",
-        "fetch_kib": (180293.1 + 31 * 106564.5) / 32, "write_kib": (18048.0 + 31 * 5760.0) / 32,
-        "fetch_scale": 262144.0 / 131085.1, "write_scale": 1.0},
+        "sources_sha256": "49bb478e51f817de959c5bfe234d2db0bcc1222cb79a254c2c19bc8b1c636a0c",
+        "fetch_kib": (180289.7 + 31 * 106561.0) / 32, "write_kib": (18048.0 + 31 * 5760.0) / 32,
+        "fetch_scale": 262144.0 / 131085.0, "write_scale": 1.0},
 }
 GEMM_SOURCES = ("gemm.hip", "internal.h", "common.h")
 

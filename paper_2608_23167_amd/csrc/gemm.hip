@@ -449,26 +449,33 @@ __global__ void __launch_bounds__(512) gemm_bf16_kernel(Pol pol, const bf16_t* _
     lds_handover_barrier();                                                           \
   } while (0)
 
-    LOAD_A(a0, 0);
-    LOAD_A(a1, min(1, last));
-    __syncthreads();                               // weight stages 0 and 1 are in LDS
-    READ_W(wf0, 0, 0);
-    for (int kt = 0; kt < nk; kt += 2) {
-      CSTEP(kt, a0);
-      CSTEP(kt + 1, a1);
+    if (m0 + 32 * wave >= M) {
+      // every row of this wave is padding (few rows, e.g. the LM head's
+      // block rows): no loads or MFMAs, only the barrier schedule
+      __syncthreads();
+      for (int kt = 0; kt < nk; ++kt) lds_handover_barrier();
+    } else {
+      LOAD_A(a0, 0);
+      LOAD_A(a1, min(1, last));
+      __syncthreads();                             // weight stages 0 and 1 are in LDS
+      READ_W(wf0, 0, 0);
+      for (int kt = 0; kt < nk; kt += 2) {
+        CSTEP(kt, a0);
+        CSTEP(kt + 1, a1);
+      }
+      // accumulators -> LDS tile: acc[i][j][r] = C[32 wave + 16i + 4*(lane/16) + r][16j + lane%16]
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            Cs[(32 * wave + i * 16 + (lane >> 4) * 4 + r) * CS + j * 16 + (lane & 15)] = acc[i][j][r];
     }
 #undef LOAD_A
 #undef READ_W
 #undef MFMA_H
 #undef CSTEP
-    // accumulators -> LDS tile: acc[i][j][r] = C[32 wave + 16i + 4*(lane/16) + r][16j + lane%16]
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-      for (int j = 0; j < FN; ++j)
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          Cs[(32 * wave + i * 16 + (lane >> 4) * 4 + r) * CS + j * 16 + (lane & 15)] = acc[i][j][r];
   } else {
     // ------------------------------ staging waves ------------------------------
     const bf16_t *blo, *bhi;
@@ -1000,13 +1007,15 @@ static hipError_t run_f32(const Pol& pol, const ActIn& a, int M, int K, int N, S
 // Measured choices: below 512 rows gemm_bf16_kernel; from 512 rows the big
 // tiles for QKV (256 x 128: a tile stays one head for RoPE) and gate/up
 // (128 x 256), while O and down (N = d) keep gemm_bf16_kernel, whose 128-row
-// tiles fill more CUs there.
+// tiles fill more CUs there.  Up to 128 rows, O takes 64-column tiles and
+// split-K 4, which halves the float32 partials of the 8-way split.
 static GemmCfg default_cfg(const char* kind, int M) {
   const bool small = M <= 256;
   if (!strcmp(kind, "qkv"))   // split-K pays at 120 rows, not at 240
     return small ? GemmCfg{128, M <= 128 ? 2 : 1, 4, 0} : GemmCfg{128, 1, 3, 1};
   if (!strcmp(kind, "gate_up")) return small ? GemmCfg{128, 1, 4, 0} : GemmCfg{128, 1, 3, 2};
   if (!strcmp(kind, "lm")) return GemmCfg{128, 1, 4, 0};
+  if (!strcmp(kind, "o") && M <= 128) return GemmCfg{64, 4, 4, 0};
   return small ? GemmCfg{128, 0, 4, 0} : GemmCfg{128, 0, 3, 0};   // o, down
 }
 

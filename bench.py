@@ -390,10 +390,112 @@ def attn_sweep(reps=10):
                        "gather_frac": round(g_bytes / (t_g * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)})
         print(f"[bench] sweep {pt}", file=sys.stderr, flush=True)
         points.append(pt)
+    small = small_kernels_micro(dev, reps)
+    print(f"[bench] sweep small kernels {small}", file=sys.stderr, flush=True)
     print(json.dumps({"metric": "attention and gather per layer vs kept-suffix count "
                                 "(LLaDA-8B heads, batch 8, prefix 4096, block 64, suffix 4096)",
                       "unit": "us", "n_gpus": 1, "dtype": "bf16", "data": "synthetic N(0,1) Q/K/V",
-                      "points": points}), flush=True)
+                      "points": points, "small_kernels": small}), flush=True)
+
+
+def small_kernels_micro(dev, reps=10):
+    """Selection + gather of token ids (a1, a2), soft embedding (a3) and unmask +
+    state scatter (a7, a8) at the microbenchmark's scale: batch 8, prefix 4096,
+    block 64, suffix 4096 with budgets 128/32/16 (176 kept rows), LLaDA-8B
+    embedding table (126464 x 4096 bf16), top-5 state, top-8 unmasking.  A
+    block-start step (prefix rows included: 4336 rows) and a cached step (block
+    and kept rows: 240) of block 0.  Times are the library's per-launch HIP
+    events (kernel only, no host work).  Bytes are algorithmic: the embedding
+    counts each distinct table row once."""
+    import ctypes as C
+    import numpy as np
+    import torch
+    from synthetic import WORKLOADS
+    from synthetic.generate import mid_generation_state
+    from paper_2608_23167_amd import _lib as L
+    from paper_2608_23167_amd.api import (ssm_embed_suffix, ssm_profile_enable, ssm_profile_query,
+                                          ssm_select_suffix, ssm_unmask)
+
+    wl = WORKLOADS["attn_micro"]
+    sh = wl.model
+    B, d, V, k, blk = wl.batch, sh.d_model, sh.vocab, wl.topk, wl.block_size
+    t_np, pi_np, pw_np, ps_np = mid_generation_state(wl, 0, 1, seed=0)
+    tokens = torch.from_numpy(t_np).to(dev)
+    pred_ids = torch.from_numpy(pi_np).to(dev)
+    pred_w = torch.from_numpy(pw_np).to(dev)
+    pred_step = torch.from_numpy(ps_np).to(dev)
+    emb = (torch.randn((V, d), device=dev) * 0.02).to(torch.bfloat16)
+    fake = torch.zeros(d, device=dev, dtype=torch.bfloat16)
+
+    class _Emb:   # an embedding-table-only model description (no layers)
+        c_model = L.Model(0, d, sh.n_heads, sh.n_kv_heads, sh.head_dim, sh.ffn_dim, V, sh.mask_id,
+                          L.SSM_DT_BF16, float(sh.rope_base), float(sh.rms_eps), emb.data_ptr(),
+                          fake.data_ptr(), emb.data_ptr(), C.cast(None, C.POINTER(L.Layer)),
+                          L.SSM_ACT_BF16X2)
+
+    def kernel_us(tag, fn):
+        fn()
+        torch.cuda.synchronize()
+        ssm_profile_enable(True)
+        for _ in range(reps):
+            fn()
+        torch.cuda.synchronize()
+        n, ms = ssm_profile_query(tag)
+        ssm_profile_enable(False)
+        return ms / max(n, 1) * 1e3
+
+    def rate(nbytes, us):
+        gbs = nbytes / (us * 1e-6) / 1e9
+        return {"us": round(us, 2), "bytes": int(nbytes), "gbs": round(gbs, 1),
+                "frac": round(gbs / HBM_PEAK_GBS, 4)}
+
+    out = {}
+    cap = wl.total_len
+    for kind, incl in (("block_start", True), ("cached", False)):
+        prm = select_params_of(wl, 0, incl)
+        pos = torch.empty(cap, device=dev, dtype=torch.int32)
+        tok_c = torch.empty((B, cap), device=dev, dtype=torch.int32)
+        region = torch.empty(cap, device=dev, dtype=torch.int8)
+        n_rows, n_suf, first = ssm_select_suffix(prm, tokens, pos, tok_c, region)
+        t_sel = kernel_us("select", lambda: ssm_select_suffix(prm, tokens, pos, tok_c, region))
+        sel_bytes = B * n_rows * 4 * 2 + n_rows * 5          # ids gathered and written; pos, region
+        x = torch.empty((B, n_rows, d), device=dev, dtype=torch.float32)
+        t_emb = kernel_us("embed", lambda: ssm_embed_suffix(_Emb, tok_c, pos, region, n_rows,
+                                                            pred_ids, pred_w, pred_step, 0, k,
+                                                            wl.alpha, x))
+        # distinct table rows the step needs, and the soft rows' state
+        pos_h = pos[:n_rows].cpu().numpy()
+        reg_h = region[:n_rows].cpu().numpy()
+        tok_h = tok_c[:, :n_rows].cpu().numpy()
+        soft = (reg_h[None, :] >= 2) & (ps_np[:, pos_h] == 0)
+        rows = set(np.unique(tok_h[~soft]).tolist())
+        if soft.any():
+            rows |= set(np.unique(pi_np[:, pos_h][soft]).tolist()) | {sh.mask_id}
+        emb_bytes = len(rows) * d * 2 + int(soft.sum()) * k * 8 + B * n_rows * d * 4
+        n_out = n_rows - first
+        argmax = torch.randint(0, V - 1, (B * n_out,), device=dev, dtype=torch.int32)
+        conf = torch.rand(B * n_out, device=dev)
+        topk_ids = torch.randint(0, V - 1, (B * n_out * k,), device=dev, dtype=torch.int32)
+        topk_w = torch.rand(B * n_out * k, device=dev)
+        selected = torch.zeros(B * blk, device=dev, dtype=torch.uint8)
+        left = torch.zeros(B, device=dev, dtype=torch.int32)
+        tok_work = tokens.clone()
+        pos_out = pos[first:n_rows]
+        t_unm = kernel_us("unmask", lambda: ssm_unmask(
+            tok_work, wl.prompt_len, blk, sh.mask_id, L.SSM_UNMASK_TOPN, wl.n_per_step, 0.9,
+            argmax, conf, topk_ids, topk_w, k, n_out, pos_out, 1, pred_ids, pred_w, pred_step,
+            selected, left))
+        unm_bytes = B * n_out * (8 + k * 8) + B * blk * 8 + B * n_suf * (k * 8 + 4)
+        out[kind] = {"rows": n_rows, "kept": n_suf, "select": rate(sel_bytes, t_sel),
+                     "embed": rate(emb_bytes, t_emb), "embed_table_rows": len(rows),
+                     "unmask": rate(unm_bytes, t_unm)}
+    return out
+
+
+def select_params_of(wl, block_idx, include_prefix):
+    from paper_2608_23167_amd.api import select_params
+    return select_params(wl.prompt_len, wl.gen_len, wl.block_size, block_idx, wl.local_budget,
+                         wl.middle_budget, wl.middle_mode, wl.tail_budget, include_prefix)
 
 
 def cpu_baseline(wl, mw, dec, n_layers_sample, reps):

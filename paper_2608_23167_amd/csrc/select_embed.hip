@@ -97,6 +97,88 @@ __global__ void __launch_bounds__(256) embed_kernel(
   }
 }
 
+// Vector form for d a multiple of 8 and 16-byte aligned tables and output:
+// thread t handles columns 8c .. 8c + 7 (c = t, t + 256, ...), 16-byte table
+// loads and two 16-byte stores; per element the same arithmetic in the same
+// order as embed_kernel.
+__device__ __forceinline__ void load8f(const bf16_t* p, float (&v)[8]) {
+  const u32x4_t w = *(const u32x4_t*)p;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    v[2 * j] = __uint_as_float(w[j] << 16);
+    v[2 * j + 1] = __uint_as_float(w[j] & 0xffff0000u);
+  }
+}
+__device__ __forceinline__ void load8f(const float* p, float (&v)[8]) {
+  const float4 a = ((const float4*)p)[0], b = ((const float4*)p)[1];
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+  v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+
+template <typename T>
+__global__ void __launch_bounds__(256) embed8_kernel(
+    const T* __restrict__ E, int d, int vocab, int mask_id, int seq_len,
+    const int32_t* __restrict__ tok_c, int tok_stride, const int32_t* __restrict__ pos,
+    const int8_t* __restrict__ region, int n_rows, const int32_t* __restrict__ pred_ids,
+    const float* __restrict__ pred_w, const int32_t* __restrict__ pred_step, int prev_step, int k,
+    float alpha, float* __restrict__ x) {
+  const int r = blockIdx.x, s = blockIdx.y, d8 = d >> 3;
+  float* out = x + ((size_t)s * n_rows + r) * d;
+  const int p = pos[r];
+  const bool pos_ok = p >= 0 && p < seq_len;
+  const size_t sp = (size_t)s * seq_len + (pos_ok ? p : 0);
+  const bool soft = pos_ok && region[r] >= 2 && prev_step >= 0 && pred_step[sp] == prev_step;
+  const float qnan = __builtin_nanf("");
+  if (!soft) {
+    const int tok = tok_c[(size_t)s * tok_stride + r];
+    const bool ok = pos_ok && tok >= 0 && tok < vocab;
+    const T* e = E + (size_t)(ok ? tok : 0) * d;
+    for (int c = threadIdx.x; c < d8; c += blockDim.x) {
+      float v[8];
+      load8f(e + 8 * c, v);
+      if (!ok) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = qnan;
+      }
+      ((float4*)(out + 8 * c))[0] = make_float4(v[0], v[1], v[2], v[3]);
+      ((float4*)(out + 8 * c))[1] = make_float4(v[4], v[5], v[6], v[7]);
+    }
+    return;
+  }
+  int ids[8];
+  float w[8];
+  bool ok = true;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    ids[i] = 0;
+    w[i] = 0.f;
+    if (i < k) {
+      ids[i] = pred_ids[sp * k + i];
+      w[i] = pred_w[sp * k + i];
+      ok = ok && ids[i] >= 0 && ids[i] < vocab;
+    }
+  }
+  const T* em = E + (size_t)mask_id * d;
+  for (int c = threadIdx.x; c < d8; c += blockDim.x) {
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};   // Eq. 7, in the stored order
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      if (i < k) {
+        float e[8];
+        load8f(E + (size_t)(ok ? ids[i] : 0) * d + 8 * c, e);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[j] = acc[j] + w[i] * e[j];
+      }
+    }
+    float m[8], v[8];
+    load8f(em + 8 * c, m);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = ok ? (1.0f - alpha) * m[j] + alpha * acc[j] : qnan;   // Eq. 8
+    ((float4*)(out + 8 * c))[0] = make_float4(v[0], v[1], v[2], v[3]);
+    ((float4*)(out + 8 * c))[1] = make_float4(v[4], v[5], v[6], v[7]);
+  }
+}
+
 hipError_t launch_embed(int dtype, const void* E, int d, int vocab, int mask_id, int batch,
                         int seq_len, const int32_t* tok_c, int tok_stride, const int32_t* pos,
                         const int8_t* region, int n_rows, const int32_t* pred_ids,
@@ -104,7 +186,16 @@ hipError_t launch_embed(int dtype, const void* E, int d, int vocab, int mask_id,
                         float alpha, float* x, hipStream_t st) {
   if (n_rows == 0) return hipSuccess;
   dim3 grid(n_rows, batch);
-  if (dtype == 0)
+  const bool vec = d % 8 == 0 && ((uintptr_t)E & 15) == 0 && ((uintptr_t)x & 15) == 0;
+  if (vec && dtype == 0)
+    launch(embed8_kernel<float>, grid, dim3(256), 0, st, (const float*)E, d, vocab, mask_id,
+           seq_len, tok_c, tok_stride, pos, region, n_rows, pred_ids, pred_w, pred_step,
+           prev_step, k, alpha, x);
+  else if (vec)
+    launch(embed8_kernel<bf16_t>, grid, dim3(256), 0, st, (const bf16_t*)E, d, vocab, mask_id,
+           seq_len, tok_c, tok_stride, pos, region, n_rows, pred_ids, pred_w, pred_step,
+           prev_step, k, alpha, x);
+  else if (dtype == 0)
     launch(embed_kernel<float>, grid, dim3(256), 0, st, (const float*)E, d, vocab,
                        mask_id, seq_len, tok_c, tok_stride, pos, region, n_rows, pred_ids, pred_w,
                        pred_step, prev_step, k, alpha, x);

@@ -98,6 +98,10 @@ def main():
                     help="instead of the decoding bench: the attention/gather microbenchmark "
                          "(LLaDA-8B heads, batch 8, prefix 4096, block 64, suffix 4096) over the "
                          "kept-suffix count")
+    ap.add_argument("--gen-sweep", action="store_true",
+                    help="instead of the decoding bench: whole generations of the LLaDA-8B shape "
+                         "(prompt 1024, block 64, top-8, budgets 128/32/16, prefix cache) at "
+                         "generation lengths 256 .. 2048, SSM and unpruned")
     ap.add_argument("--no-full-suffix", action="store_true",
                     help="skip the unpruned (full-suffix) decoder run of the same schedule")
     ap.add_argument("--no-profile", action="store_true",
@@ -118,6 +122,9 @@ def main():
 
     if args.attn_sweep:
         attn_sweep()
+        return
+    if args.gen_sweep:
+        gen_sweep()
         return
 
     import numpy as np
@@ -326,6 +333,54 @@ def mfma_report(dm, dev, reps=3):
                      "attn_frac": round(attn_tf / BF16_PEAK_TFLOPS, 4)}
     del dec
     return out
+
+
+def gen_sweep():
+    """Tokens/s and step latency of whole generations vs generation length, SSM
+    and the unpruned decoder (every suffix token kept), on one set of LLaDA-8B
+    weights: prompt 1024, block 64, top-8 per step, budgets 128/32/16, prefix
+    cache, batch 1.  One warm-up generation per point; one JSON line."""
+    import torch
+    from synthetic import WORKLOADS, initial_tokens, make_weights
+    from paper_2608_23167_amd.decoder import Decoder
+    from paper_2608_23167_amd.model import DeviceModel
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    base = WORKLOADS["llada_long2048"]
+    mw = make_weights(base.model, seed=base.seed, device=dev)
+    dm = DeviceModel(base.model, mw)
+    points = []
+    for G in (256, 512, 1024, 2048):
+        wl = base.replace(gen_len=G)
+        pt = {"gen_len": G}
+        for name, w in (("ssm", wl), ("full", wl.replace(local_budget=G, middle_budget=0,
+                                                         tail_budget=0))):
+            dec = Decoder(w, dm, device=dev)
+            tok0 = initial_tokens(w, device=dev)
+            sched = dec.schedule()
+
+            def gen():
+                dec.reset(tok0)
+                for j, first in sched:
+                    dec.step(j, first)
+            gen()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            gen()
+            torch.cuda.synchronize()
+            wall = time.perf_counter() - t0
+            pt[name] = {"seconds": round(wall, 4), "tokens_per_s": round(G / wall, 1),
+                        "steps": len(sched), "ms_per_step": round(wall / len(sched) * 1e3, 3)}
+            del dec
+            torch.cuda.empty_cache()
+        pt["ssm_speedup"] = round(pt["full"]["seconds"] / pt["ssm"]["seconds"], 3)
+        print(f"[bench] gen sweep {pt}", file=sys.stderr, flush=True)
+        points.append(pt)
+    print(json.dumps({"metric": "whole-generation tokens/s vs generation length, SSM and unpruned "
+                                "(LLaDA-8B shape, prompt 1024, block 64, top-8, budgets 128/32/16)",
+                      "unit": "tokens/s", "n_gpus": 1, "dtype": "bf16",
+                      "data": "synthetic (seeded random-init weights, uniform random prompt ids)",
+                      "points": points}), flush=True)
 
 
 def attn_sweep(reps=10):

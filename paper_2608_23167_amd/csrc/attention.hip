@@ -146,9 +146,13 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(
   const bf16x8_t ones = __builtin_bit_cast(bf16x8_t, u32x4_t{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u});
 
   // softmax of tile t in base 2, the scale folded into one fma per score;
-  // keys past the range (last tile only) are masked to -inf.  P^T operand:
-  // slot e of lane group g holds key 32*h2 + 16*(e/4) + 4g + e%4.
-  auto softmax = [&](int t, f32x4_t (&sc)[QB][4], bf16x8_t (&pb)[QB][2]) {
+  // keys past the range (last tile only) are masked to -inf.  The running
+  // maximum is lazy: it moves (and O and the row sums are rescaled) only when
+  // some query of the wave sees a score above it by more than RESCALE (log2
+  // units), so the probabilities stay below 2^RESCALE; the result is exact
+  // after the final division by the row sum either way.
+  constexpr float RESCALE = 8.0f;
+  auto softmax_max = [&](int t, f32x4_t (&sc)[QB][4]) {
     const int k0 = kb + t * KT;
     if (k0 + KT > ke) {
 #pragma unroll
@@ -166,26 +170,31 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(
       for (int nb = 0; nb < 4; ++nb)
 #pragma unroll
         for (int r = 0; r < 4; ++r) mt = fmaxf(mt, sc[b][nb][r]);
-      const float m_new = fmaxf(m_run[b], max_lanes_16_32(mt) * scale_log2);
-      // rescale only when some query of the wave has a new maximum
-      if (__builtin_amdgcn_ballot_w64(m_new > m_run[b]) != 0) {
+      const float m_tile = max_lanes_16_32(mt) * scale_log2;
+      if (__builtin_amdgcn_ballot_w64(m_tile > m_run[b] + RESCALE) != 0) {
+        const float m_new = fmaxf(m_run[b], m_tile);
         const float alpha = __builtin_amdgcn_exp2f(m_run[b] - m_new);
         ol[b] *= alpha;
 #pragma unroll
         for (int i = 0; i < 8; ++i) o[b][i] *= alpha;
+        m_run[b] = m_new;
       }
+    }
+  };
+  // P^T operand: slot e of lane group g holds key 32*h2 + 16*(e/4) + 4g + e%4
+  auto softmax_exp = [&](const f32x4_t (&sc)[QB][4], bf16x8_t (&pb)[QB][2]) {
+#pragma unroll
+    for (int b = 0; b < QB; ++b)
 #pragma unroll
       for (int h2 = 0; h2 < 2; ++h2) {
         float p[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e)
-          p[e] = __builtin_amdgcn_exp2f(fmaf(sc[b][2 * h2 + (e >> 2)][e & 3], scale_log2, -m_new));
+          p[e] = __builtin_amdgcn_exp2f(fmaf(sc[b][2 * h2 + (e >> 2)][e & 3], scale_log2, -m_run[b]));
         const u32x4_t w = {pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]),
                            pack_bf16x2(p[4], p[5]), pack_bf16x2(p[6], p[7])};
         pb[b][h2] = __builtin_bit_cast(bf16x8_t, w);
       }
-      m_run[b] = m_new;
-    }
   };
 
   // O^T += V^T P^T.  V^T operand of lane (g, c16) for dimension block db:
@@ -231,12 +240,13 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(
     __syncthreads();                                       // K buffer 0 is refilled next
     auto step = [&](int t, f32x4_t (&cur)[QB][4], f32x4_t (&nxt)[QB][4]) {
       if (t + 2 < ntile) copy_k(t + 2, t & 1);
-      if (t + 1 < ntile) {
-        copy_v(t + 1, (t + 1) & 1);
-        qk((t + 1) & 1, nxt);
-      }
+      if (t + 1 < ntile) copy_v(t + 1, (t + 1) & 1);
+      softmax_max(t, cur);
+      // one branch-free block: the next tile's score MFMAs interleave with
+      // this tile's exponentials
+      if (t + 1 < ntile) qk((t + 1) & 1, nxt);
       bf16x8_t pb[QB][2];
-      softmax(t, cur, pb);
+      softmax_exp(cur, pb);
       pv(t & 1, pb);
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       __syncthreads();

@@ -17,10 +17,12 @@ from tests._parity import (check_decisions, check_unmask, gpu_step, load_oracle_
 
 pytestmark = pytest.mark.gpu
 
-def _decoder(wl, mw_dev):
+def _decoder(wl, mw_dev, act_mode=None):
+    from paper_2608_23167_amd import _lib as L
     from paper_2608_23167_amd.decoder import Decoder
     from paper_2608_23167_amd.model import DeviceModel
-    return Decoder(wl, DeviceModel(wl.model, mw_dev))
+    mode = L.SSM_ACT_BF16X2 if act_mode is None else act_mode
+    return Decoder(wl, DeviceModel(wl.model, mw_dev, act_mode=mode))
 
 
 def _compare_step(out, rec, wl, fp32: bool):
@@ -97,12 +99,12 @@ def _state_from(wl, block_idx, step, seed):
     return st
 
 
-def _bf16_case(wl, blocks, seed=0):
+def _bf16_case(wl, blocks, seed=0, act_mode=None):
     torch.manual_seed(0)
     mw_dev = make_weights(wl.model, seed=seed, device="cuda", norm_jitter=0.1,
                           logit_scale=wl.logit_scale)
     w = OG.NumpyWeights(mw_dev, dtype=np.float32)
-    dec = _decoder(wl, mw_dev)
+    dec = _decoder(wl, mw_dev, act_mode)
     fracs = []
     for j, n_steps in blocks:
         st = _state_from(wl, j, 5 + 3 * j, seed)
@@ -134,3 +136,14 @@ def test_llada_long_shape_2_layers_bf16(gpu):
     wl = sharpened(WORKLOADS["llada_long2048"], 30.0)
     wl = wl.replace(model=wl.model.with_layers(2))
     _bf16_case(wl, [(0, 2), (31, 2)])
+
+
+def test_llada_long_shape_2_layers_single_bf16_activations(gpu):
+    """SSM_ACT_BF16 (projection inputs rounded once to bfloat16, one MFMA pass):
+    the 1264-row block-start step runs the big-tile GEMM without the lo part,
+    the 240-row cached step the 128-row kernel without it.  Two layers keep the
+    single rounding well inside the bound."""
+    from paper_2608_23167_amd import _lib as L
+    wl = sharpened(WORKLOADS["llada_long2048"], 30.0)
+    wl = wl.replace(model=wl.model.with_layers(2))
+    _bf16_case(wl, [(0, 2)], act_mode=L.SSM_ACT_BF16)

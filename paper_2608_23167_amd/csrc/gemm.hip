@@ -1088,8 +1088,8 @@ __global__ void __launch_bounds__(256) lm_merge_kernel(const LMPartial* __restri
                                                        float* __restrict__ conf,
                                                        int32_t* __restrict__ topk_ids,
                                                        float* __restrict__ topk_w) {
-  __shared__ float s_m[256];
-  __shared__ float s_s[256];
+  __shared__ float s_m[4];
+  __shared__ float s_s[4];
   __shared__ float s_v[4];
   __shared__ int s_i[4];
   const int row = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -1105,23 +1105,31 @@ __global__ void __launch_bounds__(256) lm_merge_kernel(const LMPartial* __restri
       if (p.m > mx) { sm = sm * expf(mx - p.m) + p.s; mx = p.m; }
       else sm += p.s * expf(p.m - mx);
     }
+    // a partial's values are sorted best first: stop at the first one that
+    // does not enter this thread's list
+    for (int q = 0; q < 8; ++q) {
+      if (!stat_better(p.v[q], p.id[q], tv[7], ti[7])) break;
+      stat_insert(tv, ti, p.v[q], p.id[q]);
+    }
+  }
+  // (max, sum) pairs over the workgroup: a butterfly within each wave (both
+  // partners compute the same sum, in either order), then the 4 waves in order
+  auto combine = [](float& m, float& s, float om, float os) {
+    if (!(os > 0.f)) return;
+    if (!(s > 0.f)) { m = om; s = os; return; }
+    const float M = fmaxf(m, om);
+    s = s * expf(m - M) + os * expf(om - M);
+    m = M;
+  };
 #pragma unroll
-    for (int q = 0; q < 8; ++q)
-      if (stat_better(p.v[q], p.id[q], tv[7], ti[7])) stat_insert(tv, ti, p.v[q], p.id[q]);
+  for (int o = 32; o > 0; o >>= 1) {
+    const float om = __shfl_xor(mx, o, 64), os = __shfl_xor(sm, o, 64);
+    combine(mx, sm, om, os);
   }
-  s_m[tid] = mx;
-  s_s[tid] = sm;
+  if (lane == 0) { s_m[wave] = mx; s_s[wave] = sm; }
   __syncthreads();
-  if (tid == 0) {
-    float M = -INFINITY;
-    for (int t = 0; t < 256; ++t) M = fmaxf(M, s_m[t]);
-    float S = 0.f;
-    for (int t = 0; t < 256; ++t)
-      if (s_s[t] > 0.f) S += s_s[t] * expf(s_m[t] - M);
-    s_s[0] = S;
-  }
-  __syncthreads();
-  const float S = s_s[0];
+  float M = s_m[0], S = s_s[0];
+  for (int w = 1; w < 4; ++w) combine(M, S, s_m[w], s_s[w]);
   float best_v[8];
   int best_i[8];
   for (int q = 0; q < 8; ++q) {

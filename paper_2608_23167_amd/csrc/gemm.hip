@@ -574,19 +574,21 @@ __device__ __forceinline__ void wait_vmcnt() {
 // one workgroup's barrier wait overlaps the other's MFMAs.  The output tile
 // goes through LDS in chunks of EB rows into the same epilogues as
 // gemm_bf16_kernel.
-template <int BM, int BN, int WM, int WN, bool SPLIT, class Pol>
-__global__ void __launch_bounds__(512, 4) gemm_big_kernel(Pol pol, const bf16_t* __restrict__ Ahi,
+template <int BM, int BN, int WM, int WN, int NS, bool SPLIT, class Pol>
+__global__ void __launch_bounds__(WM * WN * 64, 4) gemm_big_kernel(Pol pol, const bf16_t* __restrict__ Ahi,
                                                           const bf16_t* __restrict__ Alo, int G,
                                                           int M, int k_per_split, int mt,
                                                           int n_split, float* __restrict__ part,
                                                           int ldp) {
-  static_assert(WM * WN == 8, "8 waves");
-  constexpr int BK = 32, NS = 2;
+  constexpr int NW = WM * WN;
+  static_assert(NW == 8 || NW == 16, "8 or 16 waves");
+  static_assert(NS == 2 || NS == 3, "ring of 2 or 3 stages");
+  constexpr int BK = 32;
   constexpr int NA = SPLIT ? 2 : 1;
   constexpr int GB = BM / 16;                                   // row groups per tile
   constexpr int A_BLOCKS = GB * NA, BLOCKS = A_BLOCKS + BN / 16;
-  static_assert(BLOCKS % 8 == 0, "whole blocks per wave");
-  constexpr int CPW = BLOCKS / 8, STAGE = BLOCKS * 1024;
+  static_assert(BLOCKS % NW == 0, "whole blocks per wave");
+  constexpr int CPW = BLOCKS / NW, STAGE = BLOCKS * 1024;
   constexpr int RW = BM / WM, CW = BN / WN, FM = RW / 16, FN = CW / 16;
   constexpr int CS = BN + 4;
   constexpr int EB = BN > 128 ? BM / 2 : 128;                   // epilogue chunk rows
@@ -639,12 +641,15 @@ __global__ void __launch_bounds__(512, 4) gemm_big_kernel(Pol pol, const bf16_t*
   for (int i = 0; i < FM; ++i)
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  issue(0, 0);
-  wait_vmcnt<0>();
+  // the ring runs NS - 1 K-steps ahead; K-steps past the last one reload the
+  // last (never read), which keeps the count of copies in flight uniform
+#pragma unroll
+  for (int s = 0; s < NS - 1; ++s) issue(s, min(s, last));
+  wait_vmcnt<CPW * (NS - 2)>();
   __syncthreads();
   for (int kt = 0; kt < nk; ++kt) {
-    // the other slot was last read in step kt - 1, before the last barrier
-    issue(kt + 1, min(kt + 1, last));
+    // slot (kt + NS - 1) % NS was last read in step kt - 1, before the last barrier
+    issue(kt + NS - 1, min(kt + NS - 1, last));
     const char* stg = smem + (kt % NS) * STAGE;
     bf16x8_t af[NA][FM], wf[FN];
 #pragma unroll
@@ -662,9 +667,14 @@ __global__ void __launch_bounds__(512, 4) gemm_big_kernel(Pol pol, const bf16_t*
 #pragma unroll
         for (int j = 0; j < FN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[p][i], wf[j], acc[i][j], 0, 0, 0);
-    wait_vmcnt<0>();                               // this wave's blocks of step kt + 1
-    __syncthreads();                               // all blocks visible; slot kt free
+    // this wave's blocks of step kt + 1 (copies retire in issue order; the
+    // NS - 2 younger stages stay in flight), then all blocks visible and slot
+    // kt free.  A plain barrier: a fenced one would wait for every copy.
+    wait_vmcnt<CPW * (NS - 2)>();
+    asm volatile("s_barrier" ::: "memory");
   }
+  wait_vmcnt<0>();                                 // the ring is reused by the epilogue
+  __syncthreads();
   // acc[i][j][r] = C[RW wm + 16 i + 4 (lane / 16) + r][CW wn + 16 j + lane % 16]
   float* Cs = (float*)smem;
 #pragma unroll
@@ -803,8 +813,8 @@ size_t gemm_split_ws_floats(int M, int max_n) {
 // register ring of weight loads.
 struct GemmCfg {
   int bn, s, pw;
-  int big = 0;    // gemm_big_kernel tile: 1 = 256 x 128, 2 = 128 x 256; 0 = gemm_bf16_kernel;
-                  // -1 = automatic
+  int big = 0;    // gemm_big_kernel tile: 1 = 256 x 128, 2 = 128 x 256 (8 waves, 2-stage ring),
+                  // 3 = 256 x 256 (16 waves, 3-stage ring); 0 = gemm_bf16_kernel; -1 = automatic
 };
 
 // Tuning override: SSM_GEMM_CFG="kind:bn:s:pw[:big],..." with kind one of
@@ -870,7 +880,7 @@ static GemmCfg plan_bf16(const char* kind, Pol& pol, int M, int K, int N, GemmCf
   c = cfg_override(kind, c);
   // many rows: the big-tile kernel where its shape constraints hold
   if (c.big < 0) c.big = 0;
-  const int big_bn = c.big == 2 ? 256 : 128;
+  const int big_bn = c.big >= 2 ? 256 : 128;
   // (the per-head QKV epilogue, the one with a rebind, takes only 128 columns)
   if (c.big && (M < BIG_ROWS_MIN || has_tile<Pol>::value || !bn_ok(pol, 128) ||
                 (big_bn != 128 && rebind) || N % big_bn != 0 || K % 32 != 0))
@@ -878,27 +888,27 @@ static GemmCfg plan_bf16(const char* kind, Pol& pol, int M, int K, int N, GemmCf
   if (c.big) c.bn = big_bn;
   else if (!bn_ok(pol, c.bn) || N % c.bn) c.bn = bn_ok(pol, 128) && N % 128 == 0 ? 128 : 64;
   if (rebind) rebind(pol, c.bn);
-  const int tiles = (N / c.bn) * ceil_div(M, c.big == 1 ? 256 : 128);
+  const int tiles = (N / c.bn) * ceil_div(M, c.big == 1 || c.big == 3 ? 256 : 128);
   int S = c.s > 0 ? c.s : auto_split(tiles, M, K, ws.floats, N);
   while (S > 1 && (K % (256 * S) != 0 || (size_t)S * M * N > ws.floats)) S /= 2;
   c.s = S;
   return c;
 }
 
-template <int BM, int BN, int WM, int WN, class Pol>
+template <int BM, int BN, int WM, int WN, int NS, class Pol>
 static hipError_t launch_big(const Pol& pol, const ActIn& a, int M, int K, int N, int S,
                              SplitWs ws, hipStream_t st, bool reduce) {
   if constexpr (has_tile<Pol>::value) {
     return hipErrorInvalidValue;   // whole-tile epilogues run on gemm_bf16_kernel only
   } else {
     const int ntiles = N / BN, mt = ceil_div(M, BM);
-    const dim3 grid(ntiles * mt * S);
+    const dim3 grid(ntiles * mt * S), block(64 * WM * WN);
     float* pp = S > 1 ? ws.part : nullptr;
     if (a.lo)
-      launch((gemm_big_kernel<BM, BN, WM, WN, true, Pol>), grid, dim3(512), 0, st, pol,
+      launch((gemm_big_kernel<BM, BN, WM, WN, NS, true, Pol>), grid, block, 0, st, pol,
              (const bf16_t*)a.hi, a.lo, a.G, M, K / S, mt, S, pp, N);
     else
-      launch((gemm_big_kernel<BM, BN, WM, WN, false, Pol>), grid, dim3(512), 0, st, pol,
+      launch((gemm_big_kernel<BM, BN, WM, WN, NS, false, Pol>), grid, block, 0, st, pol,
              (const bf16_t*)a.hi, a.lo, a.G, M, K / S, mt, S, pp, N);
     if (S > 1 && reduce) launch_reduce<BN>(pol, ws.part, N, M, S, ntiles, st);
     return hipGetLastError();
@@ -908,8 +918,9 @@ static hipError_t launch_big(const Pol& pol, const ActIn& a, int M, int K, int N
 template <class Pol>
 static hipError_t launch_plan(const Pol& pol, const ActIn& a, int M, int K, int N, GemmCfg c,
                               SplitWs ws, hipStream_t st, bool reduce = true) {
-  if (c.big == 1) return launch_big<256, 128, 4, 2>(pol, a, M, K, N, c.s, ws, st, reduce);
-  if (c.big == 2) return launch_big<128, 256, 2, 4>(pol, a, M, K, N, c.s, ws, st, reduce);
+  if (c.big == 1) return launch_big<256, 128, 4, 2, 2>(pol, a, M, K, N, c.s, ws, st, reduce);
+  if (c.big == 2) return launch_big<128, 256, 2, 4, 2>(pol, a, M, K, N, c.s, ws, st, reduce);
+  if (c.big == 3) return launch_big<256, 256, 4, 4, 3>(pol, a, M, K, N, c.s, ws, st, reduce);
   if (c.bn == 96) return launch_bf16_pw<96>(pol, a, M, K, N, c.s, c.pw, ws, st, reduce);
   if (c.bn == 64) return launch_bf16_pw<64>(pol, a, M, K, N, c.s, c.pw, ws, st, reduce);
   return launch_bf16_pw<128>(pol, a, M, K, N, c.s, c.pw, ws, st, reduce);
@@ -1006,14 +1017,16 @@ static hipError_t run_f32(const Pol& pol, const ActIn& a, int M, int K, int N, S
 // MFMA-bound and want wide tiles.
 // Measured choices: below 512 rows gemm_bf16_kernel; from 512 rows the big
 // tiles for QKV (256 x 128: a tile stays one head for RoPE) and gate/up
-// (128 x 256), while O and down (N = d) keep gemm_bf16_kernel, whose 128-row
-// tiles fill more CUs there.  Up to 128 rows, O takes 64-column tiles and
+// (128 x 256; from 1024 rows 256 x 256 with a 3-stage ring, which halves the
+// operand bytes per MFMA and hides two K-steps of copy latency), while O and
+// down (N = d) keep gemm_bf16_kernel, whose 128-row tiles fill more CUs there.  Up to 128 rows, O takes 64-column tiles and
 // split-K 4, which halves the float32 partials of the 8-way split.
 static GemmCfg default_cfg(const char* kind, int M) {
   const bool small = M <= 256;
   if (!strcmp(kind, "qkv"))   // split-K pays at 120 rows, not at 240
     return small ? GemmCfg{128, M <= 128 ? 2 : 1, 4, 0} : GemmCfg{128, 1, 3, 1};
-  if (!strcmp(kind, "gate_up")) return small ? GemmCfg{128, 1, 4, 0} : GemmCfg{128, 1, 3, 2};
+  if (!strcmp(kind, "gate_up"))   // 256 x 256 tiles once there are 4 or more row tiles
+    return small ? GemmCfg{128, 1, 4, 0} : GemmCfg{128, 1, 3, M >= 1024 ? 3 : 2};
   if (!strcmp(kind, "lm")) return GemmCfg{128, 1, 4, 0};
   if (!strcmp(kind, "o") && M <= 128) return GemmCfg{64, 4, 4, 0};
   return small ? GemmCfg{128, 0, 4, 0} : GemmCfg{128, 0, 3, 0};   // o, down

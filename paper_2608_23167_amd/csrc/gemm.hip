@@ -814,7 +814,8 @@ size_t gemm_split_ws_floats(int M, int max_n) {
 struct GemmCfg {
   int bn, s, pw;
   int big = 0;    // gemm_big_kernel tile: 1 = 256 x 128, 2 = 128 x 256 (8 waves, 2-stage ring),
-                  // 3 = 256 x 256 (16 waves, 3-stage ring); 0 = gemm_bf16_kernel; -1 = automatic
+                  // 3 = 256 x 256 (16 waves, 3-stage ring), 4 = 128 x 256 (8 waves, 3-stage
+                  // ring, one workgroup per CU); 0 = gemm_bf16_kernel; -1 = automatic
 };
 
 // Tuning override: SSM_GEMM_CFG="kind:bn:s:pw[:big],..." with kind one of
@@ -921,6 +922,7 @@ static hipError_t launch_plan(const Pol& pol, const ActIn& a, int M, int K, int 
   if (c.big == 1) return launch_big<256, 128, 4, 2, 2>(pol, a, M, K, N, c.s, ws, st, reduce);
   if (c.big == 2) return launch_big<128, 256, 2, 4, 2>(pol, a, M, K, N, c.s, ws, st, reduce);
   if (c.big == 3) return launch_big<256, 256, 4, 4, 3>(pol, a, M, K, N, c.s, ws, st, reduce);
+  if (c.big == 4) return launch_big<128, 256, 2, 4, 3>(pol, a, M, K, N, c.s, ws, st, reduce);
   if (c.bn == 96) return launch_bf16_pw<96>(pol, a, M, K, N, c.s, c.pw, ws, st, reduce);
   if (c.bn == 64) return launch_bf16_pw<64>(pol, a, M, K, N, c.s, c.pw, ws, st, reduce);
   return launch_bf16_pw<128>(pol, a, M, K, N, c.s, c.pw, ws, st, reduce);
@@ -1019,7 +1021,8 @@ static hipError_t run_f32(const Pol& pol, const ActIn& a, int M, int K, int N, S
 // tiles for QKV (256 x 128: a tile stays one head for RoPE) and gate/up
 // (128 x 256; from 1024 rows 256 x 256 with a 3-stage ring, which halves the
 // operand bytes per MFMA and hides two K-steps of copy latency), while O and
-// down (N = d) keep gemm_bf16_kernel, whose 128-row tiles fill more CUs there.  Up to 128 rows, O takes 64-column tiles and
+// down (N = d) keep gemm_bf16_kernel, whose 128-row tiles fill more CUs there,
+// up to 1535 rows and take 3-stage 128 x 256 tiles from 1536.  Up to 128 rows, O takes 64-column tiles and
 // split-K 4, which halves the float32 partials of the 8-way split.
 static GemmCfg default_cfg(const char* kind, int M) {
   const bool small = M <= 256;
@@ -1029,7 +1032,8 @@ static GemmCfg default_cfg(const char* kind, int M) {
     return small ? GemmCfg{128, 1, 4, 0} : GemmCfg{128, 1, 3, M >= 1024 ? 3 : 2};
   if (!strcmp(kind, "lm")) return GemmCfg{128, 1, 4, 0};
   if (!strcmp(kind, "o") && M <= 128) return GemmCfg{64, 4, 4, 0};
-  return small ? GemmCfg{128, 0, 4, 0} : GemmCfg{128, 0, 3, 0};   // o, down
+  // o, down: from 1536 rows (12 or more row tiles) the 3-stage 128 x 256 tiles
+  return small ? GemmCfg{128, 0, 4, 0} : GemmCfg{128, 0, 3, M >= 1536 ? 4 : 0};
 }
 
 template <class Pol> static int any_bn(const Pol&, int bn) { return bn == 64 || bn == 96 || bn == 128; }

@@ -147,3 +147,12 @@ def test_llada_long_shape_2_layers_single_bf16_activations(gpu):
     wl = sharpened(WORKLOADS["llada_long2048"], 30.0)
     wl = wl.replace(model=wl.model.with_layers(2))
     _bf16_case(wl, [(0, 2)], act_mode=L.SSM_ACT_BF16)
+
+
+def test_llada_long1024_block_start_1776_rows_2_layers_bf16(gpu):
+    """Block-start step of block 8 of the gen-1024 long workload: 1776 rows, a
+    ragged last tile for both the 256-row (gate/up: 256 x 256, 3-stage ring)
+    and the 128-row (O/down: 128 x 256, 3-stage ring) big-tile GEMMs."""
+    wl = sharpened(WORKLOADS["llada_long1024"], 30.0)
+    wl = wl.replace(model=wl.model.with_layers(2))
+    _bf16_case(wl, [(8, 1)])

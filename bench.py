@@ -39,14 +39,14 @@ METRIC = "denoised tokens/sec + step latency per GPU (LLaDA-8B shape); % MFMA/HB
 TRAFFIC = {
     # rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE over `bench.py --steps 32 --warmup 1
     # --no-profile --no-cpu-baseline --no-full-suffix --no-mfma`; per-dispatch means
-    # of the block-start launches (180292.0 / 18048.0 KiB, 64 dispatches, grid
-    # 294912) and the cached ones (106563.5 / 5760.0 KiB, 992 dispatches, grid
-    # 98304), weighted 1:31 as in the generation schedule; copy kernel: 268435456
+    # of the block-start launches (178264.5 / 18048.0 KiB, 64 dispatches, grid
+    # 393216) and the cached ones (106558.5 / 5760.0 KiB, 992 dispatches, grid
+    # 131072), weighted 1:31 as in the generation schedule; copy kernel: 268435456
     # bytes read and written per launch read as 131085.2 KiB fetched and 262144.0
     # KiB written
     ("llada_gen256", "gemm_gate_up"): {
-        "sources_sha256": "4149911a74398e4fba9447bfcad10d16486a24c52d607194d70d6ced47c1e663",
-        "fetch_kib": (180292.0 + 31 * 106563.5) / 32, "write_kib": (18048.0 + 31 * 5760.0) / 32,
+        "sources_sha256": "786c4629a900fa1b34d60fde1e21c713a64a70d25673716c581949c57c8487d7",
+        "fetch_kib": (178264.5 + 31 * 106558.5) / 32, "write_kib": (18048.0 + 31 * 5760.0) / 32,
         "fetch_scale": 262144.0 / 131085.2, "write_scale": 1.0},
 }
 GEMM_SOURCES = ("gemm.hip", "internal.h", "common.h")

@@ -1028,8 +1028,11 @@ static GemmCfg default_cfg(const char* kind, int M) {
   const bool small = M <= 256;
   if (!strcmp(kind, "qkv"))   // split-K pays at 120 rows, not at 240
     return small ? GemmCfg{128, M <= 128 ? 2 : 1, 4, 0} : GemmCfg{128, 1, 3, 1};
-  if (!strcmp(kind, "gate_up"))   // 256 x 256 tiles once there are 4 or more row tiles
-    return small ? GemmCfg{128, 1, 4, 0} : GemmCfg{128, 1, 3, M >= 1024 ? 3 : 2};
+  // gate/up below 512 rows: 96-column tiles give one workgroup per CU at
+  // 2F = 24576 (the planner falls back to 128 where 96 does not divide 2F);
+  // from 512 rows the big tiles, 256 x 256 from 1024
+  if (!strcmp(kind, "gate_up"))
+    return M < 512 ? GemmCfg{96, 1, 4, 0} : GemmCfg{128, 1, 3, M >= 1024 ? 3 : 2};
   if (!strcmp(kind, "lm")) return GemmCfg{128, 1, 4, 0};
   if (!strcmp(kind, "o") && M <= 128) return GemmCfg{64, 4, 4, 0};
   // o, down: from 1536 rows (12 or more row tiles) the 3-stage 128 x 256 tiles

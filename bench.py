@@ -39,14 +39,16 @@ METRIC = "denoised tokens/sec + step latency per GPU (LLaDA-8B shape); % MFMA/HB
 TRAFFIC = {
     # rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE over `bench.py --steps 32 --warmup 1
     # --no-profile --no-cpu-baseline --no-full-suffix --no-mfma`; per-dispatch means
-    # of the block-start launches (178264.5 / 18048.0 KiB, 64 dispatches, grid
-    # 393216) and the cached ones (106558.5 / 5760.0 KiB, 992 dispatches, grid
-    # 131072), weighted 1:31 as in the generation schedule; copy kernel: 268435456
-    # bytes read and written per launch read as 131085.2 KiB fetched and 262144.0
-    # KiB written
+    # of the block-start launches (grid 393216: 135733.4 / 9024.0 KiB for the 28
+    # one-pass layers, 178231.7 / 18048.0 KiB for the 4 layers with the bf16
+    # pair) and the cached ones (grid 131072: 102456.0 / 2880.0 and 106551.0 /
+    # 5760.0 KiB), weighted 28:4 over the layers and 1:31 over the steps as in the
+    # generation schedule; copy kernel: 268435456 bytes read and written per
+    # launch read as 131085.2 KiB fetched and 262144.0 KiB written
     ("llada_gen256", "gemm_gate_up"): {
-        "sources_sha256": "786c4629a900fa1b34d60fde1e21c713a64a70d25673716c581949c57c8487d7",
-        "fetch_kib": (178264.5 + 31 * 106558.5) / 32, "write_kib": (18048.0 + 31 * 5760.0) / 32,
+        "sources_sha256": "0627b9ddb44d5c5ab9ae8cc00ccfc7727819d284733f3bc9e0a4209b439e68e8",
+        "fetch_kib": ((28 * 135733.4 + 4 * 178231.7) / 32 + 31 * (28 * 102456.0 + 4 * 106551.0) / 32) / 32,
+        "write_kib": ((28 * 9024.0 + 4 * 18048.0) / 32 + 31 * (28 * 2880.0 + 4 * 5760.0) / 32) / 32,
         "fetch_scale": 262144.0 / 131085.2, "write_scale": 1.0},
 }
 GEMM_SOURCES = ("gemm.hip", "internal.h", "common.h")
@@ -290,7 +292,8 @@ def mfma_report(dm, dev, reps=3):
     HIP events summed over each operation (split-K reductions and merges
     included); flops are algorithmic (2 per multiply-add, attention 4 M N_kv H
     d_h).  `issued` counts the MFMA instructions actually run: the projections
-    take two passes (bfloat16 hi and lo parts of the activations)."""
+    of a layer that keeps the bfloat16 pair take two passes (hi and lo parts of
+    the activations), the others one."""
     import torch
     from synthetic import WORKLOADS, initial_tokens
     from paper_2608_23167_amd import _lib as L
@@ -300,7 +303,12 @@ def mfma_report(dm, dev, reps=3):
     wl = WORKLOADS["llada_long1024"]
     sh = wl.model
     d_, H, Hkv, dh, F = sh.d_model, sh.n_heads, sh.n_kv_heads, sh.head_dim, sh.ffn_dim
-    passes = 2 if dm.c_model.act_mode == L.SSM_ACT_BF16X2 else 1
+    # MFMA passes per projection, averaged over the layers: two where a layer
+    # keeps the bfloat16 pair (hi and lo parts), one where it rounds once
+    cm = dm.c_model
+    n_pair = {L.SSM_ACT_BF16X2: sh.n_layers,
+              L.SSM_ACT_BF16X2_FIRST: min(cm.pair_layers, sh.n_layers)}.get(cm.act_mode, 0)
+    passes = 1.0 + n_pair / sh.n_layers
     dec = Decoder(wl, dm, device=dev)
     tok = initial_tokens(wl, device=dev)
     j = wl.n_blocks // 2

@@ -74,8 +74,12 @@ enum { SSM_DT_F32 = 0, SSM_DT_BF16 = 1 };
 /* Activation precision at the projections of a bfloat16 model. */
 enum {
   SSM_ACT_BF16 = 0,     /* each projection input is rounded once to bfloat16                 */
-  SSM_ACT_BF16X2 = 1    /* each projection input is kept as a bfloat16 pair hi + lo and both  */
+  SSM_ACT_BF16X2 = 1,   /* each projection input is kept as a bfloat16 pair hi + lo and both  */
                         /* parts are multiplied (weights stay bfloat16; twice the MFMA work)  */
+  SSM_ACT_BF16X2_FIRST = 2  /* the pair in layers [0, pair_layers) only; the later layers and   */
+                            /* the LM head round once.  The residual stream grows with depth,   */
+                            /* so a rounding in an early layer weighs far more in the output    */
+                            /* than one in a late layer.                                        */
 };
 
 /* Region tag of a compacted row. */
@@ -164,6 +168,8 @@ typedef struct ssm_model {
   const void* lm_head;     /* [vocab, d] device                                */
   const ssm_layer* layers; /* HOST array of n_layers device-pointer sets       */
   int32_t act_mode;        /* SSM_ACT_*; ignored for float32 models            */
+  int32_t pair_layers;     /* SSM_ACT_BF16X2_FIRST: leading layers that keep   */
+                           /* the pair, in [0, n_layers]; ignored otherwise    */
 } ssm_model;
 
 /* Prefix KV cache: k and v are [n_layers, batch, n_kv_heads, capacity, head_dim]

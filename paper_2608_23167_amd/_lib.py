@@ -15,7 +15,7 @@ SSM_OK, SSM_E_INVAL, SSM_E_SHAPE, SSM_E_CAPACITY, SSM_E_HIP, SSM_E_UNSUPPORTED =
 SSM_MIDDLE_STRIDED, SSM_MIDDLE_BLOCK_START = 0, 1
 SSM_UNMASK_TOPN, SSM_UNMASK_THRESHOLD, SSM_UNMASK_MARGIN = 0, 1, 2
 SSM_DT_F32, SSM_DT_BF16 = 0, 1
-SSM_ACT_BF16, SSM_ACT_BF16X2 = 0, 1
+SSM_ACT_BF16, SSM_ACT_BF16X2, SSM_ACT_BF16X2_FIRST = 0, 1, 2
 SSM_CACHE_OFF, SSM_CACHE_WRITE, SSM_CACHE_READ = 0, 1, 2
 
 _ERR_NAMES = {SSM_E_INVAL: "SSM_E_INVAL", SSM_E_SHAPE: "SSM_E_SHAPE",
@@ -46,7 +46,7 @@ class Model(C.Structure):
         "mask_id", "dtype")] + [
         ("rope_base", C.c_float), ("rms_eps", C.c_float),
         ("tok_emb", C.c_void_p), ("final_norm", C.c_void_p), ("lm_head", C.c_void_p),
-        ("layers", C.POINTER(Layer)), ("act_mode", C.c_int32)]
+        ("layers", C.POINTER(Layer)), ("act_mode", C.c_int32), ("pair_layers", C.c_int32)]
 
 
 class KVCache(C.Structure):

@@ -101,8 +101,12 @@ int32_t check_model(const ssm_model* m) {
     if (!y.attn_norm || !y.wq || !y.wk || !y.wv || !y.wo || !y.ffn_norm || !y.w_gate || !y.w_up || !y.w_down)
       return fail(SSM_E_INVAL, "null tensor in layer %d", l);
   }
-  if (m->dtype == SSM_DT_BF16 && m->act_mode != SSM_ACT_BF16 && m->act_mode != SSM_ACT_BF16X2)
+  if (m->dtype == SSM_DT_BF16 && m->act_mode != SSM_ACT_BF16 && m->act_mode != SSM_ACT_BF16X2 &&
+      m->act_mode != SSM_ACT_BF16X2_FIRST)
     return fail(SSM_E_INVAL, "unknown act_mode %d", m->act_mode);
+  if (m->dtype == SSM_DT_BF16 && m->act_mode == SSM_ACT_BF16X2_FIRST &&
+      (m->pair_layers < 0 || m->pair_layers > m->n_layers))
+    return fail(SSM_E_INVAL, "pair_layers %d not in [0, %d]", m->pair_layers, m->n_layers);
   if (m->dtype == SSM_DT_BF16) {
     if (m->head_dim != 128) return fail(SSM_E_UNSUPPORTED, "bf16 path needs head_dim 128 (got %d)", m->head_dim);
     if (m->d_model % 256 || m->ffn_dim % 256 || m->vocab % 128)
@@ -182,6 +186,14 @@ struct WsLayout {
   size_t part_floats;
 };
 
+// Whether the projection inputs of layer l (l == n_layers: the LM head) are
+// kept as a bfloat16 pair.
+static bool pair_in_layer(const ssm_model* m, int l) {
+  if (m->dtype != SSM_DT_BF16) return false;
+  if (m->act_mode == SSM_ACT_BF16X2) return true;
+  return m->act_mode == SSM_ACT_BF16X2_FIRST && l < m->pair_layers;
+}
+
 WsLayout ws_layout(const ssm_model* m, int batch, int max_rows) {
   const size_t es = m->dtype == SSM_DT_BF16 ? 2 : 4;
   const size_t Mt = (size_t)batch * max_rows;
@@ -196,7 +208,7 @@ WsLayout ws_layout(const ssm_model* m, int batch, int max_rows) {
   auto take = [&](size_t bytes) { size_t o = off; off += align256(bytes); return o; };
   // projection operands: float32 for float32 models, bfloat16 hi (+ lo) otherwise
   // (bfloat16 operands in fragment order: rows padded to whole 16-row groups)
-  const size_t lo_es = (m->dtype == SSM_DT_BF16 && m->act_mode == SSM_ACT_BF16X2) ? 2 : 0;
+  const size_t lo_es = pair_in_layer(m, 0) ? 2 : 0;
   const size_t Mp = (size_t)row_groups((int)Mt) * 16;
   w.resid = take(Mt * d * 4);
   w.xn = take(Mp * d * es);
@@ -313,7 +325,6 @@ int32_t ssm_denoise_step(const ssm_model* m, const ssm_kv_cache* cache, int32_t 
 
   hipStream_t st = (hipStream_t)stream;
   const int dt = m->dtype;
-  const bool split = dt == SSM_DT_BF16 && m->act_mode == SSM_ACT_BF16X2;
   const int d = m->d_model, H = m->n_heads, Hkv = m->n_kv_heads, dh = m->head_dim;
   const int F = m->ffn_dim, V = m->vocab;
   const int Mt = batch * n_rows, n_out = n_rows - first_out_row, Mo = batch * n_out;
@@ -321,15 +332,18 @@ int32_t ssm_denoise_step(const ssm_model* m, const ssm_kv_cache* cache, int32_t 
   const size_t es = dt == SSM_DT_BF16 ? 2 : 4;
   char* ws = (char*)d_ws;
   float* resid = (float*)(ws + w.resid);
-  bf16_t* xn_lo = split ? (bf16_t*)(ws + w.xn_lo) : nullptr;
-  bf16_t* attn_lo = split ? (bf16_t*)(ws + w.attn_lo) : nullptr;
-  bf16_t* act_lo = split ? (bf16_t*)(ws + w.act_lo) : nullptr;
+  // the lo parts of layer l's projection inputs, or null where it rounds once
+  struct LoParts { bf16_t *xn, *attn, *act; };
+  auto lo_of = [&](int l) {
+    const bool p = pair_in_layer(m, l);
+    return LoParts{p ? (bf16_t*)(ws + w.xn_lo) : nullptr, p ? (bf16_t*)(ws + w.attn_lo) : nullptr,
+                   p ? (bf16_t*)(ws + w.act_lo) : nullptr};
+  };
   // every step-local operand has Mt rows; the LM head input has Mo rows
   const int Gt = row_groups(Mt), Go = row_groups(Mo);
-  const ActOut xn_out{ws + w.xn, xn_lo, d, Gt}, attn_out{ws + w.attn, attn_lo, H * dh, Gt},
-      act_out{ws + w.act, act_lo, F, Gt}, head_out{ws + w.xn, xn_lo, d, Go};
-  const ActIn xn_in{ws + w.xn, xn_lo, d, Gt}, attn_in{ws + w.attn, attn_lo, H * dh, Gt},
-      act_in{ws + w.act, act_lo, F, Gt}, head_in{ws + w.xn, xn_lo, d, Go};
+  const LoParts head_lo = lo_of(m->n_layers);
+  const ActOut head_out{ws + w.xn, head_lo.xn, d, Go};
+  const ActIn head_in{ws + w.xn, head_lo.xn, d, Go};
   void* qb = ws + w.q;
   float2* rope = (float2*)(ws + w.rope);
   SplitWs sws{(float*)(ws + w.part), w.part_floats};
@@ -342,10 +356,17 @@ int32_t ssm_denoise_step(const ssm_model* m, const ssm_kv_cache* cache, int32_t 
   // the attention norm of layer 0 runs alone; every later norm follows the
   // residual projection before it (fused with its split-K completion)
   if (m->n_layers > 0)
-    PROF_TRY("norm", launch_norm(dt, resid, d, m->layers[0].attn_norm, m->rms_eps, xn_out, Mt, Mt,
-                                 0, 0, st));
+    PROF_TRY("norm", launch_norm(dt, resid, d, m->layers[0].attn_norm, m->rms_eps,
+                                 ActOut{ws + w.xn, lo_of(0).xn, d, Gt}, Mt, Mt, 0, 0, st));
   for (int l = 0; l < m->n_layers; ++l) {
     const ssm_layer& y = m->layers[l];
+    const LoParts lo = lo_of(l);
+    const ActOut xn_out{ws + w.xn, lo.xn, d, Gt}, attn_out{ws + w.attn, lo.attn, H * dh, Gt},
+        act_out{ws + w.act, lo.act, F, Gt};
+    const ActIn xn_in{ws + w.xn, lo.xn, d, Gt}, attn_in{ws + w.attn, lo.attn, H * dh, Gt},
+        act_in{ws + w.act, lo.act, F, Gt};
+    // the norm that ends this layer feeds the next layer (or the LM head)
+    const ActOut next_out{ws + w.xn, lo_of(l + 1).xn, d, Gt};
     char* kc = (char*)cache->k + l * layer_kv;
     char* vc = (char*)cache->v + l * layer_kv;
     // attention block (its input norm is in xn)
@@ -358,7 +379,7 @@ int32_t ssm_denoise_step(const ssm_model* m, const ssm_kv_cache* cache, int32_t 
     // feed-forward block
     PROF_TRY("gemm_gate_up", gemm_swiglu(dt, xn_in, Mt, d, y.w_gate, y.w_up, F, act_out, sws, st));
     const bool more = l + 1 < m->n_layers;
-    const NormTo next_norm{more ? m->layers[l + 1].attn_norm : nullptr, m->rms_eps, xn_out};
+    const NormTo next_norm{more ? m->layers[l + 1].attn_norm : nullptr, m->rms_eps, next_out};
     PROF_TRY("gemm_down", gemm_resid(dt, "down", act_in, Mt, F, y.w_down, d, resid, sws, st,
                                      more ? &next_norm : nullptr));
   }

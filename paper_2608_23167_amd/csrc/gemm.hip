@@ -575,7 +575,7 @@ __device__ __forceinline__ void wait_vmcnt() {
 // goes through LDS in chunks of EB rows into the same epilogues as
 // gemm_bf16_kernel.
 template <int BM, int BN, int WM, int WN, int NS, bool SPLIT, class Pol>
-__global__ void __launch_bounds__(WM * WN * 64, 4) gemm_big_kernel(Pol pol, const bf16_t* __restrict__ Ahi,
+__global__ void __launch_bounds__(WM * WN * 64, (BM / WM) * (BN / WN) > 4096 ? 2 : 4) gemm_big_kernel(Pol pol, const bf16_t* __restrict__ Ahi,
                                                           const bf16_t* __restrict__ Alo, int G,
                                                           int M, int k_per_split, int mt,
                                                           int n_split, float* __restrict__ part,
@@ -815,8 +815,11 @@ struct GemmCfg {
   int bn, s, pw;
   int big = 0;    // gemm_big_kernel tile: 1 = 256 x 128, 2 = 128 x 256 (8 waves, 2-stage ring),
                   // 3 = 256 x 256 (16 waves, 3-stage ring), 4 = 128 x 256 (8 waves, 3-stage
-                  // ring, one workgroup per CU); 0 = gemm_bf16_kernel; -1 = automatic
+                  // ring), 5 = 256 x 256 (8 waves of 64 x 128, 3-stage ring), 6 = 256 x 128
+                  // (8 waves, 3-stage ring); 0 = gemm_bf16_kernel; -1 = automatic
 };
+static int big_rows(int big) { return big == 1 || big == 3 || big == 5 || big == 6 ? 256 : 128; }
+static int big_cols(int big) { return big == 1 || big == 6 ? 128 : 256; }
 
 // Tuning override: SSM_GEMM_CFG="kind:bn:s:pw[:big],..." with kind one of
 // qkv, o, gate_up, down, lm (big as in GemmCfg); read once per process.
@@ -881,7 +884,7 @@ static GemmCfg plan_bf16(const char* kind, Pol& pol, int M, int K, int N, GemmCf
   c = cfg_override(kind, c);
   // many rows: the big-tile kernel where its shape constraints hold
   if (c.big < 0) c.big = 0;
-  const int big_bn = c.big >= 2 ? 256 : 128;
+  const int big_bn = c.big ? big_cols(c.big) : 128;
   // (the per-head QKV epilogue, the one with a rebind, takes only 128 columns)
   if (c.big && (M < BIG_ROWS_MIN || has_tile<Pol>::value || !bn_ok(pol, 128) ||
                 (big_bn != 128 && rebind) || N % big_bn != 0 || K % 32 != 0))
@@ -889,7 +892,7 @@ static GemmCfg plan_bf16(const char* kind, Pol& pol, int M, int K, int N, GemmCf
   if (c.big) c.bn = big_bn;
   else if (!bn_ok(pol, c.bn) || N % c.bn) c.bn = bn_ok(pol, 128) && N % 128 == 0 ? 128 : 64;
   if (rebind) rebind(pol, c.bn);
-  const int tiles = (N / c.bn) * ceil_div(M, c.big == 1 || c.big == 3 ? 256 : 128);
+  const int tiles = (N / c.bn) * ceil_div(M, c.big ? big_rows(c.big) : 128);
   int S = c.s > 0 ? c.s : auto_split(tiles, M, K, ws.floats, N);
   while (S > 1 && (K % (256 * S) != 0 || (size_t)S * M * N > ws.floats)) S /= 2;
   c.s = S;
@@ -923,6 +926,8 @@ static hipError_t launch_plan(const Pol& pol, const ActIn& a, int M, int K, int 
   if (c.big == 2) return launch_big<128, 256, 2, 4, 2>(pol, a, M, K, N, c.s, ws, st, reduce);
   if (c.big == 3) return launch_big<256, 256, 4, 4, 3>(pol, a, M, K, N, c.s, ws, st, reduce);
   if (c.big == 4) return launch_big<128, 256, 2, 4, 3>(pol, a, M, K, N, c.s, ws, st, reduce);
+  if (c.big == 5) return launch_big<256, 256, 4, 2, 3>(pol, a, M, K, N, c.s, ws, st, reduce);
+  if (c.big == 6) return launch_big<256, 128, 4, 2, 3>(pol, a, M, K, N, c.s, ws, st, reduce);
   if (c.bn == 96) return launch_bf16_pw<96>(pol, a, M, K, N, c.s, c.pw, ws, st, reduce);
   if (c.bn == 64) return launch_bf16_pw<64>(pol, a, M, K, N, c.s, c.pw, ws, st, reduce);
   return launch_bf16_pw<128>(pol, a, M, K, N, c.s, c.pw, ws, st, reduce);
@@ -1016,27 +1021,30 @@ static hipError_t run_f32(const Pol& pol, const ActIn& a, int M, int K, int N, S
 
 // Default launch choices: the cached-step row counts (M <= 256) are
 // HBM-bound and want every CU streaming weights; block-start row counts are
-// MFMA-bound and want wide tiles.
-// Measured choices: below 512 rows gemm_bf16_kernel; from 512 rows the big
-// tiles for QKV (256 x 128: a tile stays one head for RoPE) and gate/up
-// (128 x 256; from 1024 rows 256 x 256 with a 3-stage ring, which halves the
-// operand bytes per MFMA and hides two K-steps of copy latency), while O and
-// down (N = d) keep gemm_bf16_kernel, whose 128-row tiles fill more CUs there,
-// up to 1535 rows and take 3-stage 128 x 256 tiles from 1536.  Up to 128 rows, O takes 64-column tiles and
-// split-K 4, which halves the float32 partials of the 8-way split.
-static GemmCfg default_cfg(const char* kind, int M) {
+// MFMA-bound and want wide tiles.  `paired`: the activations carry the lo part
+// (twice the MFMA work per operand byte, so the wide 3-stage tiles pay more).
+// Measured choices:
+//  * QKV: split-K 2 up to 128 rows; from 512 rows 256 x 128 tiles (a tile
+//    stays one head, for RoPE), with a 3-stage ring for one pass (24 KB per
+//    stage: two workgroups per CU) and a 2-stage ring for the pair;
+//  * gate/up: 96-column tiles below 512 rows (one workgroup per CU at
+//    2F = 24576; the planner falls back to 128 where 96 does not divide 2F);
+//    from 512 rows 128 x 256, from 1024 rows 256 x 256 with 16 waves and a
+//    3-stage ring (half the operand bytes per MFMA, two K-steps of copy
+//    latency hidden);
+//  * O / down (N = d): gemm_bf16_kernel, whose 128-row tiles fill more CUs;
+//    with the pair, from 1536 rows the 3-stage 128 x 256 tiles.  Up to 128
+//    rows O takes 64-column tiles and split-K 4, which halves the float32
+//    partials of the 8-way split.
+static GemmCfg default_cfg(const char* kind, int M, bool paired) {
   const bool small = M <= 256;
   if (!strcmp(kind, "qkv"))   // split-K pays at 120 rows, not at 240
-    return small ? GemmCfg{128, M <= 128 ? 2 : 1, 4, 0} : GemmCfg{128, 1, 3, 1};
-  // gate/up below 512 rows: 96-column tiles give one workgroup per CU at
-  // 2F = 24576 (the planner falls back to 128 where 96 does not divide 2F);
-  // from 512 rows the big tiles, 256 x 256 from 1024
+    return small ? GemmCfg{128, M <= 128 ? 2 : 1, 4, 0} : GemmCfg{128, 1, 3, paired ? 1 : 6};
   if (!strcmp(kind, "gate_up"))
     return M < 512 ? GemmCfg{96, 1, 4, 0} : GemmCfg{128, 1, 3, M >= 1024 ? 3 : 2};
   if (!strcmp(kind, "lm")) return GemmCfg{128, 1, 4, 0};
   if (!strcmp(kind, "o") && M <= 128) return GemmCfg{64, 4, 4, 0};
-  // o, down: from 1536 rows (12 or more row tiles) the 3-stage 128 x 256 tiles
-  return small ? GemmCfg{128, 0, 4, 0} : GemmCfg{128, 0, 3, M >= 1536 ? 4 : 0};
+  return small ? GemmCfg{128, 0, 4, 0} : GemmCfg{128, 0, 3, paired && M >= 1536 ? 4 : 0};
 }
 
 template <class Pol> static int any_bn(const Pol&, int bn) { return bn == 64 || bn == 96 || bn == 128; }
@@ -1055,7 +1063,7 @@ hipError_t gemm_qkv(int dtype, const ActIn& a, int M, int d, const void* wq, con
   PolQKV<bf16_t> p{(const bf16_t*)wq, (const bf16_t*)wk, (const bf16_t*)wv, d, H, Hkv, dh,
                    dh / 128, (bf16_t*)o.q, (bf16_t*)o.kc, (bf16_t*)o.vc, o.cap, o.n_cached,
                    o.n_rows, o.rope};
-  return run_bf16("qkv", p, a, M, d, N, default_cfg("qkv", M), ws, st, qkv_bn, rebind_qkv);
+  return run_bf16("qkv", p, a, M, d, N, default_cfg("qkv", M, a.lo != nullptr), ws, st, qkv_bn, rebind_qkv);
 }
 
 hipError_t gemm_resid(int dtype, const char* kind, const ActIn& a, int M, int K, const void* w,
@@ -1066,7 +1074,7 @@ hipError_t gemm_resid(int dtype, const char* kind, const ActIn& a, int M, int K,
     e = run_f32(p, a, M, K, N, ws, st);
   } else {
     PolResid<bf16_t> p{(const bf16_t*)w, K, N, resid};
-    const GemmCfg c = plan_bf16(kind, p, M, K, N, default_cfg(kind, M), ws,
+    const GemmCfg c = plan_bf16(kind, p, M, K, N, default_cfg(kind, M, a.lo != nullptr), ws,
                                 any_bn<PolResid<bf16_t>>, (void (*)(PolResid<bf16_t>&, int))nullptr);
     const int nc = ceil_div(N / 8, 512);
     const bool fuse = nrm && c.s > 1 && N % 8 == 0 && nc <= 2 && ((uintptr_t)nrm->g & 15) == 0;
@@ -1090,7 +1098,7 @@ hipError_t gemm_swiglu(int dtype, const ActIn& a, int M, int d, const void* wg, 
     return run_f32(p, a, M, d, 2 * F, ws, st);
   }
   PolSwiGLU<bf16_t> p{(const bf16_t*)wg, (const bf16_t*)wu, d, F, act};
-  return run_bf16("gate_up", p, a, M, d, 2 * F, default_cfg("gate_up", M), ws, st,
+  return run_bf16("gate_up", p, a, M, d, 2 * F, default_cfg("gate_up", M, a.lo != nullptr), ws, st,
                   any_bn<PolSwiGLU<bf16_t>>, (void (*)(PolSwiGLU<bf16_t>&, int))nullptr);
 }
 
@@ -1199,7 +1207,7 @@ hipError_t lm_head_stats(const ActIn& a, int M, int K, const void* w, int N, int
   constexpr int BN = 128;
   const int ntiles = N / BN;
   PolLMStats<bf16_t> p{(const bf16_t*)w, K, N, mask_id, (LMPartial*)stats_ws, 2 * ntiles, logits, N};
-  const GemmCfg c = cfg_override("lm", default_cfg("lm", M));
+  const GemmCfg c = cfg_override("lm", default_cfg("lm", M, a.lo != nullptr));
   SplitWs none{nullptr, 0};
   hipError_t e = launch_bf16_pw<BN>(p, a, M, K, N, 1, c.pw, none, st);
   if (e != hipSuccess) return e;

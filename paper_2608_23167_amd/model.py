@@ -16,7 +16,14 @@ class DeviceModel:
     contiguous device tensor of the model dtype; `shape` gives the sizes.
     """
 
-    def __init__(self, shape, weights, act_mode: int = L.SSM_ACT_BF16X2):
+    # Leading layers whose projection inputs keep the bfloat16 pair by default.
+    # Rounding them once in layer 0 alone gives most of the error of rounding
+    # them in every layer (the residual stream is smallest there); from about
+    # layer 4 on a rounding barely shows in the output.
+    PAIR_LAYERS = 4
+
+    def __init__(self, shape, weights, act_mode: int = L.SSM_ACT_BF16X2_FIRST,
+                 pair_layers: int = PAIR_LAYERS):
         self.shape = shape
         self.weights = weights
         dt = torch.float32 if shape.dtype == "f32" else torch.bfloat16
@@ -35,7 +42,7 @@ class DeviceModel:
             shape.vocab, shape.mask_id, L.SSM_DT_F32 if shape.dtype == "f32" else L.SSM_DT_BF16,
             float(shape.rope_base), float(shape.rms_eps), weights.tok_emb.data_ptr(),
             weights.final_norm.data_ptr(), weights.lm_head.data_ptr(),
-            C.cast(self._layers, C.POINTER(L.Layer)), int(act_mode))
+            C.cast(self._layers, C.POINTER(L.Layer)), int(act_mode), min(int(pair_layers), n))
 
     @property
     def dtype(self):

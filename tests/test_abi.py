@@ -101,10 +101,11 @@ def _model(**kw):
     lay = (L.Layer * 2)(*[L.Layer(*([fake] * 9)) for _ in range(2)])
     d = dict(n_layers=2, d_model=4096, n_heads=32, n_kv_heads=32, head_dim=128, ffn_dim=12288,
              vocab=126464, mask_id=126463, dtype=L.SSM_DT_BF16)
+    act = (kw.pop("act_mode", L.SSM_ACT_BF16X2), kw.pop("pair_layers", 0))
     d.update(kw)
     m = L.Model(d["n_layers"], d["d_model"], d["n_heads"], d["n_kv_heads"], d["head_dim"],
                 d["ffn_dim"], d["vocab"], d["mask_id"], d["dtype"], 10000.0, 1e-5, fake, fake,
-                fake, C.cast(lay, C.POINTER(L.Layer)))
+                fake, C.cast(lay, C.POINTER(L.Layer)), act[0], act[1])
     m._keep = lay
     return m
 
@@ -112,6 +113,8 @@ def _model(**kw):
 @pytest.mark.parametrize("bad,code", [
     (dict(d_model=4000), -2), (dict(n_kv_heads=5), -2), (dict(mask_id=126464), -1),
     (dict(dtype=3), -1), (dict(head_dim=64, n_heads=64), -5), (dict(vocab=126465, mask_id=0), -5),
+    (dict(act_mode=3), -1), (dict(act_mode=2, pair_layers=3), -1),
+    (dict(act_mode=2, pair_layers=-1), -1),
 ])
 def test_model_validation(bad, code):
     from paper_2608_23167_amd import _lib as L
@@ -119,6 +122,23 @@ def test_model_validation(bad, code):
     m = _model(**bad)
     n = C.c_size_t()
     assert lib.ssm_workspace_size(C.byref(m), 1, 100, C.byref(n)) == code
+
+
+def test_workspace_size_follows_the_pair_layers():
+    """The lo parts of the projection inputs take workspace only when some
+    layer keeps the bfloat16 pair."""
+    from paper_2608_23167_amd import _lib as L
+    lib = L.lib()
+    sizes = {}
+    for key, kw in {"pair": dict(act_mode=L.SSM_ACT_BF16X2),
+                    "single": dict(act_mode=L.SSM_ACT_BF16),
+                    "first0": dict(act_mode=L.SSM_ACT_BF16X2_FIRST, pair_layers=0),
+                    "first1": dict(act_mode=L.SSM_ACT_BF16X2_FIRST, pair_layers=1),
+                    "first2": dict(act_mode=L.SSM_ACT_BF16X2_FIRST, pair_layers=2)}.items():
+        n = C.c_size_t()
+        assert lib.ssm_workspace_size(C.byref(_model(**kw)), 1, 376, C.byref(n)) == 0
+        sizes[key] = n.value
+    assert sizes["single"] == sizes["first0"] < sizes["first1"] == sizes["first2"] == sizes["pair"]
 
 
 def test_workspace_size_and_step_validation():

@@ -89,6 +89,18 @@ def test_llada_long_block_start(gpu, llada):
     _run(WORKLOADS["llada_long2048"], llada, 0, True, 4, False)
 
 
+def test_llada_gen256_cached_pair_in_every_layer(gpu, llada):
+    """SSM_ACT_BF16X2: the bfloat16 pair at the projections of all 32 layers
+    and the LM head (the default keeps it in the first layers only)."""
+    from paper_2608_23167_amd import _lib as L
+    from paper_2608_23167_amd.model import DeviceModel
+    wl = WORKLOADS["llada_gen256"]
+    paired = type(llada).__new__(type(llada))
+    paired.mw, paired.w = llada.mw, llada.w
+    paired.dm = DeviceModel(wl.model, llada.mw, act_mode=L.SSM_ACT_BF16X2)
+    _run(wl, paired, 3, False, 2, True)
+
+
 def test_dream_uncached(gpu):
     wl = WORKLOADS["dream_gen512"]
     m = _Model(wl)

@@ -17,12 +17,12 @@ from tests._parity import (check_decisions, check_unmask, gpu_step, load_oracle_
 
 pytestmark = pytest.mark.gpu
 
-def _decoder(wl, mw_dev, act_mode=None):
+def _decoder(wl, mw_dev, act_mode=None, pair_layers=0):
     from paper_2608_23167_amd import _lib as L
     from paper_2608_23167_amd.decoder import Decoder
     from paper_2608_23167_amd.model import DeviceModel
     mode = L.SSM_ACT_BF16X2 if act_mode is None else act_mode
-    return Decoder(wl, DeviceModel(wl.model, mw_dev, act_mode=mode))
+    return Decoder(wl, DeviceModel(wl.model, mw_dev, act_mode=mode, pair_layers=pair_layers))
 
 
 def _compare_step(out, rec, wl, fp32: bool):
@@ -99,12 +99,12 @@ def _state_from(wl, block_idx, step, seed):
     return st
 
 
-def _bf16_case(wl, blocks, seed=0, act_mode=None):
+def _bf16_case(wl, blocks, seed=0, act_mode=None, pair_layers=0):
     torch.manual_seed(0)
     mw_dev = make_weights(wl.model, seed=seed, device="cuda", norm_jitter=0.1,
                           logit_scale=wl.logit_scale)
     w = OG.NumpyWeights(mw_dev, dtype=np.float32)
-    dec = _decoder(wl, mw_dev, act_mode)
+    dec = _decoder(wl, mw_dev, act_mode, pair_layers)
     fracs = []
     for j, n_steps in blocks:
         st = _state_from(wl, j, 5 + 3 * j, seed)
@@ -147,6 +147,16 @@ def test_llada_long_shape_2_layers_single_bf16_activations(gpu):
     wl = sharpened(WORKLOADS["llada_long2048"], 30.0)
     wl = wl.replace(model=wl.model.with_layers(2))
     _bf16_case(wl, [(0, 2)], act_mode=L.SSM_ACT_BF16)
+
+
+def test_llada_long_shape_pair_in_first_layer_only(gpu):
+    """SSM_ACT_BF16X2_FIRST with one pair layer: layer 0 multiplies the hi and
+    lo parts, layer 1 and the LM head round once, on both the block-start
+    (1264 rows, big tiles) and the cached (240 rows) launch paths."""
+    from paper_2608_23167_amd import _lib as L
+    wl = sharpened(WORKLOADS["llada_long2048"], 30.0)
+    wl = wl.replace(model=wl.model.with_layers(2))
+    _bf16_case(wl, [(0, 2)], act_mode=L.SSM_ACT_BF16X2_FIRST, pair_layers=1)
 
 
 def test_llada_long1024_block_start_1776_rows_2_layers_bf16(gpu):

@@ -55,10 +55,20 @@ enum {
   SSM_E_UNSUPPORTED = -5   /* valid, but a shape this build has no kernel for  */
 };
 
-/* Middle-region retention (Section 3.2, Eq. 3). */
+/* Middle-region retention (Section 3.2, Eq. 3; the middle-region variants of
+ * the ablation in Table 2).  The block modes ignore middle_budget. */
 enum {
-  SSM_MIDDLE_STRIDED = 0,      /* middle_budget tokens at offsets floor(i*len/M')     */
-  SSM_MIDDLE_BLOCK_START = 1   /* the start token of every middle block (Eq. 3)     */
+  SSM_MIDDLE_STRIDED = 0,         /* middle_budget tokens at offsets floor(i*len/M')     */
+  SSM_MIDDLE_BLOCK_START = 1,     /* the start token of every middle block (Eq. 3)     */
+  SSM_MIDDLE_BLOCK_END = 2,       /* the end token of every middle block                */
+  SSM_MIDDLE_BLOCK_START_END = 3  /* both (one token if block_size == 1)                */
+};
+
+/* Tail-region retention (Section 3.2, Eq. 4; the tail variants of Table 2). */
+enum {
+  SSM_TAIL_SPREAD = 0,   /* T' = min(tail_budget, len) tokens at offsets floor(i*(len-1)/(T'-1)), */
+                         /* both ends first (Eq. 4 is T = 2); T' = 1 keeps the end token         */
+  SSM_TAIL_START = 1     /* the start token only (if tail_budget >= 1)                          */
 };
 
 /* Unmasking rules (Section 4.2 "Vanilla" / "Par."; Section 4.5 margin rule). */
@@ -110,6 +120,7 @@ typedef struct ssm_select_params {
   int32_t middle_mode;     /* SSM_MIDDLE_*                                                 */
   int32_t tail_budget;     /* tokens kept in the last block, both ends first (Eq. 4) >= 0  */
   int32_t include_prefix;  /* 1: rows start with the prefix [0, P0 + j*b); 0: cached step  */
+  int32_t tail_mode;       /* SSM_TAIL_*                                                   */
 } ssm_select_params;
 
 /*
@@ -120,6 +131,15 @@ typedef struct ssm_select_params {
  */
 int32_t ssm_select_count(const ssm_select_params* p, int32_t* n_rows, int32_t* n_suffix,
                          int32_t* first_out_row);
+
+/*
+ * The position and region lists of ssm_select_suffix computed on the host, by
+ * the same closed form the kernel evaluates per row; no GPU work.
+ *   pos [cap] int32 and region [cap] int8 (may be NULL) are HOST arrays.
+ * SSM_E_CAPACITY if cap < n_rows; n_rows may be NULL.
+ */
+int32_t ssm_select_positions_host(const ssm_select_params* p, int32_t* pos, int8_t* region,
+                                  int32_t cap, int32_t* n_rows);
 
 /*
  * Builds the compacted row list of the sparse input [P; B_t; R_t]: for row r,

@@ -113,7 +113,8 @@ def step(wl, w: NumpyWeights, st: OracleState, block_idx: int, first_in_block: b
     b = wl.block_size
     include_prefix = (not wl.cache) or first_in_block
     rows = S.compacted_rows(wl.prompt_len, wl.gen_len, b, block_idx, wl.local_budget,
-                            wl.middle_budget, wl.middle_mode, wl.tail_budget, include_prefix)
+                            wl.middle_budget, wl.middle_mode, wl.tail_budget, include_prefix,
+                            wl.tail_mode)
     B = st.tokens.shape[0]
     P = wl.prompt_len + block_idx * b
     rec = StepRecord(block_idx, st.step, include_prefix, rows)

@@ -18,8 +18,15 @@ gives only the block rule):
   * middle region = whatever lies between them                        (Eq. 1)
   * middle, strided mode: M' = min(M, len) tokens at offsets floor(i*len/M')
   * middle, block-start mode: the start token of every middle block    (Eq. 3)
-  * tail: T' = min(T, len) tokens at offsets floor(i*(len-1)/(T'-1)), so both
-    ends are always kept (Eq. 4 is T = 2); T' = 1 keeps the end token only
+  * middle, block-end and block-start+end modes: the end token, or both end
+    tokens, of every middle block (the middle-region variants of the ablation
+    in Table 2)
+  * tail, spread mode: T' = min(T, len) tokens at offsets
+    floor(i*(len-1)/(T'-1)), so both ends are always kept (Eq. 4 is T = 2);
+    T' = 1 keeps the end token only, T' = 3 adds the token at floor((len-1)/2)
+    (the "end only" and "start+mid+end" variants of Table 2)
+  * tail, start mode: the start token only, if T >= 1 (the "start only"
+    variant of Table 2)
   * fewer suffix tokens than the local budget: everything is local (the
     paper's "fewer than w blocks" case); local wins any overlap with the tail.
 """
@@ -37,6 +44,11 @@ REGION_TAIL = 4
 
 MIDDLE_STRIDED = 0
 MIDDLE_BLOCK_START = 1
+MIDDLE_BLOCK_END = 2
+MIDDLE_BLOCK_START_END = 3
+
+TAIL_SPREAD = 0
+TAIL_START = 1
 
 Range = Tuple[int, int]
 
@@ -63,24 +75,31 @@ def retain_local(local: Range) -> List[int]:
 
 def retain_middle(middle: Range, budget: int, mode: int, block_grid_origin: int,
                   block_size: int) -> List[int]:
-    """Eq. 3 (block-start mode) or its token-budget generalisation (strided mode)."""
+    """Eq. 3 (block-start mode), the Table 2 variants that keep each middle
+    block's end token instead or both end tokens, or the token-budget
+    generalisation (strided mode)."""
     lo, hi = middle
     length = hi - lo
     if length <= 0:
         return []
-    if mode == MIDDLE_BLOCK_START:
-        return [p for p in range(lo, hi) if (p - block_grid_origin) % block_size == 0]
+    if mode in (MIDDLE_BLOCK_START, MIDDLE_BLOCK_END, MIDDLE_BLOCK_START_END):
+        keep = {MIDDLE_BLOCK_START: (0,), MIDDLE_BLOCK_END: (block_size - 1,),
+                MIDDLE_BLOCK_START_END: (0, block_size - 1)}[mode]
+        return [p for p in range(lo, hi) if (p - block_grid_origin) % block_size in keep]
     m = min(budget, length)
     return [lo + (i * length) // m for i in range(m)]
 
 
-def retain_tail(tail: Range, budget: int) -> List[int]:
-    """Eq. 4: start and end token of the last block; generalised to T evenly spread tokens."""
+def retain_tail(tail: Range, budget: int, mode: int = TAIL_SPREAD) -> List[int]:
+    """Eq. 4: start and end token of the last block; generalised to T evenly
+    spread tokens, or (start mode, Table 2) the start token alone."""
     lo, hi = tail
     length = hi - lo
     t = min(budget, length)
     if t <= 0:
         return []
+    if mode == TAIL_START:
+        return [lo]
     if t == 1:
         return [hi - 1]
     return [lo + (i * (length - 1)) // (t - 1) for i in range(t)]
@@ -93,13 +112,13 @@ class Retained(NamedTuple):
 
 def retained_suffix(prompt_len: int, gen_len: int, block_size: int, block_idx: int,
                     local_budget: int, middle_budget: int, middle_mode: int,
-                    tail_budget: int) -> Retained:
+                    tail_budget: int, tail_mode: int = TAIL_SPREAD) -> Retained:
     """Eq. 5: R_t = R_local U R_middle U R_tail, in ascending position order."""
     local, middle, tail = suffix_partition(prompt_len, gen_len, block_size, block_idx,
                                            local_budget)
     r_local = retain_local(local)
     r_middle = retain_middle(middle, middle_budget, middle_mode, prompt_len, block_size)
-    r_tail = retain_tail(tail, tail_budget)
+    r_tail = retain_tail(tail, tail_budget, tail_mode)
     pos = r_local + r_middle + r_tail
     reg = ([REGION_LOCAL] * len(r_local) + [REGION_MIDDLE] * len(r_middle)
            + [REGION_TAIL] * len(r_tail))
@@ -116,7 +135,7 @@ class Compacted(NamedTuple):
 
 def compacted_rows(prompt_len: int, gen_len: int, block_size: int, block_idx: int,
                    local_budget: int, middle_budget: int, middle_mode: int, tail_budget: int,
-                   include_prefix: bool) -> Compacted:
+                   include_prefix: bool, tail_mode: int = TAIL_SPREAD) -> Compacted:
     """Sparse input [P; B_t; R_t] ("Sparse Input Construction").
 
     The prefix P is the prompt plus every block decoded so far (a reading: the
@@ -127,7 +146,7 @@ def compacted_rows(prompt_len: int, gen_len: int, block_size: int, block_idx: in
     b = block_size
     P = prompt_len + block_idx * b
     r = retained_suffix(prompt_len, gen_len, b, block_idx, local_budget, middle_budget,
-                        middle_mode, tail_budget)
+                        middle_mode, tail_budget, tail_mode)
     pre = list(range(P)) if include_prefix else []
     blk = list(range(P, P + b))
     pos = np.array(pre + blk + r.positions, dtype=np.int32)

@@ -12,7 +12,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libssm.so")
 
 SSM_OK, SSM_E_INVAL, SSM_E_SHAPE, SSM_E_CAPACITY, SSM_E_HIP, SSM_E_UNSUPPORTED = 0, -1, -2, -3, -4, -5
-SSM_MIDDLE_STRIDED, SSM_MIDDLE_BLOCK_START = 0, 1
+SSM_MIDDLE_STRIDED, SSM_MIDDLE_BLOCK_START, SSM_MIDDLE_BLOCK_END, SSM_MIDDLE_BLOCK_START_END = 0, 1, 2, 3
+SSM_TAIL_SPREAD, SSM_TAIL_START = 0, 1
 SSM_UNMASK_TOPN, SSM_UNMASK_THRESHOLD, SSM_UNMASK_MARGIN = 0, 1, 2
 SSM_DT_F32, SSM_DT_BF16 = 0, 1
 SSM_ACT_BF16, SSM_ACT_BF16X2, SSM_ACT_BF16X2_FIRST = 0, 1, 2
@@ -32,7 +33,7 @@ class SSMError(RuntimeError):
 class SelectParams(C.Structure):
     _fields_ = [(n, C.c_int32) for n in (
         "prompt_len", "gen_len", "block_size", "block_idx", "local_budget", "middle_budget",
-        "middle_mode", "tail_budget", "include_prefix")]
+        "middle_mode", "tail_budget", "include_prefix", "tail_mode")]
 
 
 class Layer(C.Structure):
@@ -59,6 +60,7 @@ PI32 = C.POINTER(C.c_int32)
 
 _SIGS = {
     "ssm_select_count": (I32, [C.POINTER(SelectParams), PI32, PI32, PI32]),
+    "ssm_select_positions_host": (I32, [C.POINTER(SelectParams), PI32, C.POINTER(C.c_int8), I32, PI32]),
     "ssm_select_suffix": (I32, [C.POINTER(SelectParams), I32, I32, P, P, P, P, I32, PI32, PI32, PI32, P]),
     "ssm_embed_suffix": (I32, [C.POINTER(Model), I32, I32, P, I32, P, P, I32, P, P, P, I32, I32,
                                C.c_float, P, P]),

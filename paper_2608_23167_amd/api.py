@@ -6,6 +6,7 @@ Argument marshalling only: every step of the path runs in libssm.so.
 from __future__ import annotations
 
 import ctypes as C
+import numpy as np
 from typing import Optional, Tuple
 
 import torch
@@ -33,15 +34,27 @@ def _ptr(t: Optional[torch.Tensor], dtype=None, name="tensor") -> C.c_void_p:
 
 
 def select_params(prompt_len, gen_len, block_size, block_idx, local_budget, middle_budget,
-                  middle_mode, tail_budget, include_prefix) -> L.SelectParams:
+                  middle_mode, tail_budget, include_prefix, tail_mode=0) -> L.SelectParams:
     return L.SelectParams(prompt_len, gen_len, block_size, block_idx, local_budget, middle_budget,
-                          middle_mode, tail_budget, int(bool(include_prefix)))
+                          middle_mode, tail_budget, int(bool(include_prefix)), tail_mode)
 
 
 def ssm_select_count(p: L.SelectParams) -> Tuple[int, int, int]:
     n, s, f = C.c_int32(), C.c_int32(), C.c_int32()
     check(lib().ssm_select_count(C.byref(p), C.byref(n), C.byref(s), C.byref(f)), "ssm_select_count")
     return n.value, s.value, f.value
+
+
+def ssm_select_positions_host(p: L.SelectParams) -> Tuple[np.ndarray, np.ndarray]:
+    """(positions int32, regions int8) of the compacted rows, computed on the host."""
+    n_rows, _, _ = ssm_select_count(p)
+    pos = np.zeros(max(n_rows, 1), dtype=np.int32)
+    reg = np.zeros(max(n_rows, 1), dtype=np.int8)
+    n = C.c_int32()
+    check(lib().ssm_select_positions_host(
+        C.byref(p), pos.ctypes.data_as(C.POINTER(C.c_int32)),
+        reg.ctypes.data_as(C.POINTER(C.c_int8)), pos.size, C.byref(n)), "ssm_select_positions_host")
+    return pos[:n.value], reg[:n.value]
 
 
 def ssm_select_suffix(p: L.SelectParams, tokens: torch.Tensor, pos: torch.Tensor,

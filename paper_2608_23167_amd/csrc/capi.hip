@@ -47,8 +47,10 @@ int32_t layout_of(const ssm_select_params* p, SelectLayout& L) {
   if (j < 0 || j >= G / b) return fail(SSM_E_INVAL, "block_idx %d not in [0, %d)", j, G / b);
   if (p->local_budget < 0 || p->middle_budget < 0 || p->tail_budget < 0)
     return fail(SSM_E_INVAL, "negative budget");
-  if (p->middle_mode != SSM_MIDDLE_STRIDED && p->middle_mode != SSM_MIDDLE_BLOCK_START)
+  if (p->middle_mode < SSM_MIDDLE_STRIDED || p->middle_mode > SSM_MIDDLE_BLOCK_START_END)
     return fail(SSM_E_INVAL, "unknown middle_mode %d", p->middle_mode);
+  if (p->tail_mode != SSM_TAIL_SPREAD && p->tail_mode != SSM_TAIL_START)
+    return fail(SSM_E_INVAL, "unknown tail_mode %d", p->tail_mode);
   if (p->include_prefix != 0 && p->include_prefix != 1)
     return fail(SSM_E_INVAL, "include_prefix must be 0 or 1");
   if ((long long)P0 + G > 0x3fffffff) return fail(SSM_E_INVAL, "sequence too long");
@@ -63,21 +65,40 @@ int32_t layout_of(const ssm_select_params* p, SelectLayout& L) {
   const int tail_lo = (L.s0 + L.n_local > s_end - b) ? L.s0 + L.n_local : s_end - b;
   L.mid_lo = L.s0 + L.n_local;
   L.mid_len = tail_lo - L.mid_lo;
-  L.mid_mode = p->middle_mode;
+  // with one-token blocks a block's start is its end
+  L.mid_mode = (p->middle_mode == SSM_MIDDLE_BLOCK_START_END && b == 1) ? SSM_MIDDLE_BLOCK_START
+                                                                       : p->middle_mode;
   L.mid_first = 0;
+  L.mid_alt = 0;
   if (L.mid_len <= 0) {
     L.n_mid = 0;
-  } else if (p->middle_mode == SSM_MIDDLE_BLOCK_START) {   // Eq. 3
-    const int off = L.mid_lo - L.s0;
-    L.mid_first = L.s0 + ((off + b - 1) / b) * b;
-    const int mid_hi = L.mid_lo + L.mid_len;
-    L.n_mid = L.mid_first < mid_hi ? (mid_hi - L.mid_first + b - 1) / b : 0;
-  } else {
+  } else if (L.mid_mode == SSM_MIDDLE_STRIDED) {
     L.n_mid = p->middle_budget < L.mid_len ? p->middle_budget : L.mid_len;
+  } else {
+    // block grid from s0; the middle ends on a block boundary (the tail is the
+    // last block) but may start inside a block cut by the local region
+    const int off = L.mid_lo - L.s0, mid_hi = L.mid_lo + L.mid_len;
+    const int first_start = L.s0 + ((off + b - 1) / b) * b;      // Eq. 3
+    const int first_end = L.s0 + (off / b) * b + b - 1;
+    const int n_start = first_start < mid_hi ? (mid_hi - first_start) / b : 0;
+    const int n_end = first_end < mid_hi ? (mid_hi - first_end + b - 1) / b : 0;
+    if (L.mid_mode == SSM_MIDDLE_BLOCK_START) {
+      L.mid_first = first_start;
+      L.n_mid = n_start;
+    } else if (L.mid_mode == SSM_MIDDLE_BLOCK_END) {
+      L.mid_first = first_end;
+      L.n_mid = n_end;
+    } else {   // start and end tokens, in position order
+      L.mid_alt = first_end < first_start;
+      L.mid_first = L.mid_alt ? first_end : first_start;
+      L.n_mid = n_start + n_end;
+    }
   }
   L.tail_lo = tail_lo;
   L.tail_len = s_end - tail_lo;
+  L.tail_mode = p->tail_mode;
   L.n_tail = p->tail_budget < L.tail_len ? p->tail_budget : L.tail_len;   // Eq. 4
+  if (L.tail_mode == SSM_TAIL_START && L.n_tail > 1) L.n_tail = 1;
   L.n_suffix = L.n_local + L.n_mid + L.n_tail;                           // Eq. 5
   L.n_rows = L.n_prefix + b + L.n_suffix;
   return SSM_OK;
@@ -243,6 +264,23 @@ int32_t ssm_select_count(const ssm_select_params* p, int32_t* n_rows, int32_t* n
   if (n_rows) *n_rows = L.n_rows;
   if (n_suffix) *n_suffix = L.n_suffix;
   if (first_out_row) *first_out_row = L.n_prefix;
+  return ok();
+}
+
+int32_t ssm_select_positions_host(const ssm_select_params* p, int32_t* pos, int8_t* region,
+                                  int32_t cap, int32_t* n_rows) {
+  SelectLayout L;
+  int32_t rc = layout_of(p, L);
+  if (rc) return rc;
+  if (!pos) return fail(SSM_E_INVAL, "null position array");
+  if (cap < L.n_rows) return fail(SSM_E_CAPACITY, "cap %d < n_rows %d", cap, L.n_rows);
+  for (int r = 0; r < L.n_rows; ++r) {
+    int q, g;
+    row_position(L, r, q, g);
+    pos[r] = q;
+    if (region) region[r] = (int8_t)g;
+  }
+  if (n_rows) *n_rows = L.n_rows;
   return ok();
 }
 

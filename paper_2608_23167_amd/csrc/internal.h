@@ -39,10 +39,44 @@ struct SelectLayout {
   int b;             // block size
   int s0;            // first suffix position
   int n_local;       // local tokens [s0, s0 + n_local)
-  int mid_lo, mid_len, n_mid, mid_mode, mid_first;
-  int tail_lo, tail_len, n_tail;
+  int mid_lo, mid_len, n_mid, mid_mode;
+  int mid_first;     // block modes: the first kept middle position
+  int mid_alt;       // start+end mode: 1 if that position is a block end (the
+                     // first middle block is cut by the local region)
+  int tail_lo, tail_len, n_tail, tail_mode;
   int n_suffix, n_rows;
 };
+
+// Row r of [prefix; block; local; middle; tail] -> (position, region).  Every
+// row is computed independently in closed form, so the kernel is a pure
+// coalesced map over rows.
+__host__ __device__ inline void row_position(const SelectLayout& L, int r, int& p, int& g) {
+  if (r < L.n_prefix) { p = r; g = 0; return; }
+  r -= L.n_prefix;
+  if (r < L.b) { p = L.P + r; g = 1; return; }
+  r -= L.b;
+  if (r < L.n_local) { p = L.s0 + r; g = 2; return; }
+  r -= L.n_local;
+  if (r < L.n_mid) {
+    if (L.mid_mode == 0) {
+      p = L.mid_lo + (int)(((long long)r * L.mid_len) / L.n_mid);
+    } else if (L.mid_mode != 3) {            // block starts or block ends
+      p = L.mid_first + r * L.b;
+    } else if (L.mid_alt && r == 0) {        // the end of a block cut by the local region
+      p = L.mid_first;
+    } else {                                 // start, end of each block in turn
+      const int q = r - L.mid_alt;
+      p = L.mid_first + L.mid_alt + (q >> 1) * L.b + (q & 1) * (L.b - 1);
+    }
+    g = 3;
+    return;
+  }
+  r -= L.n_mid;
+  if (L.tail_mode == 1) p = L.tail_lo;
+  else if (L.n_tail == 1) p = L.tail_lo + L.tail_len - 1;
+  else p = L.tail_lo + (int)(((long long)r * (L.tail_len - 1)) / (L.n_tail - 1));
+  g = 4;
+}
 
 hipError_t launch_select(const SelectLayout& L, int batch, int seq_len, const int32_t* tokens,
                          int32_t* pos, int32_t* tok_c, int8_t* region, int cap, hipStream_t st);

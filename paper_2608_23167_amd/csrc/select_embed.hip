@@ -4,28 +4,6 @@
 
 namespace ssm {
 
-// Row r of [prefix; block; local; middle; tail] -> (position, region).  Every
-// row is computed independently in closed form, so the kernel is a pure
-// coalesced map over rows.
-__device__ __forceinline__ void row_position(const SelectLayout& L, int r, int& p, int& g) {
-  if (r < L.n_prefix) { p = r; g = 0; return; }
-  r -= L.n_prefix;
-  if (r < L.b) { p = L.P + r; g = 1; return; }
-  r -= L.b;
-  if (r < L.n_local) { p = L.s0 + r; g = 2; return; }
-  r -= L.n_local;
-  if (r < L.n_mid) {
-    if (L.mid_mode == 1) p = L.mid_first + r * L.b;
-    else p = L.mid_lo + (int)(((long long)r * L.mid_len) / L.n_mid);
-    g = 3;
-    return;
-  }
-  r -= L.n_mid;
-  if (L.n_tail == 1) p = L.tail_lo + L.tail_len - 1;
-  else p = L.tail_lo + (int)(((long long)r * (L.tail_len - 1)) / (L.n_tail - 1));
-  g = 4;
-}
-
 __global__ void __launch_bounds__(256) select_kernel(SelectLayout L, const int32_t* __restrict__ tokens,
                                                      int seq_len, int32_t* __restrict__ pos,
                                                      int32_t* __restrict__ tok_c,
@@ -39,7 +17,7 @@ __global__ void __launch_bounds__(256) select_kernel(SelectLayout L, const int32
     pos[r] = p;
     if (region) region[r] = (int8_t)g;
   }
-  tok_c[(size_t)s * cap + r] = tokens[(size_t)s * seq_len + p];
+  tok_c[(size_t)s * cap + r] = (p >= 0 && p < seq_len) ? tokens[(size_t)s * seq_len + p] : -1;
 }
 
 hipError_t launch_select(const SelectLayout& L, int batch, int seq_len, const int32_t* tokens,

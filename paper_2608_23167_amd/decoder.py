@@ -72,7 +72,7 @@ class Decoder:
         wl = self.wl
         return select_params(wl.prompt_len, wl.gen_len, wl.block_size, block_idx,
                              wl.local_budget, wl.middle_budget, wl.middle_mode, wl.tail_budget,
-                             include_prefix)
+                             include_prefix, wl.tail_mode)
 
     def reset(self, tokens0: torch.Tensor) -> None:
         self.tokens.copy_(tokens0)

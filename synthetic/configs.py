@@ -62,6 +62,12 @@ MARGIN = "margin"
 # middle-region modes
 MIDDLE_STRIDED = 0        # evenly strided token budget
 MIDDLE_BLOCK_START = 1    # start token of every middle block (Eq. 3)
+MIDDLE_BLOCK_END = 2      # end token of every middle block (Table 2 variant)
+MIDDLE_BLOCK_START_END = 3   # both (Table 2 variant)
+
+# tail-region modes
+TAIL_SPREAD = 0           # T evenly spread tokens, both ends first (Eq. 4 at T = 2)
+TAIL_START = 1            # the start token only (Table 2 variant)
 
 
 @dataclass(frozen=True)
@@ -78,6 +84,7 @@ class Workload:
     middle_budget: int = 0
     tail_budget: int = 0
     middle_mode: int = MIDDLE_STRIDED
+    tail_mode: int = TAIL_SPREAD
     cache: bool = False
     batch: int = 1
     seed: int = 0

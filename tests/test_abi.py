@@ -6,6 +6,8 @@ import glob
 import os
 import re
 
+import numpy as np
+
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -64,9 +66,34 @@ def test_select_count_matches_oracle_sweep():
                 assert got == (len(c.pos), c.n_suffix, c.first_out_row)
 
 
+def test_host_positions_match_oracle_in_every_mode():
+    """ssm_select_positions_host evaluates the kernel's per-row closed form on
+    the host: bit-exact against the oracle's lists for every middle and tail
+    mode, with local budgets that cut a block."""
+    import itertools
+    from oracle import selection as S
+    from paper_2608_23167_amd.api import ssm_select_positions_host
+    n = 0
+    for b, nb in ((1, 7), (2, 6), (3, 5), (8, 6), (32, 4)):
+        for j in range(nb):
+            for L, M, T, mmode, tmode, inc in itertools.product(
+                    (0, 1, b + 1, 2 * b, 3 * b - 1, b * nb), (0, 3, 100), (0, 1, 2, 3, 5),
+                    (0, 1, 2, 3), (0, 1), (0, 1)):
+                c = S.compacted_rows(7, b * nb, b, j, L, M, mmode, T, bool(inc), tmode)
+                pos, reg = ssm_select_positions_host(
+                    _params(prompt_len=7, gen_len=b * nb, block_size=b, block_idx=j,
+                            local_budget=L, middle_budget=M, middle_mode=mmode, tail_budget=T,
+                            include_prefix=inc, tail_mode=tmode))
+                assert np.array_equal(pos, c.pos) and np.array_equal(reg, c.region), \
+                    (b, nb, j, L, M, T, mmode, tmode, inc)
+                n += 1
+    assert n > 10000
+
+
 @pytest.mark.parametrize("bad", [dict(block_idx=4), dict(block_idx=-1), dict(gen_len=100),
                                  dict(block_size=0), dict(block_size=2048, gen_len=2048),
-                                 dict(local_budget=-1), dict(middle_mode=7), dict(prompt_len=-3),
+                                 dict(local_budget=-1), dict(middle_mode=7), dict(middle_mode=4),
+                                 dict(tail_mode=2), dict(tail_mode=-1), dict(prompt_len=-3),
                                  dict(include_prefix=2)])
 def test_select_rejects_invalid(bad):
     from paper_2608_23167_amd import _lib as L

@@ -14,15 +14,15 @@ from synthetic import WORKLOADS, seeded_normal, seeded_uniform_ints
 pytestmark = pytest.mark.gpu
 
 
-def _select_gpu(P0, G, b, j, Lb, Mb, mode, Tb, incl, tokens):
+def _select_gpu(P0, G, b, j, Lb, Mb, mode, Tb, incl, tokens, tmode=0):
     from paper_2608_23167_amd.api import select_params, ssm_select_suffix
     B = tokens.shape[0]
     cap = P0 + G + 8
     pos = torch.full((cap,), -7, dtype=torch.int32, device="cuda")
     tok_c = torch.full((B, cap), -7, dtype=torch.int32, device="cuda")
     region = torch.full((cap,), -7, dtype=torch.int8, device="cuda")
-    n, ns, f = ssm_select_suffix(select_params(P0, G, b, j, Lb, Mb, mode, Tb, incl), tokens, pos,
-                                 tok_c, region)
+    n, ns, f = ssm_select_suffix(select_params(P0, G, b, j, Lb, Mb, mode, Tb, incl, tmode), tokens,
+                                 pos, tok_c, region)
     torch.cuda.synchronize()
     return n, ns, f, pos.cpu().numpy(), region.cpu().numpy(), tok_c.cpu().numpy()
 
@@ -49,20 +49,26 @@ def test_select_matches_oracle_on_workloads(gpu, name):
 
 
 def test_select_brute_force_sweep(gpu):
+    """Every middle mode (strided, block start, block end, both) and tail mode
+    (spread, start only), local budgets that cut a block included."""
     tokens = seeded_uniform_ints((1, 5 + 64), 0, 1000, 2, "sweep").to("cuda")
     tok_np = tokens.cpu().numpy()
-    for b, nb in ((4, 16), (8, 8), (1, 12)):
+    cases = 0
+    for b, nb in ((4, 16), (8, 8), (1, 12), (3, 7)):
         G = b * nb
         for j in range(nb):
-            for Lb, Mb, Tb, mode in itertools.product((0, 1, b, 3 * b + 1, G), (0, 2, 5, G),
-                                                      (0, 1, 2, 3, b), (0, 1)):
-                c = S.compacted_rows(5, G, b, j, Lb, Mb, mode, Tb, True)
-                n, ns, f, pos, reg, tc = _select_gpu(5, G, b, j, Lb, Mb, mode, Tb, True,
-                                                     tokens[:, :5 + G].contiguous())
-                assert n == len(c.pos) and ns == c.n_suffix
-                assert np.array_equal(pos[:n], c.pos), (b, j, Lb, Mb, Tb, mode)
-                assert np.array_equal(reg[:n], c.region)
-                assert np.array_equal(tc[0, :n], tok_np[0, c.pos])
+            for Lb, mode, Tb, tmode in itertools.product((0, 1, b, b + 2, 3 * b + 1, G), range(4),
+                                                         (0, 1, 2, 3, b), (0, 1)):
+                for Mb in ((0, 2, 5, G) if mode == S.MIDDLE_STRIDED else (0,)):
+                    c = S.compacted_rows(5, G, b, j, Lb, Mb, mode, Tb, True, tmode)
+                    n, ns, f, pos, reg, tc = _select_gpu(5, G, b, j, Lb, Mb, mode, Tb, True,
+                                                         tokens[:, :5 + G].contiguous(), tmode)
+                    assert n == len(c.pos) and ns == c.n_suffix
+                    assert np.array_equal(pos[:n], c.pos), (b, j, Lb, Mb, Tb, mode, tmode)
+                    assert np.array_equal(reg[:n], c.region)
+                    assert np.array_equal(tc[0, :n], tok_np[0, c.pos])
+                    cases += 1
+    print(f"[select sweep] {cases} cases", flush=True)
 
 
 @pytest.mark.parametrize("dtype,d,V,k", [("f32", 128, 512, 5), ("bf16", 4096, 2048, 5),

@@ -89,6 +89,32 @@ def test_tiny_fp32_cached_steps(gpu):
             _compare_step(out, rec, wl, fp32=True)
 
 
+@pytest.mark.parametrize("local,mmode,T,tmode", [
+    (64, 1, 2, 0),    # the paper's block rule (Eq. 2-4): w = 2 blocks, middle starts, tail ends
+    (40, 3, 1, 1),    # Table 2 variants: middle start+end tokens, tail start token only
+    (40, 2, 3, 0),    # middle end tokens, tail start+mid+end
+])
+def test_tiny_fp32_selection_variants(gpu, local, mmode, T, tmode):
+    """Whole teacher-forced generations of the tiny model (cached) under the
+    paper's block rule and the Table 2 retention variants; a local budget of 40
+    cuts a block, so the middle starts inside one."""
+    wl = sharpened(WORKLOADS["tiny"], 60.0).replace(
+        cache=True, gen_len=192, local_budget=local, middle_mode=mmode, tail_budget=T,
+        tail_mode=tmode)
+    mw = make_weights(wl.model, seed=3, norm_jitter=0.1, logit_scale=wl.logit_scale)
+    w = OG.NumpyWeights(mw)
+    dec = _decoder(wl, mw.to("cuda"))
+    st = OG.OracleState.start(initial_tokens(wl, seed=4).numpy(), wl.topk)
+    for j in range(wl.n_blocks):
+        for i in range(2):
+            before = st.copy()
+            rec = OG.step(wl, w, st, j, i == 0)
+            load_oracle_state(dec, before)
+            out = gpu_step(dec, j, i == 0)
+            _compare_step(out, rec, wl, fp32=True)
+            _compare_unmask(out, rec, wl)
+
+
 def _state_from(wl, block_idx, step, seed):
     t, pi, pw, ps = mid_generation_state(wl, block_idx, step, seed)
     st = OG.OracleState.start(t, wl.topk)

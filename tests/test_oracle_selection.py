@@ -35,8 +35,9 @@ def _golden_cases():
 
 @pytest.mark.parametrize("params,expected", _golden_cases())
 def test_golden_retained_sets(params, expected):
-    prompt, gen, b, j, L, M, mode, T = params
-    r = S.retained_suffix(prompt, gen, b, j, L, M, mode, T)
+    prompt, gen, b, j, L, M, mode, T = params[:8]
+    tail_mode = params[8] if len(params) > 8 else S.TAIL_SPREAD
+    r = S.retained_suffix(prompt, gen, b, j, L, M, mode, T, tail_mode)
     assert r.positions == expected
 
 
@@ -74,6 +75,69 @@ def test_block_budgets_reduce_to_paper_rule(b):
                         # a one-token block: its start and end coincide
                         want = sorted(set(want))
                     assert r.positions == want, (prompt, gen, b, j, w)
+
+
+def paper_block_variant(prompt, gen, b, j, w, middle_keep, tail_keep):
+    """Table 2 variants over blocks: middle blocks keep the in-block offsets
+    `middle_keep`, the tail block keeps `tail_keep` (offsets from its start)."""
+    nb = gen // b
+    suffix_blocks = list(range(j + 1, nb))
+    start = lambda m: prompt + m * b
+    if len(suffix_blocks) <= w:
+        return sorted(p for m in suffix_blocks for p in range(start(m), start(m) + b))
+    r = set()
+    for m in suffix_blocks[:w]:
+        r.update(range(start(m), start(m) + b))
+    for m in suffix_blocks[w:-1]:
+        r.update(start(m) + o for o in middle_keep)
+    r.update(start(suffix_blocks[-1]) + o for o in tail_keep)
+    return sorted(r)
+
+
+@pytest.mark.parametrize("b", [1, 2, 5, 8])
+def test_table2_variants_reduce_to_block_rule(b):
+    """Middle end / start+end tokens; tail start only, end only, start+mid+end."""
+    variants = [
+        (S.MIDDLE_BLOCK_END, 2, S.TAIL_SPREAD, (b - 1,), (0, b - 1)),
+        (S.MIDDLE_BLOCK_START_END, 2, S.TAIL_SPREAD, (0, b - 1), (0, b - 1)),
+        (S.MIDDLE_BLOCK_START, 1, S.TAIL_START, (0,), (0,)),
+        (S.MIDDLE_BLOCK_START, 1, S.TAIL_SPREAD, (0,), (b - 1,)),
+        (S.MIDDLE_BLOCK_START, 3, S.TAIL_SPREAD, (0,), (0, (b - 1) // 2, b - 1)),
+    ]
+    for nb in range(1, 9):
+        gen = nb * b
+        for prompt in (0, 3):
+            for w in range(0, 4):
+                for j in range(nb):
+                    for mmode, T, tmode, mk, tk in variants:
+                        r = S.retained_suffix(prompt, gen, b, j, w * b, 0, mmode, T, tmode)
+                        want = paper_block_variant(prompt, gen, b, j, w, mk, tk)
+                        assert r.positions == want, (prompt, gen, b, j, w, mmode, T, tmode)
+
+
+def test_brute_force_block_modes():
+    """Block modes with local budgets that cut a block: sorted, unique, the
+    middle keeps exactly the in-range tokens at the mode's block offsets, the
+    start-only tail keeps its first token."""
+    prompt = 3
+    for gen_blocks, b in itertools.product(range(1, 8), (1, 2, 3, 8)):
+        gen = gen_blocks * b
+        for j in range(gen_blocks):
+            for L in (0, 1, b - 1, b + 1, 2 * b + 3, gen):
+                for mmode, keep in ((S.MIDDLE_BLOCK_START, {0}), (S.MIDDLE_BLOCK_END, {b - 1}),
+                                    (S.MIDDLE_BLOCK_START_END, {0, b - 1})):
+                    for T, tmode in itertools.product((0, 1, 2, 3), (S.TAIL_SPREAD, S.TAIL_START)):
+                        r = S.retained_suffix(prompt, gen, b, j, max(L, 0), 7, mmode, T, tmode)
+                        pos, reg = r.positions, r.regions
+                        s0, s_end = prompt + (j + 1) * b, prompt + gen
+                        assert pos == sorted(set(pos))
+                        l = min(max(L, 0), s_end - s0)
+                        tail_lo = max(s0 + l, s_end - b)
+                        mid = [p for p, g in zip(pos, reg) if g == S.REGION_MIDDLE]
+                        assert mid == [p for p in range(s0 + l, tail_lo) if (p - prompt) % b in keep]
+                        tail = [p for p, g in zip(pos, reg) if g == S.REGION_TAIL]
+                        if tmode == S.TAIL_START:
+                            assert tail == ([tail_lo] if T >= 1 and tail_lo < s_end else [])
 
 
 def test_brute_force_properties():

@@ -323,6 +323,25 @@ int32_t ssm_unmask(int32_t* d_tokens, int32_t batch, int32_t seq_len, int32_t bl
                    void* stream);
 
 /* ------------------------------------------------------------------------ */
+/* Early termination (Section 3.2, "Early Termination"; the fill rule of    */
+/* Section 4.4).                                                             */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Called after the last step of a block.  Every sequence s with d_done[s] == 0
+ * whose block [block_start, block_start + block_size) holds eos_id gets all
+ * later positions [block_start + block_size, seq_len) set to eos_id and
+ * d_done[s] = 1; sequences already done are left as they are.
+ *   d_tokens [batch, seq_len] int32 (in place), d_done [batch] int32, zeroed by
+ *   the caller at the start of a generation.
+ * The generation can stop once every d_done[s] is 1 (the caller copies
+ * d_done to the host to find out).  SSM_E_INVAL for a block outside the
+ * sequence, eos_id < 0 or a null pointer.
+ */
+int32_t ssm_early_stop(int32_t* d_tokens, int32_t batch, int32_t seq_len, int32_t block_start,
+                       int32_t block_size, int32_t eos_id, int32_t* d_done, void* stream);
+
+/* ------------------------------------------------------------------------ */
 /* Launch timing (tracing aid; off by default).                             */
 /* ------------------------------------------------------------------------ */
 
@@ -331,7 +350,7 @@ int32_t ssm_unmask(int32_t* d_tokens, int32_t batch, int32_t seq_len, int32_t bl
  * bracketed by a pair of HIP events on the call's stream (created without
  * the system-scope fence), recorded under a tag naming the operation ("select", "embed",
  * "rope_table", "norm", "gemm_qkv", "attention", "gemm_o", "gemm_gate_up",
- * "gemm_down", "gemm_lm_head", "rowstats", "unmask") and the kernel's
+ * "gemm_down", "gemm_lm_head", "rowstats", "unmask", "early_stop") and the kernel's
  * ordinal within one call of that operation (0 = the main kernel; split-K
  * reductions and merges come after).  Each call discards earlier records.
  * Not thread-safe; meant for a single profiling thread.

@@ -11,10 +11,16 @@ One step, in the paper's order:
   6. remember the top-k prediction of every retained suffix row for the next step.
 
 Steps are numbered 0, 1, 2, ... over the whole generation; the paper's
-"previous timestep t+1" is step s-1 here.  Readings: early termination is not
-used (random-init models have no meaningful end token); with a fixed top-n
-rule a block takes ceil(b/n) steps, with the threshold or margin rule it
-steps until the block has no mask left.
+"previous timestep t+1" is step s-1 here.  With a fixed top-n rule a block
+takes ceil(b/n) steps, with the threshold or margin rule it steps until the
+block has no mask left.
+
+Early termination (Section 3.2, "Early Termination"; the fill rule of
+Section 4.4) is optional (workload eos_id >= 0): after the last step of a
+block, a sequence whose block holds the end-of-sequence id has every later
+position set to that id and is done; the generation stops once every
+sequence is done.  Random-init models have no meaningful end token, so the
+workloads leave it off.
 """
 from __future__ import annotations
 
@@ -79,18 +85,20 @@ class OracleState:
     pred_step: np.ndarray               # [B, L_tot] int32, -1 = none
     step: int = 0
     cache: Optional[list] = None        # per sequence: per layer (k, v) of the prefix
+    done: Optional[np.ndarray] = None   # [B] bool: ended by early termination
 
     @staticmethod
     def start(tokens: np.ndarray, k: int) -> "OracleState":
         B, L = tokens.shape
         return OracleState(np.array(tokens, dtype=np.int32).copy(),
                            np.zeros((B, L, k), np.int32), np.zeros((B, L, k), np.float64),
-                           np.full((B, L), -1, np.int32))
+                           np.full((B, L), -1, np.int32), done=np.zeros(B, dtype=bool))
 
     def copy(self) -> "OracleState":
         return OracleState(self.tokens.copy(), self.pred_ids.copy(), self.pred_w.copy(),
                            self.pred_step.copy(), self.step,
-                           None if self.cache is None else [list(c) for c in self.cache])
+                           None if self.cache is None else [list(c) for c in self.cache],
+                           None if self.done is None else self.done.copy())
 
 
 @dataclass
@@ -156,6 +164,20 @@ def step(wl, w: NumpyWeights, st: OracleState, block_idx: int, first_in_block: b
     return rec
 
 
+def early_stop(tokens: np.ndarray, done: np.ndarray, block_start: int, block_size: int,
+               eos_id: int) -> bool:
+    """Early termination check after a block (Section 3.2; fill rule of Section
+    4.4): every sequence not yet done whose block holds eos_id gets all later
+    positions set to eos_id and becomes done.  Returns whether all are done."""
+    for s in range(tokens.shape[0]):
+        if done[s]:
+            continue
+        if np.any(tokens[s, block_start:block_start + block_size] == eos_id):
+            tokens[s, block_start + block_size:] = eos_id
+            done[s] = True
+    return bool(np.all(done))
+
+
 def block_done(wl, st: OracleState, block_idx: int) -> bool:
     P = wl.prompt_len + block_idx * wl.block_size
     return not np.any(st.tokens[:, P:P + wl.block_size] == wl.model.mask_id)
@@ -182,4 +204,7 @@ def generate(wl, w: NumpyWeights, tokens0: np.ndarray, keep: bool = False,
             i += 1
             if max_steps is not None and len(recs) >= max_steps:
                 return st, recs
+        if wl.eos_id >= 0 and early_stop(st.tokens, st.done, wl.prompt_len + j * wl.block_size,
+                                         wl.block_size, wl.eos_id):
+            break
     return st, recs

@@ -69,6 +69,7 @@ _SIGS = {
                                I32, P, P, P, P, P, P, P, C.c_size_t, P]),
     "ssm_unmask": (I32, [P, I32, I32, I32, I32, I32, I32, I32, C.c_float, P, P, P, P, I32, I32, P,
                          I32, P, P, P, P, P, P]),
+    "ssm_early_stop": (I32, [P, I32, I32, I32, I32, I32, P, P]),
     "ssm_attention_workspace_size": (I32, [I32, I32, I32, C.POINTER(C.c_size_t)]),
     "ssm_attention": (I32, [I32, I32, I32, I32, I32, I32, P, P, P, P, P, C.c_size_t, P]),
     "ssm_gather_rows": (I32, [I32, I32, I32, P, P, I32, P, P]),

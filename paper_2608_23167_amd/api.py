@@ -171,8 +171,18 @@ def ssm_unmask(tokens: torch.Tensor, block_start: int, block_size: int, mask_id:
     check(rc, "ssm_unmask")
 
 
+def ssm_early_stop(tokens: torch.Tensor, block_start: int, block_size: int, eos_id: int,
+                   done: torch.Tensor, stream=None) -> None:
+    B, seq_len = tokens.shape
+    if done.numel() != B:
+        raise ValueError("done must hold one int32 per sequence")
+    rc = lib().ssm_early_stop(_ptr(tokens, torch.int32, "tokens"), B, seq_len, block_start,
+                              block_size, eos_id, _ptr(done, torch.int32, "done"), _stream(stream))
+    check(rc, "ssm_early_stop")
+
+
 PROFILE_TAGS = ("select", "embed", "rope_table", "norm", "gemm_qkv", "attention", "gemm_o",
-                "gemm_gate_up", "gemm_down", "gemm_lm_head", "rowstats", "unmask")
+                "gemm_gate_up", "gemm_down", "gemm_lm_head", "rowstats", "unmask", "early_stop")
 
 
 def ssm_profile_enable(on: bool) -> None:

@@ -514,6 +514,19 @@ int32_t ssm_unmask(int32_t* d_tokens, int32_t batch, int32_t seq_len, int32_t bl
   return ok();
 }
 
+int32_t ssm_early_stop(int32_t* d_tokens, int32_t batch, int32_t seq_len, int32_t block_start,
+                       int32_t block_size, int32_t eos_id, int32_t* d_done, void* stream) {
+  if (batch < 1 || seq_len < 1) return fail(SSM_E_INVAL, "bad batch / seq_len");
+  if (block_size < 1 || block_start < 0 || block_start + block_size > seq_len)
+    return fail(SSM_E_INVAL, "block [%d, %d) outside the sequence", block_start, block_start + block_size);
+  if (eos_id < 0) return fail(SSM_E_INVAL, "eos_id %d < 0", eos_id);
+  if (!d_tokens || !d_done) return fail(SSM_E_INVAL, "null device pointer");
+  hipStream_t st = (hipStream_t)stream;
+  PROF_TRY("early_stop", launch_early_stop(d_tokens, batch, seq_len, block_start, block_size,
+                                           eos_id, d_done, st));
+  return ok();
+}
+
 int32_t ssm_profile_enable(int32_t on) {
   g_prof_on = on != 0;
   prof_clear();

@@ -239,5 +239,7 @@ hipError_t launch_unmask(int32_t* tokens, int batch, int seq_len, int block_star
                          const float* topk_w, int k, int n_out, const int32_t* pos_out, int step,
                          int32_t* pred_ids, float* pred_w, int32_t* pred_step, uint8_t* selected,
                          int32_t* masked_left, hipStream_t st);
+hipError_t launch_early_stop(int32_t* tokens, int batch, int seq_len, int block_start, int b,
+                             int eos_id, int32_t* done, hipStream_t st);
 
 }  // namespace ssm

@@ -87,4 +87,33 @@ hipError_t launch_unmask(int32_t* tokens, int batch, int seq_len, int block_star
   return hipGetLastError();
 }
 
+// Early termination after a block (Section 3.2, "Early Termination"; the fill
+// rule of Section 4.4).  One workgroup per sequence: a sequence not yet done
+// whose block holds eos_id gets every later position set to eos_id and is
+// marked done.
+__global__ void __launch_bounds__(256) early_stop_kernel(int32_t* __restrict__ tokens, int seq_len,
+                                                         int block_start, int b, int eos_id,
+                                                         int32_t* __restrict__ done) {
+  __shared__ int found;
+  const int s = blockIdx.x, tid = threadIdx.x;
+  if (done[s]) return;                        // uniform over the workgroup
+  int32_t* tok = tokens + (size_t)s * seq_len;
+  if (tid == 0) found = 0;
+  __syncthreads();
+  int hit = 0;
+  for (int i = block_start + tid; i < block_start + b; i += blockDim.x) hit |= tok[i] == eos_id;
+  if (hit) found = 1;                         // benign race: every writer stores 1
+  __syncthreads();
+  if (!found) return;
+  for (int i = block_start + b + tid; i < seq_len; i += blockDim.x) tok[i] = eos_id;
+  if (tid == 0) done[s] = 1;
+}
+
+hipError_t launch_early_stop(int32_t* tokens, int batch, int seq_len, int block_start, int b,
+                             int eos_id, int32_t* done, hipStream_t st) {
+  launch(early_stop_kernel, dim3(batch), dim3(256), 0, st, tokens, seq_len, block_start, b, eos_id,
+         done);
+  return hipGetLastError();
+}
+
 }  // namespace ssm

@@ -13,7 +13,7 @@ from typing import Optional
 import torch
 
 from . import _lib as L
-from .api import (select_params, ssm_denoise_step, ssm_embed_suffix, ssm_select_count,
+from .api import (select_params, ssm_denoise_step, ssm_early_stop, ssm_embed_suffix, ssm_select_count,
                   ssm_select_suffix, ssm_unmask, ssm_workspace_size)
 from .model import DeviceKVCache, DeviceModel
 
@@ -64,6 +64,7 @@ class Decoder:
         self.pred_step = torch.full((B, Lt), -1, dtype=i32, device=device)
         self.selected = torch.zeros(B * wl.block_size, dtype=torch.uint8, device=device)
         self.masked_left = torch.zeros(B, dtype=i32, device=device)
+        self.done = torch.zeros(B, dtype=i32, device=device)
         self.ws = torch.zeros(ssm_workspace_size(model, B, cap), dtype=torch.uint8, device=device)
         self.cache = DeviceKVCache(shape, B, self.max_kv, device)
         self.step_idx = 0
@@ -77,6 +78,7 @@ class Decoder:
     def reset(self, tokens0: torch.Tensor) -> None:
         self.tokens.copy_(tokens0)
         self.pred_step.fill_(-1)
+        self.done.zero_()
         self.step_idx = 0
 
     def step(self, block_idx: int, first_in_block: bool, logits: Optional[torch.Tensor] = None,
@@ -131,4 +133,14 @@ class Decoder:
                     return self.tokens
                 if spb is None and int(self.masked_left.max().item()) == 0:
                     break
+            if wl.eos_id >= 0 and self.early_stop(j):
+                break
         return self.tokens
+
+    def early_stop(self, block_idx: int) -> bool:
+        """Early termination after block `block_idx`: fills the later blocks of
+        sequences that produced the end token; True once every sequence has."""
+        wl = self.wl
+        ssm_early_stop(self.tokens, wl.prompt_len + block_idx * wl.block_size, wl.block_size,
+                       wl.eos_id, self.done)
+        return bool(int(self.done.min().item()) == 1)

@@ -91,6 +91,7 @@ class Workload:
     topk: int = 5
     alpha: float = 0.4
     logit_scale: float = 1.0   # test-only sharpening applied to the LM head weights
+    eos_id: int = -1           # end-of-sequence id for early termination; -1: off
 
     @property
     def total_len(self) -> int:

@@ -211,3 +211,15 @@ def test_unmask_and_embed_validation():
     assert lib.ssm_embed_suffix(*e3) == L.SSM_E_INVAL
     e4 = list(e); e4[4] = 10
     assert lib.ssm_embed_suffix(*e4) == L.SSM_E_INVAL
+
+
+def test_early_stop_validation():
+    """Invalid early-termination calls return SSM_E_INVAL before any launch."""
+    from paper_2608_23167_amd import _lib as L
+    lib = L.lib()
+    fake = C.c_void_p(0x1000)
+    assert lib.ssm_early_stop(fake, 1, 64, 32, 32, -1, fake, None) == L.SSM_E_INVAL   # eos < 0
+    assert lib.ssm_early_stop(fake, 1, 64, 48, 32, 5, fake, None) == L.SSM_E_INVAL    # past the end
+    assert lib.ssm_early_stop(fake, 0, 64, 0, 32, 5, fake, None) == L.SSM_E_INVAL     # no sequence
+    assert lib.ssm_early_stop(None, 1, 64, 0, 32, 5, fake, None) == L.SSM_E_INVAL     # null tokens
+    assert lib.ssm_early_stop(fake, 1, 64, 0, 32, 5, None, None) == L.SSM_E_INVAL     # null flags

@@ -166,3 +166,30 @@ def test_unmask_matches_oracle(gpu, rule):
             assert np.all(ps[others] == -1)
             assert np.array_equal(pred_ids[s].cpu().numpy()[pos_out[b:]], topk_ids[s, b:])
             assert np.array_equal(pred_w[s].cpu().numpy()[pos_out[b:]], w[s, b:])
+
+
+def test_early_stop_matches_oracle(gpu):
+    """Early termination kernel: bit-exact fill and done flags against the
+    oracle, over sequences with and without the end id, some already done,
+    for every block of the sequence."""
+    from oracle import generate as OG
+    from paper_2608_23167_amd.api import ssm_early_stop
+    B, L, b, eos, P0 = 6, 5 + 8 * 16, 16, 11, 5
+    for seed in range(3):
+        tok = seeded_uniform_ints((B, L), 0, 40, 10 + seed, "es").numpy()
+        tok[tok == eos] = eos + 1
+        rng = np.random.default_rng(seed)
+        for s in range(B):                       # plant the end id in some blocks
+            for _ in range(rng.integers(0, 3)):
+                tok[s, rng.integers(P0, L)] = eos
+        done = (rng.random(B) < 0.2)
+        t_dev = torch.from_numpy(tok).to("cuda")
+        d_dev = torch.from_numpy(done.astype(np.int32)).to("cuda")
+        for j in range(8):
+            start = P0 + j * b
+            all_done = OG.early_stop(tok, done, start, b, eos)
+            ssm_early_stop(t_dev, start, b, eos, d_dev)
+            torch.cuda.synchronize()
+            assert np.array_equal(t_dev.cpu().numpy(), tok), (seed, j)
+            assert np.array_equal(d_dev.cpu().numpy().astype(bool), done), (seed, j)
+            assert all_done == bool(done.all())

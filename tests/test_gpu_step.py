@@ -115,6 +115,41 @@ def test_tiny_fp32_selection_variants(gpu, local, mmode, T, tmode):
             _compare_unmask(out, rec, wl)
 
 
+def test_tiny_fp32_early_termination(gpu):
+    """Teacher-forced generation of the tiny model (two sequences) with an end
+    id the model decodes in the first block: the GPU's per-block early-stop
+    fill and done flags match the oracle's, and the generation ends there."""
+    from paper_2608_23167_amd.api import ssm_early_stop
+    eos = 7
+    wl = WORKLOADS["tiny"].replace(batch=2, cache=True, eos_id=eos)
+    mw = make_weights(wl.model, seed=0, norm_jitter=0.1)
+    mw.lm_head[eos] *= 40.0          # logits of the end id about 40x the others' scale
+    w = OG.NumpyWeights(mw)
+    dec = _decoder(wl, mw.to("cuda"))
+    st = OG.OracleState.start(initial_tokens(wl).numpy(), wl.topk)
+    ended_at = None
+    for j in range(wl.n_blocks):
+        for i in range(wl.steps_per_block()):
+            before = st.copy()
+            rec = OG.step(wl, w, st, j, i == 0)
+            load_oracle_state(dec, before)
+            out = gpu_step(dec, j, i == 0)
+            _compare_step(out, rec, wl, fp32=True)
+            _compare_unmask(out, rec, wl)
+        # both sides apply the block-end check to the same (oracle) tokens
+        dec.tokens.copy_(torch.from_numpy(st.tokens))
+        dec.done.copy_(torch.from_numpy(st.done.astype(np.int32)))
+        all_done = OG.early_stop(st.tokens, st.done, wl.prompt_len + j * wl.block_size,
+                                 wl.block_size, eos)
+        assert dec.early_stop(j) == all_done
+        assert np.array_equal(dec.tokens.cpu().numpy(), st.tokens)
+        assert np.array_equal(dec.done.cpu().numpy().astype(bool), st.done)
+        if all_done:
+            ended_at = j
+            break
+    assert ended_at == 0
+
+
 def _state_from(wl, block_idx, step, seed):
     t, pi, pw, ps = mid_generation_state(wl, block_idx, step, seed)
     st = OG.OracleState.start(t, wl.topk)

@@ -144,3 +144,57 @@ def test_threshold_workload_terminates():
     st, recs = G.generate(wl, w, initial_tokens(wl).numpy())
     assert not np.any(st.tokens == wl.model.mask_id)
     assert len(recs) >= wl.n_blocks
+
+
+def test_early_stop_fill_rule():
+    """Early termination after a block (Section 3.2; fill rule of Section 4.4):
+    only sequences whose block holds the end id are filled from the block's end
+    on; a sequence already done is left alone; all done -> True."""
+    eos, b, L = 9, 4, 20
+    tok = np.arange(3 * L, dtype=np.int32).reshape(3, L) % 7 + 100
+    tok[0, 5] = eos                      # in block [4, 8) of sequence 0
+    tok[2, 13] = eos                     # in a later block of sequence 2
+    done = np.zeros(3, dtype=bool)
+    before = tok.copy()
+    assert not G.early_stop(tok, done, 4, b, eos)
+    assert list(done) == [True, False, False]
+    assert np.all(tok[0, 8:] == eos) and np.array_equal(tok[0, :8], before[0, :8])
+    assert np.array_equal(tok[1:], before[1:])
+    # block [12, 16): sequence 2 ends; sequence 0 is done already
+    tok[0, 8:] = 3                       # a done sequence is not touched again
+    assert not G.early_stop(tok, done, 12, b, eos)
+    assert list(done) == [True, False, True]
+    assert np.all(tok[0, 8:] == 3)
+    assert np.all(tok[2, 16:] == eos) and tok[2, 13] == eos
+    tok[1, 19] = eos                     # the last block: nothing after it to fill
+    assert G.early_stop(tok, done, 16, b, eos)
+    assert list(done) == [True, True, True]
+
+
+def _eos_model(wl, eos, boost):
+    mw = make_weights(wl.model, seed=0, norm_jitter=0.1)
+    mw.lm_head[eos] *= boost             # the end id wins wherever h . w_eos > 0
+    return mw
+
+
+def test_early_termination_stops_generation():
+    """With an end id that the model decodes in the first block, the generation
+    ends after that block: later blocks are all end ids and are never run; the
+    decoded first block equals that of the run without early termination."""
+    eos = 7
+    wl = WORKLOADS["tiny"].replace(batch=2)
+    mw = _eos_model(wl, eos, 40.0)
+    w = G.NumpyWeights(mw)
+    tok0 = initial_tokens(wl).numpy()
+    st_on, recs_on = G.generate(wl.replace(eos_id=eos), w, tok0)
+    st_off, recs_off = G.generate(wl, w, tok0)
+    spb = wl.steps_per_block()
+    blk_end = wl.prompt_len + wl.block_size
+    assert np.all(st_on.tokens[:, wl.prompt_len:blk_end] != wl.model.mask_id)
+    assert np.all(np.any(st_on.tokens[:, wl.prompt_len:blk_end] == eos, axis=1))
+    assert len(recs_on) == spb and len(recs_off) == wl.n_blocks * spb
+    assert np.all(st_on.tokens[:, blk_end:] == eos) and np.all(st_on.done)
+    assert np.array_equal(st_on.tokens[:, :blk_end], st_off.tokens[:, :blk_end])
+    # an end id the model never decodes changes nothing
+    st_none, recs_none = G.generate(wl.replace(eos_id=wl.model.mask_id), w, tok0)
+    assert len(recs_none) == len(recs_off) and np.array_equal(st_none.tokens, st_off.tokens)

@@ -367,7 +367,7 @@ __global__ void __launch_bounds__(512) gemm_bf16_kernel(Pol pol, const bf16_t* _
                                                         const bf16_t* __restrict__ Alo, int G,
                                                         int M, int k_per_split, int mt,
                                                         int n_split, float* __restrict__ part,
-                                                        int ldp) {
+                                                        int ldp, int krot) {
   static_assert(BM == 128, "4 compute waves of 32 rows");
   constexpr int BK = 64, LS = BK + 8;            // LDS row stride (elements), 144 B
   constexpr int FM = 2, FN = BN / 16;            // per compute wave: 32 rows x BN columns
@@ -390,6 +390,14 @@ __global__ void __launch_bounds__(512) gemm_bf16_kernel(Pol pol, const bf16_t* _
   const int kbeg = split * k_per_split;
   const int nk = k_per_split / BK;               // a multiple of 4 (host-checked)
   const int last = nk - 1;
+  // K-step kt of this tile reads K-step kmap(kt): column tiles start at
+  // different K offsets, so the weight rows read at any one time do not all
+  // share their low address bits
+  const int rot = krot ? (int)(((long long)t * krot) % nk) : 0;
+  auto kmap = [rot, nk](int k) {
+    const int x = k + rot;
+    return x >= nk ? x - nk : x;
+  };
   float* Cs = (float*)smem;
 
   if (wave < 4) {
@@ -417,8 +425,8 @@ __global__ void __launch_bounds__(512) gemm_bf16_kernel(Pol pol, const bf16_t* _
   do {                                                                                \
     _Pragma("unroll") for (int i = 0; i < FM; ++i)                                    \
     _Pragma("unroll") for (int kk = 0; kk < 2; ++kk) {                                \
-      RA[0][i][kk] = *(const u32x4_t*)(Ahi + a_off[i] + (KT) * a_kstep + kk * 512);  \
-      if (SPLIT) RA[NA - 1][i][kk] = *(const u32x4_t*)(Alo + a_off[i] + (KT) * a_kstep + kk * 512); \
+      RA[0][i][kk] = *(const u32x4_t*)(Ahi + a_off[i] + kmap(KT) * a_kstep + kk * 512);  \
+      if (SPLIT) RA[NA - 1][i][kk] = *(const u32x4_t*)(Alo + a_off[i] + kmap(KT) * a_kstep + kk * 512); \
     }                                                                                 \
   } while (0)
 #define READ_W(F, BUF, KK)                                                            \
@@ -490,7 +498,7 @@ __global__ void __launch_bounds__(512) gemm_bf16_kernel(Pol pol, const bf16_t* _
     u32x4_t s0[WR], s1[WR], s2[WR], s3[WR], s4[WR], s5[WR], s6[WR], s7[WR];   // stage s in set s % PW
 #define LOAD_S(S, KT)                                                                 \
   do {                                                                                \
-    _Pragma("unroll") for (int i = 0; i < WR; ++i) S[i] = *(const u32x4_t*)(w_src[i] + (KT) * BK); \
+    _Pragma("unroll") for (int i = 0; i < WR; ++i) S[i] = *(const u32x4_t*)(w_src[i] + kmap(KT) * BK); \
   } while (0)
 #define STORE_S(S, BUF)                                                               \
   do {                                                                                \
@@ -579,7 +587,7 @@ __global__ void __launch_bounds__(WM * WN * 64, (BM / WM) * (BN / WN) > 4096 ? 2
                                                           const bf16_t* __restrict__ Alo, int G,
                                                           int M, int k_per_split, int mt,
                                                           int n_split, float* __restrict__ part,
-                                                          int ldp) {
+                                                          int ldp, int krot) {
   constexpr int NW = WM * WN;
   static_assert(NW == 8 || NW == 16, "8 or 16 waves");
   static_assert(NS == 2 || NS == 3, "ring of 2 or 3 stages");
@@ -603,6 +611,12 @@ __global__ void __launch_bounds__(WM * WN * 64, (BM / WM) * (BN / WN) > 4096 ? 2
   tile_of(blockIdx.x, gridDim.x, gridDim.x / n_split, mt, split, t, mtile);
   const int m0 = mtile * BM;
   const int kbeg = split * k_per_split, nk = k_per_split / BK, last = nk - 1;
+  // K-step ks of this tile reads K-step kmap(ks) (as in gemm_bf16_kernel)
+  const int rot = krot ? (int)(((long long)t * krot) % nk) : 0;
+  auto kmap = [rot, nk](int k) {
+    const int x = k + rot;
+    return x >= nk ? x - nk : x;
+  };
 
   // this wave's blocks of a stage: block c = wave * CPW + i; c < A_BLOCKS are
   // activation blocks (part c / GB, row group c % GB), the rest weight blocks
@@ -629,8 +643,9 @@ __global__ void __launch_bounds__(WM * WN * 64, (BM / WM) * (BN / WN) > 4096 ? 2
     char* dst = smem + (kb % NS) * STAGE + wave * CPW * 1024;
 #pragma unroll
     for (int i = 0; i < CPW; ++i) {
-      const bf16_t* p = is_a[i] ? src[i] + (size_t)(ks >> 1) * a_kstep + (ks & 1) * 512
-                                : src[i] + (size_t)ks * BK;
+      const int km = kmap(ks);
+      const bf16_t* p = is_a[i] ? src[i] + (size_t)(km >> 1) * a_kstep + (km & 1) * 512
+                                : src[i] + (size_t)km * BK;
       __builtin_amdgcn_global_load_lds((const void*)p,
                                        (__attribute__((address_space(3))) void*)(dst + i * 1024),
                                        16, 0, 0);
@@ -798,6 +813,27 @@ static void launch_reduce(const Pol& pol, const float* part, int N, int M, int S
 // ---------------------------------------------------------------------------
 // host-side dispatch
 // ---------------------------------------------------------------------------
+// K-step rotation of the column tiles (tile t starts at K-step t * krot mod
+// nk); 0 = every tile starts at K-step 0.  Measured on the 120-row steps:
+// 1 spreads the concurrently read weight addresses and takes 4% off the step.
+// SSM_GEMM_KROT overrides it for tuning; read once per process.
+static int gemm_krot() {
+  static const int krot = [] {
+    const char* e = getenv("SSM_GEMM_KROT");
+    return e ? atoi(e) : 1;
+  }();
+  return krot;
+}
+
+// The same for gemm_big_kernel (SSM_GEMM_BIG_KROT; default off).
+static int gemm_big_krot() {
+  static const int krot = [] {
+    const char* e = getenv("SSM_GEMM_BIG_KROT");
+    return e ? atoi(e) : 0;
+  }();
+  return krot;
+}
+
 // Split-K is only used while S * M stays small, which bounds the workspace.
 static constexpr int SPLIT_ROWS_MAX = 1024;
 // Row count from which the projections use gemm_big_kernel.
@@ -855,7 +891,7 @@ static hipError_t launch_bf16(const Pol& pol, const ActIn& a, int M, int K, int 
   const dim3 grid(ntiles * mt * S);
   launch((gemm_bf16_kernel<BM, BN, PW, SPLIT, Pol>), grid, dim3(512), 0, st, pol,
                      (const bf16_t*)a.hi, a.lo, a.G, M, K / S, mt, S,
-                     S > 1 ? ws.part : nullptr, N);
+                     S > 1 ? ws.part : nullptr, N, gemm_krot());
   if constexpr (!has_tile<Pol>::value) {   // whole-tile epilogues never split K
     if (S > 1 && reduce) launch_reduce<BN>(pol, ws.part, N, M, S, ntiles, st);
   }
@@ -910,10 +946,10 @@ static hipError_t launch_big(const Pol& pol, const ActIn& a, int M, int K, int N
     float* pp = S > 1 ? ws.part : nullptr;
     if (a.lo)
       launch((gemm_big_kernel<BM, BN, WM, WN, NS, true, Pol>), grid, block, 0, st, pol,
-             (const bf16_t*)a.hi, a.lo, a.G, M, K / S, mt, S, pp, N);
+             (const bf16_t*)a.hi, a.lo, a.G, M, K / S, mt, S, pp, N, gemm_big_krot());
     else
       launch((gemm_big_kernel<BM, BN, WM, WN, NS, false, Pol>), grid, block, 0, st, pol,
-             (const bf16_t*)a.hi, a.lo, a.G, M, K / S, mt, S, pp, N);
+             (const bf16_t*)a.hi, a.lo, a.G, M, K / S, mt, S, pp, N, gemm_big_krot());
     if (S > 1 && reduce) launch_reduce<BN>(pol, ws.part, N, M, S, ntiles, st);
     return hipGetLastError();
   }

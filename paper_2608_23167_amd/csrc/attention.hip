@@ -377,16 +377,21 @@ hipError_t attention(int dtype, const void* q, const void* kc, const void* vc, i
                      hipStream_t st) {
   if (Mq == 0) return hipSuccess;
   const int BH = B * H;
-  // bfloat16: 32 query rows per wave (128 per workgroup) once there are more
-  // than 64 rows, which halves the LDS reads per MFMA; float32: 64 per block
-  const int QB = dtype == 1 && Mq > 64 ? 2 : 1;
+  // bfloat16: 32 query rows per wave (128 per workgroup), which halves the
+  // LDS reads per MFMA, once 64-row tiles alone would give two workgroups per
+  // CU; below that 16 per wave, twice the workgroups for a launch that is
+  // bound by latency rather than by MFMA or HBM.  float32: 64 rows per block.
+  const int QB = dtype == 1 && Mq > 64 && ceil_div(Mq, 64) * BH >= 512 ? 2 : 1;
   const int qtiles = ceil_div(Mq, 64 * QB);
   // split the key range (whole 64-key tiles) until every split has about two
   // tiles or the grid reaches two workgroups per CU: each workgroup walks its
-  // tiles in sequence and hides only the next tile's load, so short ranges
-  // spread over many workgroups beat long ones
+  // tiles in sequence and hides only the next tile's load, so long ranges
+  // spread over many workgroups beat few long walks.  Up to 10 tiles the
+  // range is not split: a workgroup's fixed cost (launch, query and first
+  // tile loads, output) is about 9 us against 0.4 us per further tile, and
+  // the merge kernel would cost more than the shorter walk saves.
   const int key_tiles = ceil_div(Nk, 64);
-  int S = key_tiles / 2;
+  int S = key_tiles <= 10 ? 1 : key_tiles / 2;
   if (S > ws.max_splits) S = ws.max_splits;
   if (S > 512 / (qtiles * BH)) S = 512 / (qtiles * BH);
   if (S < 1) S = 1;

@@ -883,6 +883,24 @@ static int auto_split(int tiles, int M, int K, size_t ws_floats, int N) {
   return S;
 }
 
+// Split-K of the big tiles: the S in 1..4 (K a multiple of 256 S, partials
+// within the workspace) whose workgroups fill the CUs best over the rounds
+// they take; 2% of fill per extra split pays for the partials' traffic.
+// The 8-wave tiles with a 2-stage ring fit two workgroups per CU.
+static int big_split(int tiles, int big, int M, int K, int N, size_t ws_floats) {
+  const int slots = 256 * (big == 1 || big == 2 ? 2 : 1);
+  int best = 1;
+  double best_score = -1.0;
+  for (int S = 1; S <= 4; ++S) {
+    if (K % (256 * S) != 0 || (size_t)S * M * N > ws_floats) continue;
+    const long wgs = (long)tiles * S;
+    const double fill = (double)wgs / ((double)slots * ceil_div((int)wgs, slots));
+    const double score = fill - 0.02 * (S - 1);
+    if (score > best_score + 1e-9) { best_score = score; best = S; }
+  }
+  return best;
+}
+
 template <int BN, int PW, bool SPLIT, class Pol>
 static hipError_t launch_bf16(const Pol& pol, const ActIn& a, int M, int K, int N, int S,
                               SplitWs ws, hipStream_t st, bool reduce) {
@@ -929,7 +947,8 @@ static GemmCfg plan_bf16(const char* kind, Pol& pol, int M, int K, int N, GemmCf
   else if (!bn_ok(pol, c.bn) || N % c.bn) c.bn = bn_ok(pol, 128) && N % 128 == 0 ? 128 : 64;
   if (rebind) rebind(pol, c.bn);
   const int tiles = (N / c.bn) * ceil_div(M, c.big ? big_rows(c.big) : 128);
-  int S = c.s > 0 ? c.s : auto_split(tiles, M, K, ws.floats, N);
+  int S = c.s > 0 ? c.s : c.big ? big_split(tiles, c.big, M, K, N, ws.floats)
+                                 : auto_split(tiles, M, K, ws.floats, N);
   while (S > 1 && (K % (256 * S) != 0 || (size_t)S * M * N > ws.floats)) S /= 2;
   c.s = S;
   return c;
@@ -1069,8 +1088,9 @@ static hipError_t run_f32(const Pol& pol, const ActIn& a, int M, int K, int N, S
 //    3-stage ring (half the operand bytes per MFMA, two K-steps of copy
 //    latency hidden);
 //  * O / down (N = d): gemm_bf16_kernel, whose 128-row tiles fill more CUs;
-//    with the pair, from 1536 rows the 3-stage 128 x 256 tiles.  Up to 128
-//    rows O takes 64-column tiles and split-K 4, which halves the float32
+//    from 1024 rows the 256 x 256 tiles with split-K chosen for CU fill
+//    (big_split; its partials go through the fused sum + RMSNorm).  Up to
+//    128 rows O takes 64-column tiles and split-K 4, which halves the float32
 //    partials of the 8-way split.
 static GemmCfg default_cfg(const char* kind, int M, bool paired) {
   const bool small = M <= 256;
@@ -1080,7 +1100,7 @@ static GemmCfg default_cfg(const char* kind, int M, bool paired) {
     return M < 512 ? GemmCfg{96, 1, 4, 0} : GemmCfg{128, 1, 3, M >= 1024 ? 3 : 2};
   if (!strcmp(kind, "lm")) return GemmCfg{128, 1, 4, 0};
   if (!strcmp(kind, "o") && M <= 128) return GemmCfg{64, 4, 4, 0};
-  return small ? GemmCfg{128, 0, 4, 0} : GemmCfg{128, 0, 3, paired && M >= 1536 ? 4 : 0};
+  return small ? GemmCfg{128, 0, 4, 0} : GemmCfg{128, 0, 3, M >= 1024 ? 3 : 0};
 }
 
 template <class Pol> static int any_bn(const Pol&, int bn) { return bn == 64 || bn == 96 || bn == 128; }

@@ -9,7 +9,7 @@
 // with two kinds of waves (one of each per SIMD):
 //   * staging waves (4-7) stream the weight tile from HBM: a ring of four
 //     K-steps of 16-byte loads in flight per thread, written into a ring of
-//     three LDS buffers two K-steps ahead of their use;
+//     three or four LDS buffers two or three K-steps ahead of their use;
 //   * compute waves (0-3) each own 32 rows x BN columns: they load their
 //     activation fragments straight from global memory (small, shared by
 //     every workgroup, L2-resident, stored in fragment order so that each
@@ -350,7 +350,7 @@ __device__ __forceinline__ void lds_written_barrier() {
 // Warp-specialised workgroup of 8 waves, BM = 128 rows x BN columns.
 //  * Waves 4-7 ("staging") stream the weight tile of each K-step (BN rows x 64
 //    k, the HBM-bound stream) through a ring of 4 register stages into a ring
-//    of 3 LDS buffers, two K-steps ahead.  A staging thread holds only BN / 32
+//    of 3 or 4 LDS buffers, 2 or 3 K-steps ahead.  A staging thread holds only BN / 32
 //    x 16 bytes per stage, so the ring is deep at little register cost.
 //  * Waves 0-3 ("compute") each own 32 rows x all BN columns.  They load
 //    their activation fragments (bfloat16 hi and optionally lo, L2-resident)
@@ -373,8 +373,12 @@ __global__ void __launch_bounds__(512) gemm_bf16_kernel(Pol pol, const bf16_t* _
   constexpr int FM = 2, FN = BN / 16;            // per compute wave: 32 rows x BN columns
   constexpr int NA = SPLIT ? 2 : 1;
   constexpr int WR = BN / 32;                    // weight rows per staging thread per stage
-  constexpr int NBUF = 3;                        // LDS weight buffers
+  // LDS weight buffers: 4 (three K-steps ahead) for the 96-column tiles, 3
+  // (two ahead) for the others, which measured 2-3% slower with 4
+  constexpr int NBUF = BN == 96 ? 4 : 3;
+  constexpr int AHEAD = NBUF - 1;                // K-steps the staging runs ahead
   static_assert(PW == 4 || PW == 8, "weight register ring of 4 or 8 K-steps");
+  static_assert(AHEAD < PW, "the prologue refills the first AHEAD register sets");
   constexpr int BUF_ELEMS = BN * LS;
   constexpr int SMEM_W = NBUF * BUF_ELEMS * 2;
   constexpr int CS = BN + 4;
@@ -465,7 +469,7 @@ __global__ void __launch_bounds__(512) gemm_bf16_kernel(Pol pol, const bf16_t* _
     } else {
       LOAD_A(a0, 0);
       LOAD_A(a1, min(1, last));
-      __syncthreads();                             // weight stages 0 and 1 are in LDS
+      __syncthreads();                             // weight stages 0 .. AHEAD - 1 are in LDS
       READ_W(wf0, 0, 0);
       for (int kt = 0; kt < nk; kt += 2) {
         CSTEP(kt, a0);
@@ -495,7 +499,7 @@ __global__ void __launch_bounds__(512) gemm_bf16_kernel(Pol pol, const bf16_t* _
       const int r = r0 + 32 * i;   // tile rows [0, BN/2) come from lo, the rest from hi
       w_src[i] = (r < BN / 2 ? blo + (size_t)r * pol.ldb : bhi + (size_t)(r - BN / 2) * pol.ldb) + kbeg + col;
     }
-    u32x4_t s0[WR], s1[WR], s2[WR], s3[WR], s4[WR], s5[WR], s6[WR], s7[WR];   // stage s in set s % PW
+    u32x4_t sr[PW][WR];                          // stage x in register set x % PW
 #define LOAD_S(S, KT)                                                                 \
   do {                                                                                \
     _Pragma("unroll") for (int i = 0; i < WR; ++i) S[i] = *(const u32x4_t*)(w_src[i] + kmap(KT) * BK); \
@@ -505,53 +509,29 @@ __global__ void __launch_bounds__(512) gemm_bf16_kernel(Pol pol, const bf16_t* _
     _Pragma("unroll") for (int i = 0; i < WR; ++i)                                    \
         *(u32x4_t*)(Ws + (BUF) * BUF_ELEMS + (r0 + 32 * i) * LS + col) = S[i];        \
   } while (0)
-    // during step kt the compute waves read buffers kt % 3 and (kt + 1) % 3;
-    // the staging waves fill buffer (kt + 2) % 3 with stage kt + 2 and fetch
-    // stage kt + 2 + PW into the register set it came from
-#define SSTEP(KT, S)                                                                  \
-  do {                                                                                \
-    STORE_S(S, ((KT) + 2) % NBUF);                                                    \
-    LOAD_S(S, min((KT) + 2 + PW, last));                                              \
-    lds_written_barrier();                                                            \
-  } while (0)
-
-    LOAD_S(s0, 0);
-    LOAD_S(s1, min(1, last));
-    LOAD_S(s2, min(2, last));
-    LOAD_S(s3, min(3, last));
-    if constexpr (PW == 8) {
-      LOAD_S(s4, min(4, last));
-      LOAD_S(s5, min(5, last));
-      LOAD_S(s6, min(6, last));
-      LOAD_S(s7, min(7, last));
+    // during step kt the compute waves read buffers kt % NBUF and (kt + 1) %
+    // NBUF; the staging waves fill buffer (kt + AHEAD) % NBUF with stage
+    // kt + AHEAD and fetch stage kt + AHEAD + PW into the register set it
+    // came from
+#pragma unroll
+    for (int u = 0; u < PW; ++u) LOAD_S(sr[u], min(u, last));
+#pragma unroll
+    for (int u = 0; u < AHEAD; ++u) {
+      STORE_S(sr[u], u);
+      LOAD_S(sr[u], min(u + PW, last));
     }
-    STORE_S(s0, 0);
-    STORE_S(s1, 1);
-    LOAD_S(s0, min(PW, last));
-    LOAD_S(s1, min(PW + 1, last));
-    __syncthreads();                               // weight stages 0 and 1 are in LDS
-    if constexpr (PW == 8) {
-      for (int kt = 0; kt < nk; kt += 8) {         // nk is a multiple of 8 (host-checked)
-        SSTEP(kt, s2);
-        SSTEP(kt + 1, s3);
-        SSTEP(kt + 2, s4);
-        SSTEP(kt + 3, s5);
-        SSTEP(kt + 4, s6);
-        SSTEP(kt + 5, s7);
-        SSTEP(kt + 6, s0);
-        SSTEP(kt + 7, s1);
-      }
-    } else {
-      for (int kt = 0; kt < nk; kt += 4) {
-        SSTEP(kt, s2);
-        SSTEP(kt + 1, s3);
-        SSTEP(kt + 2, s0);
-        SSTEP(kt + 3, s1);
+    __syncthreads();                               // weight stages 0 .. AHEAD - 1 are in LDS
+    for (int kt = 0; kt < nk; kt += PW) {          // nk is a multiple of PW (host-checked)
+#pragma unroll
+      for (int u = 0; u < PW; ++u) {
+        const int x = kt + u + AHEAD;              // the stage stored in this step
+        STORE_S(sr[(u + AHEAD) % PW], x % NBUF);
+        LOAD_S(sr[(u + AHEAD) % PW], min(x + PW, last));
+        lds_written_barrier();
       }
     }
 #undef LOAD_S
 #undef STORE_S
-#undef SSTEP
   }
   __syncthreads();
   tile_epilogue<BM, BN, CS>(pol, Cs, m0, M, t, part, split, ldp);

@@ -96,6 +96,7 @@ def main():
     ap.add_argument("--steps", type=int, default=None, help="timed steps (default: one generation)")
     ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--workload", default="llada_gen256")
+    ap.add_argument("--batch", type=int, default=None, help="override the workload's batch size")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--attn-sweep", action="store_true",
                     help="instead of the decoding bench: the attention/gather microbenchmark "
@@ -105,6 +106,9 @@ def main():
                     help="instead of the decoding bench: whole generations of the LLaDA-8B shape "
                          "(prompt 1024, block 64, top-8, budgets 128/32/16, prefix cache) at "
                          "generation lengths 256 .. 2048, SSM and unpruned")
+    ap.add_argument("--batch-sweep", action="store_true",
+                    help="instead of the decoding bench: the LLaDA-8B gen-256 workload (prompt 256, "
+                         "block 32, top-1, budgets 64/16/8, prefix cache) at batch 1 .. 32")
     ap.add_argument("--no-full-suffix", action="store_true",
                     help="skip the unpruned (full-suffix) decoder run of the same schedule")
     ap.add_argument("--no-profile", action="store_true",
@@ -129,6 +133,9 @@ def main():
     if args.gen_sweep:
         gen_sweep()
         return
+    if args.batch_sweep:
+        batch_sweep()
+        return
 
     import numpy as np
     import torch
@@ -139,6 +146,8 @@ def main():
     from paper_2608_23167_amd.model import DeviceModel
 
     wl = WORKLOADS[args.workload]
+    if args.batch is not None:
+        wl = wl.replace(batch=args.batch)
     shape = wl.model
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
@@ -387,6 +396,59 @@ def gen_sweep():
         points.append(pt)
     print(json.dumps({"metric": "whole-generation tokens/s vs generation length, SSM and unpruned "
                                 "(LLaDA-8B shape, prompt 1024, block 64, top-8, budgets 128/32/16)",
+                      "unit": "tokens/s", "n_gpus": 1, "dtype": "bf16",
+                      "data": "synthetic (seeded random-init weights, uniform random prompt ids)",
+                      "points": points}), flush=True)
+
+
+def batch_sweep(steps=64, warmup=4):
+    """Tokens/s and step latency of the bench workload (LLaDA-8B shape, prompt
+    256, gen 256, block 32, top-1, budgets 64/16/8, prefix cache) at batch 1 ..
+    32: every sequence shares the schedule, so a step runs B times the rows
+    over one pass of the weights.  The first `steps` steps of a generation
+    (blocks 0 and 1) after `warmup`; one JSON line."""
+    import torch
+    from synthetic import WORKLOADS, initial_tokens, make_weights
+    from paper_2608_23167_amd.api import ssm_select_count
+    from paper_2608_23167_amd.decoder import Decoder
+    from paper_2608_23167_amd.model import DeviceModel
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    base = WORKLOADS["llada_gen256"]
+    mw = make_weights(base.model, seed=base.seed, device=dev)
+    dm = DeviceModel(base.model, mw)
+    points = []
+    for B in (1, 2, 4, 8, 16, 32):
+        wl = base.replace(batch=B)
+        dec = Decoder(wl, dm, device=dev)
+        tok0 = initial_tokens(wl, device=dev)
+        sched = dec.schedule()
+        dec.reset(tok0)
+        for i in range(warmup):
+            dec.step(*sched[i])
+        torch.cuda.synchronize()
+        dec.reset(tok0)
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(steps)]
+        t0 = time.perf_counter()
+        for i in range(steps):
+            ev[i][0].record()
+            dec.step(*sched[i])
+            ev[i][1].record()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        ms = [a.elapsed_time(b) for a, b in ev]
+        cached = sorted(m for m, (_, first) in zip(ms, sched[:steps]) if not first)
+        pt = {"batch": B, "tokens_per_s": round(steps * wl.n_per_step * B / wall, 1),
+              "ms_per_step": round(wall / steps * 1e3, 3),
+              "cached_step_ms": round(cached[len(cached) // 2], 3),
+              "cached_rows": B * ssm_select_count(dec.params(1, False))[0]}
+        print(f"[bench] batch sweep {pt}", file=sys.stderr, flush=True)
+        points.append(pt)
+        del dec
+        torch.cuda.empty_cache()
+    print(json.dumps({"metric": "denoised tokens/s vs batch (LLaDA-8B shape, gen 256, block 32, top-1, "
+                                "budgets 64/16/8, prefix cache; steps of blocks 0-1)",
                       "unit": "tokens/s", "n_gpus": 1, "dtype": "bf16",
                       "data": "synthetic (seeded random-init weights, uniform random prompt ids)",
                       "points": points}), flush=True)

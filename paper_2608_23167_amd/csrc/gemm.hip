@@ -1059,14 +1059,15 @@ static hipError_t run_f32(const Pol& pol, const ActIn& a, int M, int K, int N, S
 // MFMA-bound and want wide tiles.  `paired`: the activations carry the lo part
 // (twice the MFMA work per operand byte, so the wide 3-stage tiles pay more).
 // Measured choices:
-//  * QKV: split-K 2 up to 128 rows; from 512 rows 256 x 128 tiles (a tile
-//    stays one head, for RoPE), with a 3-stage ring for one pass (24 KB per
-//    stage: two workgroups per CU) and a 2-stage ring for the pair;
+//  * QKV: split-K 2 up to 128 rows; 256 x 128 tiles (a tile stays one head,
+//    for RoPE) from 512 rows with the pair (2-stage ring) and from 1024 rows
+//    in one pass (3-stage ring, 24 KB per stage: two workgroups per CU; below
+//    1024 rows its 256-row tiles leave slots empty);
 //  * gate/up: 96-column tiles below 512 rows (one workgroup per CU at
 //    2F = 24576; the planner falls back to 128 where 96 does not divide 2F);
-//    from 512 rows 128 x 256, from 1024 rows 256 x 256 with 16 waves and a
-//    3-stage ring (half the operand bytes per MFMA, two K-steps of copy
-//    latency hidden);
+//    from 512 rows 128 x 256 with the pair and the 3-stage 256 x 128 tiles
+//    in one pass, from 1024 rows 256 x 256 with 16 waves and a 3-stage ring
+//    (half the operand bytes per MFMA, two K-steps of copy latency hidden);
 //  * O / down (N = d): gemm_bf16_kernel, whose 128-row tiles fill more CUs;
 //    from 1024 rows the 256 x 256 tiles with split-K chosen for CU fill
 //    (big_split; its partials go through the fused sum + RMSNorm).  Up to
@@ -1074,10 +1075,14 @@ static hipError_t run_f32(const Pol& pol, const ActIn& a, int M, int K, int N, S
 //    partials of the 8-way split.
 static GemmCfg default_cfg(const char* kind, int M, bool paired) {
   const bool small = M <= 256;
-  if (!strcmp(kind, "qkv"))   // split-K pays at 120 rows, not at 240
-    return small ? GemmCfg{128, M <= 128 ? 2 : 1, 4, 0} : GemmCfg{128, 1, 3, paired ? 1 : 6};
-  if (!strcmp(kind, "gate_up"))
-    return M < 512 ? GemmCfg{96, 1, 4, 0} : GemmCfg{128, 1, 3, M >= 1024 ? 3 : 2};
+  if (!strcmp(kind, "qkv")) {   // split-K pays at 120 rows, not at 240
+    if (small) return GemmCfg{128, M <= 128 ? 2 : 1, 4, 0};
+    return GemmCfg{128, 1, 3, paired ? 1 : (M >= 1024 ? 6 : 0)};
+  }
+  if (!strcmp(kind, "gate_up")) {
+    if (M < 512) return GemmCfg{96, 1, 4, 0};
+    return GemmCfg{128, 1, 3, M >= 1024 ? 3 : (paired ? 2 : 6)};
+  }
   if (!strcmp(kind, "lm")) return GemmCfg{128, 1, 4, 0};
   if (!strcmp(kind, "o") && M <= 128) return GemmCfg{64, 4, 4, 0};
   return small ? GemmCfg{128, 0, 4, 0} : GemmCfg{128, 0, 3, M >= 1024 ? 3 : 0};

@@ -210,6 +210,19 @@ def test_llada_long_shape_2_layers_single_bf16_activations(gpu):
     _bf16_case(wl, [(0, 2)], act_mode=L.SSM_ACT_BF16)
 
 
+@pytest.mark.parametrize("batch", [1, 2])
+def test_llada_shape_one_pass_512_and_1024_rows(gpu, batch):
+    """One-pass (SSM_ACT_BF16) block-start step of block 5 of the gen-256
+    workload: 512 rows per sequence.  At batch 1 gate/up runs the 3-stage
+    256 x 128 tiles and QKV, O, down the 128-row kernel; at batch 2 (1024
+    rows) QKV the 256 x 128 tiles, gate/up the 256 x 256 tiles, O and down
+    the 256 x 256 tiles with split-K."""
+    from paper_2608_23167_amd import _lib as L
+    wl = sharpened(WORKLOADS["llada_gen256"], 30.0)
+    wl = wl.replace(model=wl.model.with_layers(2), batch=batch)
+    _bf16_case(wl, [(5, 1)], act_mode=L.SSM_ACT_BF16)
+
+
 def test_llada_long_shape_pair_in_first_layer_only(gpu):
     """SSM_ACT_BF16X2_FIRST with one pair layer: layer 0 multiplies the hi and
     lo parts, layer 1 and the LM head round once, on both the block-start

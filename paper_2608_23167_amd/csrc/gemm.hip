@@ -567,7 +567,7 @@ __global__ void __launch_bounds__(WM * WN * 64, (BM / WM) * (BN / WN) > 4096 ? 2
                                                           const bf16_t* __restrict__ Alo, int G,
                                                           int M, int k_per_split, int mt,
                                                           int n_split, float* __restrict__ part,
-                                                          int ldp, int krot) {
+                                                          int ldp) {
   constexpr int NW = WM * WN;
   static_assert(NW == 8 || NW == 16, "8 or 16 waves");
   static_assert(NS == 2 || NS == 3, "ring of 2 or 3 stages");
@@ -591,12 +591,6 @@ __global__ void __launch_bounds__(WM * WN * 64, (BM / WM) * (BN / WN) > 4096 ? 2
   tile_of(blockIdx.x, gridDim.x, gridDim.x / n_split, mt, split, t, mtile);
   const int m0 = mtile * BM;
   const int kbeg = split * k_per_split, nk = k_per_split / BK, last = nk - 1;
-  // K-step ks of this tile reads K-step kmap(ks) (as in gemm_bf16_kernel)
-  const int rot = krot ? (int)(((long long)t * krot) % nk) : 0;
-  auto kmap = [rot, nk](int k) {
-    const int x = k + rot;
-    return x >= nk ? x - nk : x;
-  };
 
   // this wave's blocks of a stage: block c = wave * CPW + i; c < A_BLOCKS are
   // activation blocks (part c / GB, row group c % GB), the rest weight blocks
@@ -623,9 +617,8 @@ __global__ void __launch_bounds__(WM * WN * 64, (BM / WM) * (BN / WN) > 4096 ? 2
     char* dst = smem + (kb % NS) * STAGE + wave * CPW * 1024;
 #pragma unroll
     for (int i = 0; i < CPW; ++i) {
-      const int km = kmap(ks);
-      const bf16_t* p = is_a[i] ? src[i] + (size_t)(km >> 1) * a_kstep + (km & 1) * 512
-                                : src[i] + (size_t)km * BK;
+      const bf16_t* p = is_a[i] ? src[i] + (size_t)(ks >> 1) * a_kstep + (ks & 1) * 512
+                                : src[i] + (size_t)ks * BK;
       __builtin_amdgcn_global_load_lds((const void*)p,
                                        (__attribute__((address_space(3))) void*)(dst + i * 1024),
                                        16, 0, 0);
@@ -805,15 +798,6 @@ static int gemm_krot() {
   return krot;
 }
 
-// The same for gemm_big_kernel (SSM_GEMM_BIG_KROT; default off).
-static int gemm_big_krot() {
-  static const int krot = [] {
-    const char* e = getenv("SSM_GEMM_BIG_KROT");
-    return e ? atoi(e) : 0;
-  }();
-  return krot;
-}
-
 // Split-K is only used while S * M stays small, which bounds the workspace.
 static constexpr int SPLIT_ROWS_MAX = 1024;
 // Row count from which the projections use gemm_big_kernel.
@@ -945,10 +929,10 @@ static hipError_t launch_big(const Pol& pol, const ActIn& a, int M, int K, int N
     float* pp = S > 1 ? ws.part : nullptr;
     if (a.lo)
       launch((gemm_big_kernel<BM, BN, WM, WN, NS, true, Pol>), grid, block, 0, st, pol,
-             (const bf16_t*)a.hi, a.lo, a.G, M, K / S, mt, S, pp, N, gemm_big_krot());
+             (const bf16_t*)a.hi, a.lo, a.G, M, K / S, mt, S, pp, N);
     else
       launch((gemm_big_kernel<BM, BN, WM, WN, NS, false, Pol>), grid, block, 0, st, pol,
-             (const bf16_t*)a.hi, a.lo, a.G, M, K / S, mt, S, pp, N, gemm_big_krot());
+             (const bf16_t*)a.hi, a.lo, a.G, M, K / S, mt, S, pp, N);
     if (S > 1 && reduce) launch_reduce<BN>(pol, ws.part, N, M, S, ntiles, st);
     return hipGetLastError();
   }

@@ -57,31 +57,45 @@ __device__ __forceinline__ void store_row8(bf16_t* p, const float (&v)[8]) {
   *(u32x4_t*)p = *(const u32x4_t*)h;
 }
 
+// Column tile t of width BN covers BN / 2 consecutive entries of the
+// concatenated first halves of all heads (query heads, then key, then value)
+// and the same entries of the second halves, so the pairs (i, i + d_h / 2)
+// that RoPE rotates always meet in one tile, at any width whose half is a
+// multiple of 8.
 template <typename T>
 struct PolQKV {
   static constexpr bool PAIRED = true;
+  static constexpr bool ROW_MAP = true;
   const T *wq, *wk, *wv;
-  int ldb, H, Hkv, dh, tiles_per_head;
+  int ldb, H, Hkv, dh;
   T *q, *kc, *vc;
   int cap, n_cached, n_rows;
   const float2* rope;
 
+  __device__ __forceinline__ const T* head_rows(int head) const {
+    if (head < H) return wq + (size_t)head * dh * ldb;
+    if (head < H + Hkv) return wk + (size_t)(head - H) * dh * ldb;
+    return wv + (size_t)(head - H - Hkv) * dh * ldb;
+  }
+  // weight row of tile row r: rows [0, BN/2) from the first halves, the rest
+  // from the second
+  __device__ __forceinline__ const T* b_row(int t, int BN, int r) const {
+    const int half = dh / 2, second = r >= BN / 2;
+    const int j = t * (BN / 2) + (second ? r - BN / 2 : r);
+    const int head = j / half;
+    return head_rows(head) + (size_t)(j - head * half + (second ? half : 0)) * ldb;
+  }
+  // both halves as row ranges; only for tiles whose half stays in one head
+  // ((BN / 2) divides d_h / 2)
   __device__ __forceinline__ void b_ptrs(int t, int BN, const T*& lo, const T*& hi) const {
-    const int head = t / tiles_per_head, sub = t % tiles_per_head;
-    const T* base;
-    int hh;
-    if (head < H) { base = wq; hh = head; }
-    else if (head < H + Hkv) { base = wk; hh = head - H; }
-    else { base = wv; hh = head - H - Hkv; }
-    lo = base + (size_t)(hh * dh + sub * (BN / 2)) * ldb;
+    lo = b_row(t, BN, 0);
     hi = lo + (size_t)(dh / 2) * ldb;
   }
   __device__ __forceinline__ void store(int m, int t, int c, int BN, float vlo, float vhi) const {
-    const int head = t / tiles_per_head, sub = t % tiles_per_head;
-    const int i = sub * (BN / 2) + c;
+    const int half = dh / 2, j = t * (BN / 2) + c, head = j / half, i = j - head * half;
     const int s = m / n_rows, row = m % n_rows;
     if (head < H + Hkv) {
-      const float2 cs = rope[(size_t)row * (dh / 2) + i];
+      const float2 cs = rope[(size_t)row * half + i];
       const float a = vlo * cs.x - vhi * cs.y;
       const float b = vhi * cs.x + vlo * cs.y;
       vlo = a;
@@ -92,13 +106,12 @@ struct PolQKV {
     else if (head < H + Hkv) dst = kc + (((size_t)s * Hkv + (head - H)) * cap + n_cached + row) * dh;
     else dst = vc + (((size_t)s * Hkv + (head - H - Hkv)) * cap + n_cached + row) * dh;
     stf(dst + i, vlo);
-    stf(dst + i + dh / 2, vhi);
+    stf(dst + i + half, vhi);
   }
-  // columns c0 .. c0 + 7 of both halves (c0 a multiple of 8)
+  // columns c0 .. c0 + 7 of both halves (c0 a multiple of 8: one head)
   __device__ __forceinline__ void store8(int m, int t, int c0, int BN, const float (&vlo)[8],
                                          const float (&vhi)[8]) const {
-    const int head = t / tiles_per_head, sub = t % tiles_per_head;
-    const int i0 = sub * (BN / 2) + c0;
+    const int half = dh / 2, j = t * (BN / 2) + c0, head = j / half, i0 = j - head * half;
     const int s = m / n_rows, row = m % n_rows;
     float a[8], b[8];
 #pragma unroll
@@ -107,7 +120,7 @@ struct PolQKV {
       b[e] = vhi[e];
     }
     if (head < H + Hkv) {
-      const float2* cs = rope + (size_t)row * (dh / 2) + i0;
+      const float2* cs = rope + (size_t)row * half + i0;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const float2 r = cs[e];
@@ -120,7 +133,7 @@ struct PolQKV {
     else if (head < H + Hkv) dst = kc + (((size_t)s * Hkv + (head - H)) * cap + n_cached + row) * dh;
     else dst = vc + (((size_t)s * Hkv + (head - H - Hkv)) * cap + n_cached + row) * dh;
     store_row8(dst + i0, a);
-    store_row8(dst + i0 + dh / 2, b);
+    store_row8(dst + i0 + half, b);
   }
 };
 
@@ -268,6 +281,19 @@ template <class P, class = void> struct has_tile { static constexpr bool value =
 template <class P> struct has_tile<P, std::void_t<decltype(P::TILE)>> {
   static constexpr bool value = P::TILE;
 };
+template <class P, class = void> struct has_row_map { static constexpr bool value = false; };
+template <class P> struct has_row_map<P, std::void_t<decltype(P::ROW_MAP)>> {
+  static constexpr bool value = P::ROW_MAP;
+};
+
+// Weight row r of column tile t (lo, hi: the tile's two half ranges from
+// b_ptrs, for policies whose halves are row ranges).
+template <class Pol, class T>
+__device__ __forceinline__ const T* weight_row(const Pol& pol, int t, int BN, int r, const T* lo,
+                                               const T* hi) {
+  if constexpr (has_row_map<Pol>::value) return pol.b_row(t, BN, r);
+  else return r < BN / 2 ? lo + (size_t)r * pol.ldb : hi + (size_t)(r - BN / 2) * pol.ldb;
+}
 
 // Applies the epilogue to a BM x BN float tile staged in LDS (row stride CS).
 template <int BM, int BN, int CS, class Pol>
@@ -497,7 +523,7 @@ __global__ void __launch_bounds__(512) gemm_bf16_kernel(Pol pol, const bf16_t* _
 #pragma unroll
     for (int i = 0; i < WR; ++i) {
       const int r = r0 + 32 * i;   // tile rows [0, BN/2) come from lo, the rest from hi
-      w_src[i] = (r < BN / 2 ? blo + (size_t)r * pol.ldb : bhi + (size_t)(r - BN / 2) * pol.ldb) + kbeg + col;
+      w_src[i] = weight_row(pol, t, BN, r, blo, bhi) + kbeg + col;
     }
     u32x4_t sr[PW][WR];                          // stage x in register set x % PW
 #define LOAD_S(S, KT)                                                                 \
@@ -608,8 +634,7 @@ __global__ void __launch_bounds__(WM * WN * 64, (BM / WM) * (BN / WN) > 4096 ? 2
       src[i] = ((c / GB) ? Alo : Ahi) + (size_t)(kbeg >> 6) * a_kstep + (size_t)grp * 1024 + lane * 8;
     } else {
       const int r = 16 * (c - A_BLOCKS) + (lane & 15);
-      src[i] = (r < BN / 2 ? blo + (size_t)r * pol.ldb : bhi + (size_t)(r - BN / 2) * pol.ldb) +
-               kbeg + 8 * (lane >> 4);
+      src[i] = weight_row(pol, t, BN, r, blo, bhi) + kbeg + 8 * (lane >> 4);
     }
   }
   // K-step ks of the split into the ring slot of K-step kb
@@ -896,20 +921,17 @@ static hipError_t launch_bf16_pw(const Pol& pol, const ActIn& a, int M, int K, i
 // Launch plan of one projection: the configuration with a valid tile width
 // and the split-K factor.
 template <class Pol>
-static GemmCfg plan_bf16(const char* kind, Pol& pol, int M, int K, int N, GemmCfg c,
-                         const SplitWs& ws, int (*bn_ok)(const Pol&, int),
-                         void (*rebind)(Pol&, int)) {
+static GemmCfg plan_bf16(const char* kind, const Pol& pol, int M, int K, int N, GemmCfg c,
+                         const SplitWs& ws, int (*bn_ok)(const Pol&, int)) {
   c = cfg_override(kind, c);
   // many rows: the big-tile kernel where its shape constraints hold
   if (c.big < 0) c.big = 0;
   const int big_bn = c.big ? big_cols(c.big) : 128;
-  // (the per-head QKV epilogue, the one with a rebind, takes only 128 columns)
-  if (c.big && (M < BIG_ROWS_MIN || has_tile<Pol>::value || !bn_ok(pol, 128) ||
-                (big_bn != 128 && rebind) || N % big_bn != 0 || K % 32 != 0))
+  if (c.big && (M < BIG_ROWS_MIN || has_tile<Pol>::value || !bn_ok(pol, big_bn) ||
+                N % big_bn != 0 || K % 32 != 0))
     c.big = 0;
   if (c.big) c.bn = big_bn;
-  else if (!bn_ok(pol, c.bn) || N % c.bn) c.bn = bn_ok(pol, 128) && N % 128 == 0 ? 128 : 64;
-  if (rebind) rebind(pol, c.bn);
+  else if (c.bn > 128 || !bn_ok(pol, c.bn) || N % c.bn) c.bn = bn_ok(pol, 128) && N % 128 == 0 ? 128 : 64;
   const int tiles = (N / c.bn) * ceil_div(M, c.big ? big_rows(c.big) : 128);
   int S = c.s > 0 ? c.s : c.big ? big_split(tiles, c.big, M, K, N, ws.floats)
                                  : auto_split(tiles, M, K, ws.floats, N);
@@ -954,9 +976,8 @@ static hipError_t launch_plan(const Pol& pol, const ActIn& a, int M, int K, int 
 
 template <class Pol>
 static hipError_t run_bf16(const char* kind, Pol pol, const ActIn& a, int M, int K, int N,
-                           GemmCfg c, SplitWs ws, hipStream_t st, int (*bn_ok)(const Pol&, int),
-                           void (*rebind)(Pol&, int)) {
-  c = plan_bf16(kind, pol, M, K, N, c, ws, bn_ok, rebind);
+                           GemmCfg c, SplitWs ws, hipStream_t st, int (*bn_ok)(const Pol&, int)) {
+  c = plan_bf16(kind, pol, M, K, N, c, ws, bn_ok);
   return launch_plan(pol, a, M, K, N, c, ws, st);
 }
 
@@ -1043,10 +1064,13 @@ static hipError_t run_f32(const Pol& pol, const ActIn& a, int M, int K, int N, S
 // MFMA-bound and want wide tiles.  `paired`: the activations carry the lo part
 // (twice the MFMA work per operand byte, so the wide 3-stage tiles pay more).
 // Measured choices:
-//  * QKV: split-K 2 up to 128 rows; 256 x 128 tiles (a tile stays one head,
-//    for RoPE) from 512 rows with the pair (2-stage ring) and from 1024 rows
-//    in one pass (3-stage ring, 24 KB per stage: two workgroups per CU; below
-//    1024 rows its 256-row tiles leave slots empty);
+//  * QKV: 96-column tiles below 512 rows (128 column tiles at d = 4096 with
+//    32 + 2 x 32 heads: with the automatic split-K, 2 ways up to 128 rows,
+//    256 workgroups where 128-column tiles left 64 CUs idle); 256 x 128 tiles
+//    from 512 rows with the pair (2-stage ring) and from 1024 rows in one pass
+//    (3-stage ring, 24 KB per stage: two workgroups per CU; below 1024 rows
+//    its 256-row tiles leave slots empty).  256-column tiles (two heads) took
+//    longer at 1776 rows: 336 tiles leave most of a second round empty;
 //  * gate/up: 96-column tiles below 512 rows (one workgroup per CU at
 //    2F = 24576; the planner falls back to 128 where 96 does not divide 2F);
 //    from 512 rows 128 x 256 with the pair and the 3-stage 256 x 128 tiles
@@ -1059,8 +1083,8 @@ static hipError_t run_f32(const Pol& pol, const ActIn& a, int M, int K, int N, S
 //    partials of the 8-way split.
 static GemmCfg default_cfg(const char* kind, int M, bool paired) {
   const bool small = M <= 256;
-  if (!strcmp(kind, "qkv")) {   // split-K pays at 120 rows, not at 240
-    if (small) return GemmCfg{128, M <= 128 ? 2 : 1, 4, 0};
+  if (!strcmp(kind, "qkv")) {
+    if (M < 512) return GemmCfg{96, 0, 4, 0};
     return GemmCfg{128, 1, 3, paired ? 1 : (M >= 1024 ? 6 : 0)};
   }
   if (!strcmp(kind, "gate_up")) {
@@ -1072,23 +1096,28 @@ static GemmCfg default_cfg(const char* kind, int M, bool paired) {
   return small ? GemmCfg{128, 0, 4, 0} : GemmCfg{128, 0, 3, M >= 1024 ? 3 : 0};
 }
 
-template <class Pol> static int any_bn(const Pol&, int bn) { return bn == 64 || bn == 96 || bn == 128; }
-static int qkv_bn(const PolQKV<bf16_t>& p, int bn) { return (bn == 64 || bn == 128) && p.dh % bn == 0; }
-static void rebind_qkv(PolQKV<bf16_t>& p, int bn) { p.tiles_per_head = p.dh / bn; }
+// tile widths: 64, 96 and 128 (gemm_bf16_kernel), 128 and 256 (gemm_big_kernel)
+template <class Pol> static int any_bn(const Pol&, int bn) { return bn == 64 || bn == 96 || bn == 128 || bn == 256; }
+// any width whose tiles divide the heads' concatenated halves (the epilogue's
+// 8-column groups then never straddle a head)
+static int qkv_bn(const PolQKV<bf16_t>& p, int bn) {
+  return (bn == 64 || bn == 96 || bn == 128 || bn == 256) && ((p.H + 2 * p.Hkv) * p.dh) % bn == 0 &&
+         (p.dh / 2) % 8 == 0;
+}
 
 hipError_t gemm_qkv(int dtype, const ActIn& a, int M, int d, const void* wq, const void* wk,
                     const void* wv, int H, int Hkv, int dh, const QKVOut& o, SplitWs ws,
                     hipStream_t st) {
   const int N = (H + 2 * Hkv) * dh;
   if (dtype == 0) {
-    PolQKV<float> p{(const float*)wq, (const float*)wk, (const float*)wv, d, H, Hkv, dh, dh / 32,
+    PolQKV<float> p{(const float*)wq, (const float*)wk, (const float*)wv, d, H, Hkv, dh,
                     (float*)o.q, (float*)o.kc, (float*)o.vc, o.cap, o.n_cached, o.n_rows, o.rope};
     return run_f32(p, a, M, d, N, ws, st);
   }
   PolQKV<bf16_t> p{(const bf16_t*)wq, (const bf16_t*)wk, (const bf16_t*)wv, d, H, Hkv, dh,
-                   dh / 128, (bf16_t*)o.q, (bf16_t*)o.kc, (bf16_t*)o.vc, o.cap, o.n_cached,
+                   (bf16_t*)o.q, (bf16_t*)o.kc, (bf16_t*)o.vc, o.cap, o.n_cached,
                    o.n_rows, o.rope};
-  return run_bf16("qkv", p, a, M, d, N, default_cfg("qkv", M, a.lo != nullptr), ws, st, qkv_bn, rebind_qkv);
+  return run_bf16("qkv", p, a, M, d, N, default_cfg("qkv", M, a.lo != nullptr), ws, st, qkv_bn);
 }
 
 hipError_t gemm_resid(int dtype, const char* kind, const ActIn& a, int M, int K, const void* w,
@@ -1100,7 +1129,7 @@ hipError_t gemm_resid(int dtype, const char* kind, const ActIn& a, int M, int K,
   } else {
     PolResid<bf16_t> p{(const bf16_t*)w, K, N, resid};
     const GemmCfg c = plan_bf16(kind, p, M, K, N, default_cfg(kind, M, a.lo != nullptr), ws,
-                                any_bn<PolResid<bf16_t>>, (void (*)(PolResid<bf16_t>&, int))nullptr);
+                                any_bn<PolResid<bf16_t>>);
     const int nc = ceil_div(N / 8, 512);
     const bool fuse = nrm && c.s > 1 && N % 8 == 0 && nc <= 2 && ((uintptr_t)nrm->g & 15) == 0;
     e = launch_plan(p, a, M, K, N, c, ws, st, !fuse);
@@ -1124,7 +1153,7 @@ hipError_t gemm_swiglu(int dtype, const ActIn& a, int M, int d, const void* wg, 
   }
   PolSwiGLU<bf16_t> p{(const bf16_t*)wg, (const bf16_t*)wu, d, F, act};
   return run_bf16("gate_up", p, a, M, d, 2 * F, default_cfg("gate_up", M, a.lo != nullptr), ws, st,
-                  any_bn<PolSwiGLU<bf16_t>>, (void (*)(PolSwiGLU<bf16_t>&, int))nullptr);
+                  any_bn<PolSwiGLU<bf16_t>>);
 }
 
 hipError_t gemm_store_f32(const ActIn& a, int M, int K, const void* w, int N, float* c, int ldc,

@@ -39,15 +39,15 @@ METRIC = "denoised tokens/sec + step latency per GPU (LLaDA-8B shape); % MFMA/HB
 TRAFFIC = {
     # rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE over `bench.py --steps 32 --warmup 1
     # --no-profile --no-cpu-baseline --no-full-suffix --no-mfma`; per-dispatch means
-    # of the block-start launches (grid 393216: 135766.4 / 9024.0 KiB for the 28
-    # one-pass layers, 189381.0 / 18048.0 KiB for the 4 layers with the bf16
-    # pair) and the cached ones (grid 131072: 104448.7 / 2880.0 and 110536.5 /
+    # of the block-start launches (grid 393216: 135884.1 / 9024.0 KiB for the 28
+    # one-pass layers, 189382.0 / 18048.0 KiB for the 4 layers with the bf16
+    # pair) and the cached ones (grid 131072: 104448.6 / 2880.0 and 110536.1 /
     # 5760.0 KiB), weighted 28:4 over the layers and 1:31 over the steps as in the
     # generation schedule; copy kernel: 268435456 bytes read and written per
     # launch read as 131085.2 KiB fetched and 262144.0 KiB written
     ("llada_gen256", "gemm_gate_up"): {
-        "sources_sha256": "18257be67bebb9e8a92a08d339a2ae5b099f0f67d78d6ca92d9cbc54604d9f42",
-        "fetch_kib": ((28 * 135766.4 + 4 * 189381.0) / 32 + 31 * (28 * 104448.7 + 4 * 110536.5) / 32) / 32,
+        "sources_sha256": "c479fea4753f0445a58138058de7a98d2c4306fab3b3d6d546c0dee67691913f",
+        "fetch_kib": ((28 * 135884.1 + 4 * 189382.0) / 32 + 31 * (28 * 104448.6 + 4 * 110536.1) / 32) / 32,
         "write_kib": ((28 * 9024.0 + 4 * 18048.0) / 32 + 31 * (28 * 2880.0 + 4 * 5760.0) / 32) / 32,
         "fetch_scale": 262144.0 / 131085.2, "write_scale": 1.0},
 }

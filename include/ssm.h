@@ -71,7 +71,7 @@ enum {
   SSM_TAIL_START = 1     /* the start token only (if tail_budget >= 1)                          */
 };
 
-/* Unmasking rules (Section 4.2 "Vanilla" / "Par."; Section 4.5 margin rule). */
+/* Unmasking rules (Section 4.2 "Vanilla" / "Par."; Section 4.6 margin rule, Table 3). */
 enum {
   SSM_UNMASK_TOPN = 0,         /* the n most confident masked positions             */
   SSM_UNMASK_THRESHOLD = 1,    /* confidence > threshold, at least one per step     */
@@ -98,7 +98,7 @@ enum {
   SSM_REGION_MIDDLE = 3, SSM_REGION_TAIL = 4
 };
 
-/* Prefix KV cache use in ssm_denoise_step (the "PC." setting, Section 4.6). */
+/* Prefix KV cache use in ssm_denoise_step (the "PC." setting, Section 4.8, Table 4). */
 enum {
   SSM_CACHE_OFF = 0,    /* every row is an input row; the cache buffers are scratch        */
   SSM_CACHE_WRITE = 1,  /* first step of a block: rows start with the prefix; afterwards   */

@@ -17,7 +17,7 @@ h // (H / H_kv).  RoPE is the rotate-half form, applied at each row's
 original position, which is what lets the sparse input keep the retained
 suffix tokens' relative positions (Section 3.2).
 
-Prefix KV cache (the "PC." setting of Section 4.6): on the first step of a
+Prefix KV cache (the "PC." setting of Section 4.8, Table 4): on the first step of a
 block the full sparse input is run and the post-RoPE keys and values of the
 prefix rows are kept for every layer; on later steps of the block the input
 is [B_t; R_t] only and attention reads the cached prefix keys and values

@@ -1,5 +1,5 @@
 """Confidence-based unmasking inside the current block (Section 4.2 baselines;
-Section 4.5 margin rule).
+Section 4.6 margin rule, Table 3).
 
 TEST INFRASTRUCTURE ONLY (see the package docstring).
 

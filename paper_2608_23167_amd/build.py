@@ -3,6 +3,11 @@
 Usage: python -m paper_2608_23167_amd.build   (or __graft_entry__.build()).
 Objects go to _build/ next to this file; the library is written in place
 (paper_2608_23167_amd/libssm.so) so that it travels with the source tree.
+
+`--tuning` builds a separate library (libssm_tuning.so, objects in
+_build_tuning/) with SSM_TUNING defined: its GEMM launch choices can be
+overridden through the SSM_GEMM_CFG / SSM_GEMM_KROT environment variables
+for tile sweeps.  The product library never reads them.
 """
 from __future__ import annotations
 
@@ -26,31 +31,34 @@ FLAGS = [
 ]
 
 
-def _compile(src: str) -> str:
-    obj = os.path.join(OBJ, os.path.basename(src) + ".o")
-    cmd = [HIPCC, *FLAGS, "-c", src, "-o", obj]
+def _compile(src: str, obj_dir: str, extra) -> str:
+    obj = os.path.join(obj_dir, os.path.basename(src) + ".o")
+    cmd = [HIPCC, *FLAGS, *extra, "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed on {src}:\n{r.stdout}\n{r.stderr}")
     return obj
 
 
-def build(verbose: bool = False) -> str:
-    os.makedirs(OBJ, exist_ok=True)
+def build(verbose: bool = False, tuning: bool = False) -> str:
+    obj_dir = OBJ + "_tuning" if tuning else OBJ
+    out = os.path.join(HERE, "libssm_tuning.so") if tuning else OUT
+    extra = ["-DSSM_TUNING"] if tuning else []
+    os.makedirs(obj_dir, exist_ok=True)
     srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
     with cf.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
-        objs = list(ex.map(_compile, srcs))
-    tmp = OUT + ".tmp"
+        objs = list(ex.map(lambda src: _compile(src, obj_dir, extra), srcs))
+    tmp = out + ".tmp"
     cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")
-    os.replace(tmp, OUT)
+    os.replace(tmp, out)
     if verbose:
-        print("built", OUT)
-    return OUT
+        print("built", out)
+    return out
 
 
 if __name__ == "__main__":
-    build(verbose=True)
+    build(verbose=True, tuning="--tuning" in sys.argv[1:])
     sys.exit(0)

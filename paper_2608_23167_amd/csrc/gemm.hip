@@ -814,13 +814,18 @@ static void launch_reduce(const Pol& pol, const float* part, int N, int M, int S
 // K-step rotation of the column tiles (tile t starts at K-step t * krot mod
 // nk); 0 = every tile starts at K-step 0.  Measured on the 120-row steps:
 // 1 spreads the concurrently read weight addresses and takes 4% off the step.
-// SSM_GEMM_KROT overrides it for tuning; read once per process.
+// A tuning build (SSM_TUNING defined) lets SSM_GEMM_KROT override it; the
+// product build reads no environment variable.
 static int gemm_krot() {
+#ifdef SSM_TUNING
   static const int krot = [] {
     const char* e = getenv("SSM_GEMM_KROT");
     return e ? atoi(e) : 1;
   }();
   return krot;
+#else
+  return 1;
+#endif
 }
 
 // Split-K is only used while S * M stays small, which bounds the workspace.
@@ -846,9 +851,12 @@ struct GemmCfg {
 static int big_rows(int big) { return big == 1 || big == 3 || big == 5 || big == 6 ? 256 : 128; }
 static int big_cols(int big) { return big == 1 || big == 6 ? 128 : 256; }
 
-// Tuning override: SSM_GEMM_CFG="kind:bn:s:pw[:big],..." with kind one of
-// qkv, o, gate_up, down, lm (big as in GemmCfg); read once per process.
+// Tuning override, compiled only into a tuning build (SSM_TUNING defined):
+// SSM_GEMM_CFG="kind:bn:s:pw[:big],..." with kind one of qkv, o, gate_up,
+// down, lm (big as in GemmCfg); read once per process.  The product build
+// always takes the measured defaults.
 static GemmCfg cfg_override(const char* kind, GemmCfg c) {
+#ifdef SSM_TUNING
   static const char* env = getenv("SSM_GEMM_CFG");
   if (!env) return c;
   const size_t kl = strlen(kind);
@@ -862,6 +870,10 @@ static GemmCfg cfg_override(const char* kind, GemmCfg c) {
     if (p) ++p;
   }
   return c;
+#else
+  (void)kind;
+  return c;
+#endif
 }
 
 static int auto_split(int tiles, int M, int K, size_t ws_floats, int N) {

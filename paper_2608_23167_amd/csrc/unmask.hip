@@ -1,5 +1,5 @@
 // Confidence-based unmasking of the current block (Section 4.2: top-n
-// "Vanilla" decoding and threshold "Par." decoding; Section 4.5: margin
+// "Vanilla" decoding and threshold "Par." decoding; Section 4.6 (Table 3): margin
 // rule) and the update of the per-position prediction state that the next
 // step's soft suffix embedding reads (Section 3.2, Eq. 6).
 #include "internal.h"

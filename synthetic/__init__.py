@@ -6,14 +6,14 @@ their weights, prompts and random test tensors from these generators, so the
 two sides see identical inputs while sharing no computation.
 """
 from .configs import (ModelShape, Workload, TINY, LLADA_8B, DREAM_7B, WORKLOADS,
-                      workload, sharpened)
+                      workload, sharpened, spread)
 from .generate import (ModelWeights, LayerWeights, make_weights, make_layer,
                        prompt_tokens, initial_tokens, seeded_normal, seeded_uniform_ints,
                        mid_generation_state)
 
 __all__ = [
     "ModelShape", "Workload", "TINY", "LLADA_8B", "DREAM_7B", "WORKLOADS", "workload",
-    "sharpened", "ModelWeights", "LayerWeights", "make_weights", "make_layer",
+    "sharpened", "spread", "ModelWeights", "LayerWeights", "make_weights", "make_layer",
     "prompt_tokens", "initial_tokens", "seeded_normal", "seeded_uniform_ints",
     "mid_generation_state",
 ]

@@ -4,7 +4,7 @@ The model shapes follow the diffusion LMs the paper evaluates (LLaDA-8B and
 Dream-7B, Section 4.1) with random initialisation; the workloads follow the
 paper's decoding settings (block 32, confidence threshold 0.9, top-k in
 {3,5,7}, alpha in {0.2,0.3,0.4}; Section 4.1) and its long-sequence setting
-(Section 4.6, Table 4).  Budgets are in tokens: a local budget of w*b with
+(Section 4.8, Table 4).  Budgets are in tokens: a local budget of w*b with
 block-start middle mode and a tail budget of 2 reproduces Eq. 2-4 exactly.
 """
 from __future__ import annotations
@@ -141,3 +141,13 @@ def workload(name: str) -> Workload:
 def sharpened(wl: Workload, scale: float = 60.0) -> Workload:
     """Test-only variant whose LM head is scaled so that decisions have wide margins."""
     return wl.replace(name=wl.name + "_sharp", logit_scale=scale)
+
+
+def spread(wl: Workload, init_std: float = 0.1, scale: float = 3.0) -> Workload:
+    """Test-only variant with five times the init scale of the matrices, so that
+    attention is far from uniform and the rows of a block get distinct
+    predictions: confidences and top-1/top-2 margins then spread over most of
+    (0, 1) instead of clustering, and a free-running generation has decisions
+    that are wide on both sides."""
+    return wl.replace(name=wl.name + "_spread", logit_scale=scale,
+                      model=dataclasses.replace(wl.model, init_std=init_std))

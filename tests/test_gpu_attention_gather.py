@@ -64,20 +64,33 @@ def test_attention_matches_oracle(gpu, B, H, Hkv, n_q, n_keys, cap):
         assert _rel(got[s], ref) < TOL, (s, _rel(got[s], ref))
 
 
-@pytest.mark.parametrize("kept", [176, 4096])
-def test_attention_microbench_shape_sampled(gpu, kept):
+@pytest.mark.parametrize("kept", [0, 48, 176, 512, 4096])
+def test_attention_microbench_shape_every_row(gpu, kept):
     """Batch 8, 32 heads: prefix 4096 + block 64 + kept suffix rows attend to
-    all prefix, block and kept keys; sampled rows checked against the oracle."""
+    all prefix, block and kept keys, at points of the kept-suffix sweep (0:
+    block only, 48: the first point with middle and tail, 176: the workload's
+    budgets, 512, 4096: the whole suffix).  Every element of every row of two
+    of the eight sequences is checked against the float64 oracle, within the
+    bound that the bfloat16 rounding of the probabilities allows: each
+    p_j moves by at most 2^-9 p_j and so does their sum, so an output element
+    moves by at most 2^-8 sum_j p_j |v_j| (taken as 2^-7, plus 1e-6 for the
+    float32 softmax and accumulation); sum_j p_j |v_j| is the oracle's
+    attention over |v|."""
     B, H = 8, 32
     n_q = 64 + kept
     n_keys = 4096 + 64 + kept
     q, k, v = _inputs(B, H, H, n_q, n_keys, seed=kept)
     got = _run(q, k, v, n_keys)
-    rng = np.random.default_rng(kept)
-    for s in (0, 3, 7):
-        rows = sorted(set(rng.integers(0, n_q, size=6).tolist()) | {0, n_q - 1})
+    rows = list(range(n_q))
+    for s in (0, 7):
         ref = _oracle_rows(q, k, v, n_keys, s, rows)
-        assert _rel(got[s, rows], ref) < TOL, (s, rows, _rel(got[s, rows], ref))
+        bound = 2.0 ** -7 * _oracle_rows(q, k, v.abs(), n_keys, s, rows) + 1e-6
+        err = np.abs(got[s].astype(np.float64) - ref)
+        worst = float(np.max(err / bound))
+        print(f"[attention] kept {kept} sequence {s}: {n_q} rows x {n_keys} keys, rel "
+              f"{_rel(got[s], ref):.2e}, worst error / bound {worst:.3f}", flush=True)
+        assert worst <= 1.0, (s, worst)
+        assert _rel(got[s], ref) < TOL
 
 
 def test_gather_rows_bit_exact(gpu):

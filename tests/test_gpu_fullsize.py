@@ -4,6 +4,14 @@ launch configuration the benchmark uses (teacher-forced steps).
 
 Cached steps read a seeded synthetic prefix cache that both sides share, so
 a cached step is checked without an oracle block-start step first.
+
+The LM head is sharpened (logit scale 30, both sides) so that argmax
+decisions have probability margins above 1e-3: each test asserts that some
+are checked under the fixed error budget of tests/_parity.py.  At random
+initialisation the masked rows of a block are near-identical, so their
+confidences nearly tie and no unmasking comparison lies outside the budget;
+the unmasking stage is then checked for consistency instead: the rule applied
+to the GPU's own confidences must pick exactly the GPU's positions.
 """
 import time
 
@@ -13,12 +21,13 @@ import torch
 
 import oracle.generate as OG
 from synthetic import WORKLOADS, make_weights, mid_generation_state
-from tests._parity import (check_decisions, check_unmask, gpu_step, load_oracle_state,
-                           put_synthetic_cache, rel_err)
+from tests._parity import (check_decisions, check_unmask, check_unmask_consistency, gpu_step,
+                           load_oracle_state, put_synthetic_cache, rel_err)
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
 TOL = 2e-2
+LOGIT_SCALE = 30.0
 
 
 def _state(wl, block_idx, step, seed):
@@ -35,7 +44,7 @@ class _Model:
     def __init__(self, wl):
         from paper_2608_23167_amd.model import DeviceModel
         t0 = time.time()
-        self.mw = make_weights(wl.model, seed=wl.seed, device="cuda")
+        self.mw = make_weights(wl.model, seed=wl.seed, device="cuda", logit_scale=LOGIT_SCALE)
         self.dm = DeviceModel(wl.model, self.mw)
         self.w = OG.NumpyWeights(self.mw, dtype=np.float32)
         print(f"[fullsize] weights of {wl.model.name} ready in {time.time() - t0:.1f} s", flush=True)
@@ -62,13 +71,15 @@ def _run(wl, model, block_idx, first, seed, synthetic_cache):
     out = gpu_step(dec, block_idx, first)
     e_h = rel_err(out["hidden"], rec.hidden)
     e_l = max(rel_err(out["logits"][s], rec.stats[s].logits) for s in range(wl.batch))
-    pinned, total = check_decisions(out, rec, wl)
-    n_unmask = check_unmask(out, rec, wl)
+    dc = check_decisions(out, rec, wl, fp32=False)
+    uc = check_unmask(out, rec, wl, fp32=False)
+    n_cons = check_unmask_consistency(out, rec, wl)
     print(f"[fullsize] {wl.name} block {block_idx} {'start' if first else 'cached'} rows "
-          f"{out['info'].n_rows}: hidden rel {e_h:.2e} logits rel {e_l:.2e} pinned {pinned}/{total} "
-          f"unmask-checked {n_unmask} (oracle {t_or:.1f} s)", flush=True)
+          f"{out['info'].n_rows}: hidden rel {e_h:.2e} logits rel {e_l:.2e}; argmax {dc}; "
+          f"unmask {uc}; unmask consistency {n_cons} (oracle {t_or:.1f} s)", flush=True)
     assert np.array_equal(out["pos"], rec.rows.pos)
     assert e_h < TOL and e_l < TOL
+    assert dc.checked > 0
     del dec
     torch.cuda.empty_cache()
 
@@ -89,6 +100,26 @@ def test_llada_long_block_start(gpu, llada):
     _run(WORKLOADS["llada_long2048"], llada, 0, True, 4, False)
 
 
+def test_llada_long_late_block_cached(gpu, llada):
+    """Block 20 of the gen-2048 long workload: 1280 cached prefix keys plus the
+    block and its retained suffix."""
+    _run(WORKLOADS["llada_long2048"], llada, 20, False, 6, True)
+
+
+def test_llada_long_last_block_cached(gpu, llada):
+    """The last block of the gen-2048 long workload: prefix 3008 (cached), no
+    suffix left, 64 query rows over 3072 keys."""
+    _run(WORKLOADS["llada_long2048"], llada, 31, False, 7, True)
+
+
+def test_llada_long1024_block_start_1776_rows(gpu, llada):
+    """The block-start step on which the MFMA fraction is reported: block 8 of
+    the gen-1024 long workload, prefix 1536 + block 64 + 176 retained suffix
+    rows = 1776 rows through all 32 layers (big-tile GEMMs with ragged last
+    tiles, long-key attention)."""
+    _run(WORKLOADS["llada_long1024"], llada, 8, True, 8, False)
+
+
 def test_llada_gen256_cached_pair_in_every_layer(gpu, llada):
     """SSM_ACT_BF16X2: the bfloat16 pair at the projections of all 32 layers
     and the LM head (the default keeps it in the first layers only)."""
@@ -101,7 +132,20 @@ def test_llada_gen256_cached_pair_in_every_layer(gpu, llada):
     _run(wl, paired, 3, False, 2, True)
 
 
-def test_dream_uncached(gpu):
-    wl = WORKLOADS["dream_gen512"]
-    m = _Model(wl)
-    _run(wl, m, 0, True, 5, False)
+@pytest.fixture(scope="module")
+def dream():
+    m = _Model(WORKLOADS["dream_gen512"])
+    yield m
+    del m
+
+
+def test_dream_uncached(gpu, dream):
+    _run(WORKLOADS["dream_gen512"], dream, 0, True, 5, False)
+
+
+@pytest.mark.xfail(strict=True, reason="bfloat16 q/k/v/P give 2.39e-2 relative hidden error over "
+                   "28 layers of 1024 distinct random-token rows (bound 2e-2)")
+def test_dream_last_block_uncached(gpu, dream):
+    """The last block of the Dream-7B workload (no cache): prefix 992 + block
+    32 = 1024 rows, no suffix left."""
+    _run(WORKLOADS["dream_gen512"], dream, 15, True, 9, False)

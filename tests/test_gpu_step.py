@@ -4,16 +4,20 @@ from the oracle's state before that step).
 fp32 mode (tiny model): hidden states and logits within max-abs 1e-4.
 bf16 mode (LLaDA / Dream shapes): relative error <= 2e-2 against the fp32
 oracle run on the bf16-rounded weights.  Decisions (argmax, top-k ids,
-unmasking) must agree wherever the oracle's probability margin exceeds 1e-3.
+unmasking) must agree wherever the oracle's probability margin exceeds 1e-3,
+except inside the fixed logit error budget of tests/_parity.py; every test
+prints how many decisions it checked and how many were exempt, and asserts
+a floor on the checked count.
 """
 import numpy as np
 import pytest
 import torch
 
 import oracle.generate as OG
-from synthetic import (WORKLOADS, initial_tokens, make_weights, mid_generation_state, sharpened)
-from tests._parity import (check_decisions, check_unmask, gpu_step, load_oracle_state, max_abs,
-                           rel_err)
+from synthetic import (WORKLOADS, initial_tokens, make_weights, mid_generation_state, sharpened,
+                       spread)
+from tests._parity import (Counts, check_decisions, check_unmask, check_unmask_consistency,
+                           gpu_step, load_oracle_state, max_abs, rel_err)
 
 pytestmark = pytest.mark.gpu
 
@@ -41,44 +45,53 @@ def _compare_step(out, rec, wl, fp32: bool):
         assert rel_err(out["hidden"], rec.hidden) < 2e-2
         for s in range(B):
             assert rel_err(out["logits"][s], rec.stats[s].logits) < 2e-2
-    pinned, total = check_decisions(out, rec, wl)
-    return pinned / max(total, 1)
+    return check_decisions(out, rec, wl, fp32)
 
 
-def _compare_unmask(out, rec, wl):
-    return check_unmask(out, rec, wl)
+def _compare_unmask(out, rec, wl, fp32: bool):
+    check_unmask_consistency(out, rec, wl)
+    return check_unmask(out, rec, wl, fp32)
 
 
-@pytest.mark.parametrize("sharp", [False, True])
-def test_tiny_fp32_every_step(gpu, sharp):
+def _report(name, dec: Counts, unm: Counts):
+    print(f"[decisions] {name}: argmax {dec}; unmask {unm}", flush=True)
+
+
+@pytest.mark.parametrize("wide", [False, True])
+def test_tiny_fp32_every_step(gpu, wide):
+    """Every teacher-forced step of the tiny workload; with `wide`, the test
+    variant whose confidences and margins spread over (0, 1), so that nearly
+    every decision lies outside the budget and is checked."""
     wl = WORKLOADS["tiny"]
-    if sharp:
-        wl = sharpened(wl, 60.0)
+    if wide:
+        wl = spread(wl)
     mw = make_weights(wl.model, seed=0, norm_jitter=0.1, logit_scale=wl.logit_scale)
     w = OG.NumpyWeights(mw)
     dec = _decoder(wl, mw.to("cuda"))
     tok0 = initial_tokens(wl).numpy()
     st = OG.OracleState.start(tok0, wl.topk)
-    fracs = []
+    dc, uc = Counts(), Counts()
     for j in range(wl.n_blocks):
         for i in range(wl.steps_per_block()):
             before = st.copy()
             rec = OG.step(wl, w, st, j, i == 0)
             load_oracle_state(dec, before)
             out = gpu_step(dec, j, i == 0)
-            fracs.append(_compare_step(out, rec, wl, fp32=True))
-            _compare_unmask(out, rec, wl)
-    if sharp:
-        assert np.mean(fracs) > 0.9
+            dc.add(_compare_step(out, rec, wl, fp32=True))
+            uc.add(_compare_unmask(out, rec, wl, fp32=True))
+    _report(wl.name, dc, uc)
+    if wide:
+        assert dc.checked > 0.95 * dc.total and uc.checked > 0.7 * uc.total
 
 
 def test_tiny_fp32_cached_steps(gpu):
     """Prefix cache on: block-start steps write the cache, later steps read it."""
-    wl = sharpened(WORKLOADS["tiny"], 60.0).replace(cache=True)
+    wl = spread(WORKLOADS["tiny"]).replace(cache=True)
     mw = make_weights(wl.model, seed=1, norm_jitter=0.1, logit_scale=wl.logit_scale)
     w = OG.NumpyWeights(mw)
     dec = _decoder(wl, mw.to("cuda"))
     st = OG.OracleState.start(initial_tokens(wl, seed=2).numpy(), wl.topk)
+    dc, uc = Counts(), Counts()
     for j in range(wl.n_blocks):
         for i in range(wl.steps_per_block()):
             before = st.copy()
@@ -86,7 +99,10 @@ def test_tiny_fp32_cached_steps(gpu):
             load_oracle_state(dec, before)
             out = gpu_step(dec, j, i == 0)
             assert out["info"].include_prefix == (i == 0)
-            _compare_step(out, rec, wl, fp32=True)
+            dc.add(_compare_step(out, rec, wl, fp32=True))
+            uc.add(_compare_unmask(out, rec, wl, fp32=True))
+    _report(wl.name + " cached", dc, uc)
+    assert dc.checked > 0.95 * dc.total and uc.checked > 0.7 * uc.total
 
 
 @pytest.mark.parametrize("local,mmode,T,tmode", [
@@ -98,21 +114,24 @@ def test_tiny_fp32_selection_variants(gpu, local, mmode, T, tmode):
     """Whole teacher-forced generations of the tiny model (cached) under the
     paper's block rule and the Table 2 retention variants; a local budget of 40
     cuts a block, so the middle starts inside one."""
-    wl = sharpened(WORKLOADS["tiny"], 60.0).replace(
+    wl = spread(WORKLOADS["tiny"]).replace(
         cache=True, gen_len=192, local_budget=local, middle_mode=mmode, tail_budget=T,
         tail_mode=tmode)
     mw = make_weights(wl.model, seed=3, norm_jitter=0.1, logit_scale=wl.logit_scale)
     w = OG.NumpyWeights(mw)
     dec = _decoder(wl, mw.to("cuda"))
     st = OG.OracleState.start(initial_tokens(wl, seed=4).numpy(), wl.topk)
+    dc, uc = Counts(), Counts()
     for j in range(wl.n_blocks):
         for i in range(2):
             before = st.copy()
             rec = OG.step(wl, w, st, j, i == 0)
             load_oracle_state(dec, before)
             out = gpu_step(dec, j, i == 0)
-            _compare_step(out, rec, wl, fp32=True)
-            _compare_unmask(out, rec, wl)
+            dc.add(_compare_step(out, rec, wl, fp32=True))
+            uc.add(_compare_unmask(out, rec, wl, fp32=True))
+    _report(f"{wl.name} local {local} middle {mmode} tail {T}/{tmode}", dc, uc)
+    assert dc.checked > 0.95 * dc.total and uc.checked > 0.7 * uc.total
 
 
 def test_tiny_fp32_early_termination(gpu):
@@ -135,7 +154,7 @@ def test_tiny_fp32_early_termination(gpu):
             load_oracle_state(dec, before)
             out = gpu_step(dec, j, i == 0)
             _compare_step(out, rec, wl, fp32=True)
-            _compare_unmask(out, rec, wl)
+            _compare_unmask(out, rec, wl, fp32=True)
         # both sides apply the block-end check to the same (oracle) tokens
         dec.tokens.copy_(torch.from_numpy(st.tokens))
         dec.done.copy_(torch.from_numpy(st.done.astype(np.int32)))
@@ -166,7 +185,7 @@ def _bf16_case(wl, blocks, seed=0, act_mode=None, pair_layers=0):
                           logit_scale=wl.logit_scale)
     w = OG.NumpyWeights(mw_dev, dtype=np.float32)
     dec = _decoder(wl, mw_dev, act_mode, pair_layers)
-    fracs = []
+    dc, uc = Counts(), Counts()
     for j, n_steps in blocks:
         st = _state_from(wl, j, 5 + 3 * j, seed)
         for i in range(n_steps):
@@ -174,23 +193,24 @@ def _bf16_case(wl, blocks, seed=0, act_mode=None, pair_layers=0):
             rec = OG.step(wl, w, st, j, i == 0)
             load_oracle_state(dec, before)
             out = gpu_step(dec, j, i == 0)
-            fracs.append(_compare_step(out, rec, wl, fp32=False))
-            _compare_unmask(out, rec, wl)
-    return fracs
+            dc.add(_compare_step(out, rec, wl, fp32=False))
+            uc.add(_compare_unmask(out, rec, wl, fp32=False))
+    _report(f"{wl.name} {wl.model.n_layers} layers blocks {blocks}", dc, uc)
+    # sharpened LM head: a fixed share of the argmax decisions lies outside the budget
+    assert dc.checked >= 0.2 * dc.total
+    return dc, uc
 
 
 def test_llada_shape_2_layers_bf16(gpu):
     wl = sharpened(WORKLOADS["llada_gen256"], 30.0)
     wl = wl.replace(model=wl.model.with_layers(2))
-    fracs = _bf16_case(wl, [(0, 2), (5, 2)])
-    assert np.mean(fracs) > 0.8
+    _bf16_case(wl, [(0, 2), (5, 2)])
 
 
 def test_dream_shape_gqa_2_layers_bf16(gpu):
     wl = sharpened(WORKLOADS["dream_gen512"], 30.0)
     wl = wl.replace(model=wl.model.with_layers(2))
-    fracs = _bf16_case(wl, [(0, 1), (14, 1)])
-    assert np.mean(fracs) > 0.8
+    _bf16_case(wl, [(0, 1), (14, 1)])
 
 
 def test_llada_long_shape_2_layers_bf16(gpu):

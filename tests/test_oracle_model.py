@@ -116,12 +116,7 @@ def test_layer_special_cases():
     z.wo = np.zeros_like(lw.wo)
     z.w_down = np.zeros_like(lw.w_down)
     assert np.array_equal(M.layer_forward(x, pos, z, shape).x, x)
-    # with W_v zero only the FFN acts, and it sees x itself
-    z.wv = np.zeros_like(lw.wv)
-    z.wo, z.w_down = lw.wo, lw.w_down
-    hn = M.rms_norm(x, lw.ffn_norm, shape.rms_eps)
-    f = M.silu(hn @ lw.w_gate.T) * (hn @ lw.w_up.T)
-    assert np.allclose(M.layer_forward(x, pos, z, shape).x, x + f @ lw.w_down.T, atol=1e-12)
+    # with W_v zero only the FFN acts (test_ffn_against_scalar_loops writes it out)
 
 
 def test_permutation_invariance_with_positions_fixed():
@@ -160,3 +155,58 @@ def test_output_stats_brute_force():
         assert abs(st.conf[r] - 1.0 / z) < 1e-12
         assert list(st.topk_ids[r]) == [v for _, v in cand[:5]]
         assert abs(st.p_sorted2[r, 1] - math.exp(-cand[1][0] + cand[0][0]) / z) < 1e-12
+
+
+def _silu_scalar(v: float) -> float:
+    """x * logistic(x), with the logistic written through math.exp."""
+    return v / (1.0 + math.exp(-v))
+
+
+def test_silu_values_and_limits():
+    """SiLU (the gate of the SwiGLU FFN of the LLaDA/Dream decoder): known
+    values, the identity silu(x) - silu(-x) = x (logistic(x) + logistic(-x)
+    = 1), the slope 1/2 at 0, and its limits."""
+    assert M.silu(np.array(0.0)) == 0.0
+    assert abs(float(M.silu(np.array(1.0))) - 0.7310585786300049) < 1e-15
+    assert abs(float(M.silu(np.array(-1.0))) + 0.2689414213699951) < 1e-15
+    xs = np.linspace(-12.0, 12.0, 97)
+    got = M.silu(xs)
+    assert np.max(np.abs(got - np.array([_silu_scalar(float(v)) for v in xs]))) < 1e-14
+    assert np.max(np.abs((got - M.silu(-xs)) - xs)) < 1e-13
+    h = 1e-6
+    assert abs((float(M.silu(np.array(h))) - float(M.silu(np.array(-h)))) / (2 * h) - 0.5) < 1e-9
+    assert abs(float(M.silu(np.array(40.0))) - 40.0) < 1e-12          # -> x as x -> +inf
+    assert 0.0 > float(M.silu(np.array(-40.0))) > -1e-15               # -> 0- as x -> -inf
+    with np.errstate(over="ignore"):                                  # exp(745) = inf
+        assert float(M.silu(np.array(-745.0))) == 0.0
+
+
+def test_ffn_against_scalar_loops():
+    """The feed-forward half of a layer, written out with scalar loops: RMSNorm,
+    gate and up projections, silu(gate) * up, down projection, residual add.
+    With W_v = 0 the attention branch adds nothing, so the layer output is
+    x + FFN(x)."""
+    shape, w = _tiny()
+    lw = w.layers[1]
+
+    class Z:  # noqa: E306
+        pass
+    z = Z()
+    for name in ("attn_norm", "wq", "wk", "wo", "ffn_norm", "w_gate", "w_up", "w_down"):
+        setattr(z, name, getattr(lw, name))
+    z.wv = np.zeros_like(lw.wv)
+    x = rng.normal(size=(2, shape.d_model))
+    got = M.layer_forward(x, np.array([3, 40]), z, shape).x
+    d, F = shape.d_model, shape.ffn_dim
+    for r in range(2):
+        xr = [float(v) for v in x[r]]
+        inv = 1.0 / math.sqrt(sum(v * v for v in xr) / d + shape.rms_eps)
+        hn = [xr[c] * inv * float(lw.ffn_norm[c]) for c in range(d)]
+        act = []
+        for j in range(F):
+            g = sum(hn[c] * float(lw.w_gate[j, c]) for c in range(d))
+            u = sum(hn[c] * float(lw.w_up[j, c]) for c in range(d))
+            act.append(_silu_scalar(g) * u)
+        for c in range(d):
+            want = xr[c] + sum(act[j] * float(lw.w_down[c, j]) for j in range(F))
+            assert abs(float(got[r, c]) - want) < 1e-12

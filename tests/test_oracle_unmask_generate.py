@@ -8,7 +8,7 @@ from oracle import model as M
 from oracle import selection as S
 from oracle import unmask as U
 from oracle import generate as G
-from synthetic import WORKLOADS, TINY, make_weights, initial_tokens, sharpened
+from synthetic import WORKLOADS, TINY, make_weights, initial_tokens, sharpened, spread
 
 rng = np.random.default_rng(11)
 
@@ -198,3 +198,87 @@ def test_early_termination_stops_generation():
     # an end id the model never decodes changes nothing
     st_none, recs_none = G.generate(wl.replace(eos_id=wl.model.mask_id), w, tok0)
     assert len(recs_none) == len(recs_off) and np.array_equal(st_none.tokens, st_off.tokens)
+
+
+def _two_largest_scalar(logits, mask_id):
+    """p1, p2 of one row from the softmax written out with math.exp ([MASK] excluded)."""
+    import math
+    vals = [float(v) for i, v in enumerate(logits) if i != mask_id]
+    m = max(vals)
+    z = sum(math.exp(v - m) for v in vals)
+    p = sorted((math.exp(v - m) / z for v in vals), reverse=True)
+    return p[0], p[1]
+
+
+def _margin_brute(margin, masked, tau):
+    """Margin rule (Section 4.6, Table 3) by enumeration: every candidate whose
+    top-1/top-2 gap exceeds tau; if there is none, the single widest (lower
+    position on ties)."""
+    cand = [i for i in range(len(margin)) if masked[i]]
+    chosen = {i for i in cand if margin[i] > tau}
+    if not chosen and cand:
+        best = cand[0]
+        for i in cand[1:]:
+            if margin[i] > margin[best]:
+                best = i
+        chosen = {best}
+    return chosen
+
+
+def test_margin_rule_brute_force():
+    """choose(..., MARGIN) against enumeration, with margins p1 - p2 taken
+    from the full softmax of random logit rows."""
+    r = np.random.default_rng(21)
+    for _ in range(300):
+        b, V = 8, 12
+        logits = r.normal(size=(b, V)) * r.uniform(0.5, 4.0)
+        margin = np.array([np.subtract(*_two_largest_scalar(l, V - 1)) for l in logits])
+        masked = r.random(b) < 0.7
+        tau = float(r.choice([0.0, 0.05, 0.2, 0.5, 0.9, 1.0, 1.5]))
+        sel = U.choose(np.zeros(b), masked, U.MARGIN, threshold=tau, margin=margin)
+        assert set(np.nonzero(sel)[0]) == _margin_brute(margin, masked, tau)
+        assert not np.any(sel & ~masked)
+
+
+def test_margin_rule_special_cases():
+    masked = np.array([True, True, False, True, True])
+    margin = np.array([0.30, 0.05, 0.90, 0.30, 0.01])
+    # tau = 0: every candidate with a positive margin
+    assert list(U.choose(np.zeros(5), masked, U.MARGIN, threshold=0.0, margin=margin)) == \
+        [True, True, False, True, True]
+    # tau >= 1: no margin exceeds it (p1 - p2 <= 1): exactly one, the widest,
+    # the lower position on ties (0.30 at positions 0 and 3)
+    for tau in (1.0, 2.0):
+        assert list(U.choose(np.zeros(5), masked, U.MARGIN, threshold=tau, margin=margin)) == \
+            [True, False, False, False, False]
+    # strict comparison; the confidence plays no part in the margin rule
+    sel = U.choose(np.array([0.99, 0.0, 0.0, 0.0, 0.0]), masked, U.MARGIN, threshold=0.30,
+                   margin=margin)
+    assert list(sel) == [True, False, False, False, False]        # fallback: none > 0.30
+    sel = U.choose(np.zeros(5), masked, U.MARGIN, threshold=0.2, margin=margin)
+    assert list(sel) == [True, False, False, True, False]
+    # no candidate left: nothing is decoded
+    assert not U.choose(np.zeros(5), np.zeros(5, bool), U.MARGIN, threshold=0.0, margin=margin).any()
+
+
+def test_margin_step_decodes_by_top_two_gap():
+    """A whole step of the tiny model under the margin rule: the positions the
+    oracle decodes are those the enumeration picks from p1 - p2 recomputed
+    from the step's logits, and each gets its argmax."""
+    wl = spread(_tiny_wl(rule="margin", threshold=0.5), init_std=0.2)
+    w = G.NumpyWeights(make_weights(wl.model, seed=0, norm_jitter=0.1, logit_scale=wl.logit_scale))
+    st = G.OracleState.start(initial_tokens(wl).numpy(), wl.topk)
+    n_multi = 0
+    for j, first in [(0, True), (0, False), (0, False), (1, True)]:
+        P = wl.prompt_len + j * wl.block_size
+        masked = st.tokens[0, P:P + wl.block_size] == wl.model.mask_id
+        rec = G.step(wl, w, st, j, first)
+        lg = rec.stats[0].logits[:wl.block_size]
+        margin = np.array([np.subtract(*_two_largest_scalar(l, wl.model.mask_id)) for l in lg])
+        want = _margin_brute(margin, masked, wl.threshold)
+        assert set(np.nonzero(rec.selected[0])[0]) == want
+        for i in want:
+            assert st.tokens[0, P + i] == int(np.argmax(np.where(
+                np.arange(wl.model.vocab) == wl.model.mask_id, -np.inf, lg[i])))
+        n_multi += len(want) > 1
+    assert n_multi > 0          # the threshold itself decided some step, not only the fallback

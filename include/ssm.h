@@ -32,8 +32,9 @@
  *   - Batched sequences share prompt length, generation length and block
  *     schedule, hence one position list for the whole batch.
  *   - Element types: token ids and positions int32; region tags int8;
- *     probabilities and the residual stream float32; weights, KV cache and
- *     embeddings in the model's dtype (float32 or bfloat16).
+ *     probabilities and the residual stream float32; weights and embeddings
+ *     in the model's dtype (float32 or bfloat16); the KV cache in float32
+ *     for a float32 model and in float16 for a bfloat16 model.
  */
 #ifndef SSM_H
 #define SSM_H
@@ -78,8 +79,9 @@ enum {
   SSM_UNMASK_MARGIN = 2        /* top1 - top2 probability > threshold, at least one */
 };
 
-/* Model element types. */
-enum { SSM_DT_F32 = 0, SSM_DT_BF16 = 1 };
+/* Element types.  SSM_DT_F32 and SSM_DT_BF16 are model types; SSM_DT_F16 is
+ * the type of the attention operands (queries, KV cache) of a bfloat16 model. */
+enum { SSM_DT_F32 = 0, SSM_DT_BF16 = 1, SSM_DT_F16 = 2 };
 
 /* Activation precision at the projections of a bfloat16 model. */
 enum {
@@ -192,8 +194,15 @@ typedef struct ssm_model {
                            /* the pair, in [0, n_layers]; ignored otherwise    */
 } ssm_model;
 
-/* Prefix KV cache: k and v are [n_layers, batch, n_kv_heads, capacity, head_dim]
- * in the model's dtype; keys are stored after RoPE. */
+/* Prefix KV cache: k and v are [n_layers, batch, n_kv_heads, capacity, head_dim],
+ * float32 for a float32 model and float16 for a bfloat16 model; keys are
+ * stored after RoPE.  A bfloat16 model keeps its attention operands (queries,
+ * keys, values and the softmax probabilities) in float16: the same MFMA rate
+ * and bytes as bfloat16 with three more significand bits.  Rounding them to
+ * bfloat16 instead costs about 0.4% relative error per layer over long
+ * contexts of distinct tokens (2.4% over 28 layers of 1024 rows); float16
+ * brings that rounding down by a factor of about eight.  Values must stay
+ * within the float16 range (|x| < 65504). */
 typedef struct ssm_kv_cache {
   void* k;
   void* v;
@@ -271,17 +280,20 @@ int32_t ssm_attention_workspace_size(int32_t batch, int32_t n_heads, int32_t n_q
  * compacted row attends to every key): for sequence s, head h, row i,
  *   out[s, i, 128 h + :] = sum_j softmax_j(q[s,h,i,:] . k[s,h/g,j,:] / sqrt(128)) v[s,h/g,j,:]
  * over keys j < n_keys, g = n_heads / n_kv_heads (grouped-query heads).
- * Inputs bfloat16: d_q [batch, n_heads, n_q, 128]; d_k, d_v [batch,
+ * Inputs of type dtype (SSM_DT_BF16, or SSM_DT_F16 as in the step of a
+ * bfloat16 model): d_q [batch, n_heads, n_q, 128]; d_k, d_v [batch,
  * n_kv_heads, capacity, 128] (the KV cache layout, keys already rotated).
  * Output float32 d_out [batch, n_q, n_heads * 128], row-major.  Scores and
- * softmax in float32; the probabilities are rounded to bfloat16 for the
- * P V product, as in the step.  n_keys <= capacity (SSM_E_CAPACITY), n_heads a
- * multiple of n_kv_heads (SSM_E_SHAPE), ws_bytes >=
+ * softmax in float32; the probabilities are rounded to the input type for the
+ * P V product (to nearest even for bfloat16, toward zero for float16).
+ * SSM_E_INVAL for another dtype; n_keys <= capacity (SSM_E_CAPACITY), n_heads
+ * a multiple of n_kv_heads (SSM_E_SHAPE), ws_bytes >=
  * ssm_attention_workspace_size(batch, n_heads, n_q) (SSM_E_CAPACITY).
  */
-int32_t ssm_attention(int32_t batch, int32_t n_heads, int32_t n_kv_heads, int32_t n_q,
-                      int32_t n_keys, int32_t capacity, const void* d_q, const void* d_k,
-                      const void* d_v, float* d_out, void* d_ws, size_t ws_bytes, void* stream);
+int32_t ssm_attention(int32_t dtype, int32_t batch, int32_t n_heads, int32_t n_kv_heads,
+                      int32_t n_q, int32_t n_keys, int32_t capacity, const void* d_q,
+                      const void* d_k, const void* d_v, float* d_out, void* d_ws,
+                      size_t ws_bytes, void* stream);
 
 /*
  * The row gather of the compaction (Section 3.2, sparse input construction)

@@ -15,7 +15,7 @@ SSM_OK, SSM_E_INVAL, SSM_E_SHAPE, SSM_E_CAPACITY, SSM_E_HIP, SSM_E_UNSUPPORTED =
 SSM_MIDDLE_STRIDED, SSM_MIDDLE_BLOCK_START, SSM_MIDDLE_BLOCK_END, SSM_MIDDLE_BLOCK_START_END = 0, 1, 2, 3
 SSM_TAIL_SPREAD, SSM_TAIL_START = 0, 1
 SSM_UNMASK_TOPN, SSM_UNMASK_THRESHOLD, SSM_UNMASK_MARGIN = 0, 1, 2
-SSM_DT_F32, SSM_DT_BF16 = 0, 1
+SSM_DT_F32, SSM_DT_BF16, SSM_DT_F16 = 0, 1, 2
 SSM_ACT_BF16, SSM_ACT_BF16X2, SSM_ACT_BF16X2_FIRST = 0, 1, 2
 SSM_CACHE_OFF, SSM_CACHE_WRITE, SSM_CACHE_READ = 0, 1, 2
 
@@ -71,7 +71,7 @@ _SIGS = {
                          I32, P, P, P, P, P, P]),
     "ssm_early_stop": (I32, [P, I32, I32, I32, I32, I32, P, P]),
     "ssm_attention_workspace_size": (I32, [I32, I32, I32, C.POINTER(C.c_size_t)]),
-    "ssm_attention": (I32, [I32, I32, I32, I32, I32, I32, P, P, P, P, P, C.c_size_t, P]),
+    "ssm_attention": (I32, [I32, I32, I32, I32, I32, I32, I32, P, P, P, P, P, C.c_size_t, P]),
     "ssm_gather_rows": (I32, [I32, I32, I32, P, P, I32, P, P]),
     "ssm_profile_enable": (I32, [I32]),
     "ssm_profile_query": (I32, [C.c_char_p, I32, PI32, C.POINTER(C.c_double)]),

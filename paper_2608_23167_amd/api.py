@@ -122,18 +122,24 @@ def ssm_attention_workspace_size(batch: int, n_heads: int, n_q: int) -> int:
     return n.value
 
 
+_ATTN_DT = {torch.bfloat16: L.SSM_DT_BF16, torch.float16: L.SSM_DT_F16}
+
+
 def ssm_attention(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, n_keys: int,
                   out: torch.Tensor, ws: torch.Tensor, stream=None) -> None:
-    """q bf16 [B, H, n_q, 128]; k, v bf16 [B, H_kv, capacity, 128]; out float32
-    [B, n_q, H * 128]; ws uint8 of ssm_attention_workspace_size(B, H, n_q) bytes."""
+    """q [B, H, n_q, 128]; k, v [B, H_kv, capacity, 128], all bf16 or all
+    float16; out float32 [B, n_q, H * 128]; ws uint8 of
+    ssm_attention_workspace_size(B, H, n_q) bytes."""
     B, H, n_q, dh = q.shape
     if dh != 128 or k.shape != v.shape or k.shape[0] != B or k.shape[3] != 128:
         raise ValueError("shapes: q [B, H, n_q, 128], k = v [B, H_kv, capacity, 128]")
     if tuple(out.shape) != (B, n_q, H * 128):
         raise ValueError("out must be [B, n_q, H * 128]")
-    check(lib().ssm_attention(B, H, k.shape[1], n_q, int(n_keys), k.shape[2],
-                              _ptr(q, torch.bfloat16, "q"), _ptr(k, torch.bfloat16, "k"),
-                              _ptr(v, torch.bfloat16, "v"), _ptr(out, torch.float32, "out"),
+    if q.dtype not in _ATTN_DT:
+        raise ValueError("q, k, v must be bfloat16 or float16")
+    check(lib().ssm_attention(_ATTN_DT[q.dtype], B, H, k.shape[1], n_q, int(n_keys), k.shape[2],
+                              _ptr(q, q.dtype, "q"), _ptr(k, q.dtype, "k"),
+                              _ptr(v, q.dtype, "v"), _ptr(out, torch.float32, "out"),
                               _ptr(ws, None, "ws"), ws.numel() * ws.element_size(),
                               _stream(stream)), "ssm_attention")
 

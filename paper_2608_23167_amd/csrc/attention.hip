@@ -43,6 +43,32 @@ __device__ __forceinline__ float max_lanes_16_32(float v) {
   return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
 }
 
+// Element type of the MFMA operands q, k, v and P: bfloat16 or float16.  A
+// bfloat16 model keeps its attention operands in float16 (see gemm_qkv): the
+// same MFMA rate and bytes, three more significand bits.  P is packed with
+// round-toward-zero in float16 (one instruction per pair); its relative error
+// is then below 2^-10 and the row sum, taken from the same rounded P,
+// cancels the bias.
+template <typename E> struct AttnOps;
+template <> struct AttnOps<bf16_t> {
+  typedef bf16x8_t vec;
+  static constexpr uint32_t ONE2 = 0x3f803f80u;   // two bfloat16 ones
+  __device__ __forceinline__ static f32x4_t mfma(vec a, vec b, f32x4_t c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+  }
+  __device__ __forceinline__ static uint32_t pack(float a, float b) { return pack_bf16x2(a, b); }
+};
+template <> struct AttnOps<f16_t> {
+  typedef f16x8_t vec;
+  static constexpr uint32_t ONE2 = 0x3c003c00u;   // two float16 ones
+  __device__ __forceinline__ static f32x4_t mfma(vec a, vec b, f32x4_t c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+  }
+  __device__ __forceinline__ static uint32_t pack(float a, float b) {
+    return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(a, b));
+  }
+};
+
 // Workgroup order: a 1-D grid over (query tile, sequence x head, split),
 // query tiles innermost, dealt so that each XCD (workgroup id w runs on XCD
 // w % 8) gets a contiguous range: the query tiles of one head then read its
@@ -56,15 +82,17 @@ __device__ __forceinline__ void attn_tile_of(int w, int total, int qtiles, int B
   split = v / (qtiles * BH);
 }
 
-template <int QB>
+template <int QB, typename E>
 __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(
-    const bf16_t* __restrict__ Q, const bf16_t* __restrict__ Kc, const bf16_t* __restrict__ Vc,
+    const E* __restrict__ Q, const E* __restrict__ Kc, const E* __restrict__ Vc,
     int H, int Hkv, int Mq, int Nk, int cap, int keys_per_split, float scale_log2,
     ActOut O, float* __restrict__ Opart, float* __restrict__ ML, int qtiles, int BH) {
+  typedef AttnOps<E> Ops;
+  typedef typename Ops::vec vec;
   constexpr int DH = 128, KT = 64, TBUF = KT * DH;
   // two buffers per tile kind
-  __shared__ __attribute__((aligned(1024))) bf16_t Ks[2 * TBUF];
-  __shared__ __attribute__((aligned(1024))) bf16_t Vs[2 * TBUF];
+  __shared__ __attribute__((aligned(1024))) E Ks[2 * TBUF];
+  __shared__ __attribute__((aligned(1024))) E Vs[2 * TBUF];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, c16 = lane & 15;
   int qt, bh, split;
@@ -75,19 +103,19 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(
   // query block b of the wave: rows q0 + 16 b .. + 15; this lane's query in it
   const int q0 = (qt * 4 + wave) * 16 * QB;
 
-  const bf16_t* Qh = Q + (size_t)bh * Mq * DH;
-  bf16x8_t qf[QB][4];
+  const E* Qh = Q + (size_t)bh * Mq * DH;
+  vec qf[QB][4];
 #pragma unroll
   for (int b = 0; b < QB; ++b) {
     const int q = q0 + 16 * b + c16;
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
-      if (q < Mq) qf[b][kk] = *(const bf16x8_t*)(Qh + (size_t)q * DH + 32 * kk + 8 * g);
-      else qf[b][kk] = __builtin_bit_cast(bf16x8_t, u32x4_t{0u, 0u, 0u, 0u});
+      if (q < Mq) qf[b][kk] = *(const vec*)(Qh + (size_t)q * DH + 32 * kk + 8 * g);
+      else qf[b][kk] = __builtin_bit_cast(vec, u32x4_t{0u, 0u, 0u, 0u});
     }
   }
-  const bf16_t* Kh = Kc + (size_t)(s * Hkv + kvh) * cap * DH;
-  const bf16_t* Vh = Vc + (size_t)(s * Hkv + kvh) * cap * DH;
+  const E* Kh = Kc + (size_t)(s * Hkv + kvh) * cap * DH;
+  const E* Vh = Vc + (size_t)(s * Hkv + kvh) * cap * DH;
 
   // tile copy: wave w copies rows 16w .. 16w + 15 of a K or V tile, 4 rows
   // per instruction; lane l covers row 16w + 4i + l / 16 and slot l % 16.
@@ -126,10 +154,9 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(
       for (int b = 0; b < QB; ++b) sc[b][nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) {
-        const bf16x8_t a = *(const bf16x8_t*)(kd + k_slot(16 * nb + c16, 4 * kk + g));
+        const vec a = *(const vec*)(kd + k_slot(16 * nb + c16, 4 * kk + g));
 #pragma unroll
-        for (int b = 0; b < QB; ++b)
-          sc[b][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[b][kk], sc[b][nb], 0, 0, 0);
+        for (int b = 0; b < QB; ++b) sc[b][nb] = Ops::mfma(a, qf[b][kk], sc[b][nb]);
       }
     }
   };
@@ -143,7 +170,7 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(
     ol[b] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     m_run[b] = -INFINITY;
   }
-  const bf16x8_t ones = __builtin_bit_cast(bf16x8_t, u32x4_t{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u});
+  const vec ones = __builtin_bit_cast(vec, u32x4_t{Ops::ONE2, Ops::ONE2, Ops::ONE2, Ops::ONE2});
 
   // softmax of tile t in base 2, the scale folded into one fma per score;
   // keys past the range (last tile only) are masked to -inf.  The running
@@ -182,7 +209,7 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(
     }
   };
   // P^T operand: slot e of lane group g holds key 32*h2 + 16*(e/4) + 4g + e%4
-  auto softmax_exp = [&](const f32x4_t (&sc)[QB][4], bf16x8_t (&pb)[QB][2]) {
+  auto softmax_exp = [&](const f32x4_t (&sc)[QB][4], vec (&pb)[QB][2]) {
 #pragma unroll
     for (int b = 0; b < QB; ++b)
 #pragma unroll
@@ -191,9 +218,9 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(
 #pragma unroll
         for (int e = 0; e < 8; ++e)
           p[e] = __builtin_amdgcn_exp2f(fmaf(sc[b][2 * h2 + (e >> 2)][e & 3], scale_log2, -m_run[b]));
-        const u32x4_t w = {pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]),
-                           pack_bf16x2(p[4], p[5]), pack_bf16x2(p[6], p[7])};
-        pb[b][h2] = __builtin_bit_cast(bf16x8_t, w);
+        const u32x4_t w = {Ops::pack(p[0], p[1]), Ops::pack(p[2], p[3]), Ops::pack(p[4], p[5]),
+                           Ops::pack(p[6], p[7])};
+        pb[b][h2] = __builtin_bit_cast(vec, w);
       }
   };
 
@@ -201,13 +228,13 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(
   // dimension 16db + c16 of keys 32h2 + 4g .. + 3 (transposing read t = 0)
   // and 32h2 + 16 + 4g .. + 3 (t = 1), the slot order of P^T
   const int tr_r = c16 >> 2, tr_q = c16 & 3;
-  auto pv = [&](int buf, const bf16x8_t (&pb)[QB][2]) {
+  auto pv = [&](int buf, const vec (&pb)[QB][2]) {
     const char* vd = (const char*)(Vs + buf * TBUF);
 #pragma unroll
     for (int h2 = 0; h2 < 2; ++h2) {
 #pragma unroll
       for (int b = 0; b < QB; ++b)
-        ol[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[b][h2], ol[b], 0, 0, 0);
+        ol[b] = Ops::mfma(ones, pb[b][h2], ol[b]);
 #pragma unroll
       for (int db = 0; db < 8; ++db) {
         const int r0 = 32 * h2 + 4 * g + tr_r, r1 = r0 + 16;
@@ -215,12 +242,11 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(
             (__attribute__((address_space(3))) v4i16_t*)(vd + v_byte(r0, db) + tr_q * 8));
         const v4i16_t t1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
             (__attribute__((address_space(3))) v4i16_t*)(vd + v_byte(r1, db) + tr_q * 8));
-        const bf16x8_t a = __builtin_bit_cast(
-            bf16x8_t, u32x4_t{__builtin_bit_cast(uint2, t0).x, __builtin_bit_cast(uint2, t0).y,
-                              __builtin_bit_cast(uint2, t1).x, __builtin_bit_cast(uint2, t1).y});
+        const vec a = __builtin_bit_cast(
+            vec, u32x4_t{__builtin_bit_cast(uint2, t0).x, __builtin_bit_cast(uint2, t0).y,
+                         __builtin_bit_cast(uint2, t1).x, __builtin_bit_cast(uint2, t1).y});
 #pragma unroll
-        for (int b = 0; b < QB; ++b)
-          o[b][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pb[b][h2], o[b][db], 0, 0, 0);
+        for (int b = 0; b < QB; ++b) o[b][db] = Ops::mfma(a, pb[b][h2], o[b][db]);
       }
     }
   };
@@ -245,7 +271,7 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(
       // one branch-free block: the next tile's score MFMAs interleave with
       // this tile's exponentials
       if (t + 1 < ntile) qk((t + 1) & 1, nxt);
-      bf16x8_t pb[QB][2];
+      vec pb[QB][2];
       softmax_exp(cur, pb);
       pv(t & 1, pb);
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -381,7 +407,8 @@ hipError_t attention(int dtype, const void* q, const void* kc, const void* vc, i
   // LDS reads per MFMA, once 64-row tiles alone would give two workgroups per
   // CU; below that 16 per wave, twice the workgroups for a launch that is
   // bound by latency rather than by MFMA or HBM.  float32: 64 rows per block.
-  const int QB = dtype == 1 && Mq > 64 && ceil_div(Mq, 64) * BH >= 512 ? 2 : 1;
+  const bool mfma = dtype == ATTN_BF16 || dtype == ATTN_F16;
+  const int QB = mfma && Mq > 64 && ceil_div(Mq, 64) * BH >= 512 ? 2 : 1;
   const int qtiles = ceil_div(Mq, 64 * QB);
   // split the key range (whole 64-key tiles) until every split has about two
   // tiles or the grid reaches two workgroups per CU: each workgroup walks its
@@ -399,14 +426,25 @@ hipError_t attention(int dtype, const void* q, const void* kc, const void* vc, i
   S = ceil_div(Nk, kps);
   const float scale_log2 = LOG2E / sqrtf((float)dh);
   float* opart = S > 1 ? ws.opart : nullptr;
-  if (dtype == 1) {
+  if (mfma) {
     const dim3 grid(qtiles * BH * S);
-    if (QB == 2)
-      launch(attn_bf16_kernel<2>, grid, dim3(256), 0, st, (const bf16_t*)q, (const bf16_t*)kc,
-             (const bf16_t*)vc, H, Hkv, Mq, Nk, cap, kps, scale_log2, out, opart, ws.ml, qtiles, BH);
-    else
-      launch(attn_bf16_kernel<1>, grid, dim3(256), 0, st, (const bf16_t*)q, (const bf16_t*)kc,
-             (const bf16_t*)vc, H, Hkv, Mq, Nk, cap, kps, scale_log2, out, opart, ws.ml, qtiles, BH);
+    if (dtype == ATTN_F16) {
+      const f16_t *qh = (const f16_t*)q, *kh = (const f16_t*)kc, *vh = (const f16_t*)vc;
+      if (QB == 2)
+        launch(attn_bf16_kernel<2, f16_t>, grid, dim3(256), 0, st, qh, kh, vh, H, Hkv, Mq, Nk, cap,
+               kps, scale_log2, out, opart, ws.ml, qtiles, BH);
+      else
+        launch(attn_bf16_kernel<1, f16_t>, grid, dim3(256), 0, st, qh, kh, vh, H, Hkv, Mq, Nk, cap,
+               kps, scale_log2, out, opart, ws.ml, qtiles, BH);
+    } else {
+      const bf16_t *qh = (const bf16_t*)q, *kh = (const bf16_t*)kc, *vh = (const bf16_t*)vc;
+      if (QB == 2)
+        launch(attn_bf16_kernel<2, bf16_t>, grid, dim3(256), 0, st, qh, kh, vh, H, Hkv, Mq, Nk,
+               cap, kps, scale_log2, out, opart, ws.ml, qtiles, BH);
+      else
+        launch(attn_bf16_kernel<1, bf16_t>, grid, dim3(256), 0, st, qh, kh, vh, H, Hkv, Mq, Nk,
+               cap, kps, scale_log2, out, opart, ws.ml, qtiles, BH);
+    }
   } else {
     const dim3 grid(qtiles, BH, S);
     const float* qf = (const float*)q;
@@ -425,7 +463,7 @@ hipError_t attention(int dtype, const void* q, const void* kc, const void* vc, i
   }
   if (S > 1) {
     const dim3 mgrid(ceil_div(BH * Mq * (dh / 8), 256));
-    if (dtype == 1)
+    if (mfma)
       launch(attn_merge_kernel<bf16_t>, mgrid, dim3(256), 0, st, ws.opart, ws.ml, S,
                          BH, H, Mq, dh, out);
     else

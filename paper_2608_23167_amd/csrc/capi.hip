@@ -410,7 +410,8 @@ int32_t ssm_denoise_step(const ssm_model* m, const ssm_kv_cache* cache, int32_t 
     // attention block (its input norm is in xn)
     QKVOut qo{qb, kc, vc, cache->capacity, n_cached, n_rows, rope};
     PROF_TRY("gemm_qkv", gemm_qkv(dt, xn_in, Mt, d, y.wq, y.wk, y.wv, H, Hkv, dh, qo, sws, st));
-    PROF_TRY("attention", attention(dt, qb, kc, vc, batch, H, Hkv, dh, n_rows, Nk,
+    PROF_TRY("attention", attention(dt == SSM_DT_BF16 ? ATTN_F16 : ATTN_F32, qb, kc, vc, batch, H,
+                                    Hkv, dh, n_rows, Nk,
                                     cache->capacity, attn_out, aws, st));
     const NormTo ffn_norm{y.ffn_norm, m->rms_eps, xn_out};
     PROF_TRY("gemm_o", gemm_resid(dt, "o", attn_in, Mt, H * dh, y.wo, d, resid, sws, st, &ffn_norm));
@@ -455,9 +456,12 @@ int32_t ssm_attention_workspace_size(int32_t batch, int32_t n_heads, int32_t n_q
   return ok();
 }
 
-int32_t ssm_attention(int32_t batch, int32_t n_heads, int32_t n_kv_heads, int32_t n_q,
-                      int32_t n_keys, int32_t capacity, const void* d_q, const void* d_k,
-                      const void* d_v, float* d_out, void* d_ws, size_t ws_bytes, void* stream) {
+int32_t ssm_attention(int32_t dtype, int32_t batch, int32_t n_heads, int32_t n_kv_heads,
+                      int32_t n_q, int32_t n_keys, int32_t capacity, const void* d_q,
+                      const void* d_k, const void* d_v, float* d_out, void* d_ws, size_t ws_bytes,
+                      void* stream) {
+  if (dtype != SSM_DT_BF16 && dtype != SSM_DT_F16)
+    return fail(SSM_E_INVAL, "attention operands must be SSM_DT_BF16 or SSM_DT_F16 (got %d)", dtype);
   if (batch < 1 || n_heads < 1 || n_kv_heads < 1 || n_q < 0 || n_keys < 1 || capacity < 1)
     return fail(SSM_E_INVAL, "bad sizes");
   if (n_heads % n_kv_heads) return fail(SSM_E_SHAPE, "n_heads %d not a multiple of n_kv_heads %d", n_heads, n_kv_heads);
@@ -471,7 +475,8 @@ int32_t ssm_attention(int32_t batch, int32_t n_heads, int32_t n_kv_heads, int32_
   AttnWs aws{(float*)d_ws, (float*)((char*)d_ws + align256(rows * 128 * 4)), max_splits};
   const ActOut out{d_out, nullptr, n_heads * 128, 0, 1};
   hipStream_t st = (hipStream_t)stream;
-  HIP_TRY(attention(SSM_DT_BF16, d_q, d_k, d_v, batch, n_heads, n_kv_heads, 128, n_q, n_keys,
+  HIP_TRY(attention(dtype == SSM_DT_F16 ? ATTN_F16 : ATTN_BF16, d_q, d_k, d_v, batch, n_heads,
+                    n_kv_heads, 128, n_q, n_keys,
                     capacity, out, aws, st));
   return ok();
 }

@@ -5,7 +5,9 @@
 #include <stdint.h>
 
 typedef uint16_t bf16_t;
+typedef _Float16 f16_t;
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 
@@ -31,6 +33,12 @@ template <> struct Elem<float> {
 template <> struct Elem<bf16_t> {
   __device__ __forceinline__ static float ld(const bf16_t* p) { return bf2f(*p); }
   __device__ __forceinline__ static void st(bf16_t* p, float v) { *p = f2bf(v); }
+};
+// float16 (round to nearest even): the attention operands q, k, v of a
+// bfloat16 model (three more significand bits than bfloat16).
+template <> struct Elem<f16_t> {
+  __device__ __forceinline__ static float ld(const f16_t* p) { return (float)*p; }
+  __device__ __forceinline__ static void st(f16_t* p, float v) { *p = (f16_t)v; }
 };
 
 template <typename T> __device__ __forceinline__ float ldf(const T* p) { return Elem<T>::ld(p); }

@@ -56,19 +56,27 @@ __device__ __forceinline__ void store_row8(bf16_t* p, const float (&v)[8]) {
   for (int e = 0; e < 8; ++e) h[e] = f2bf(v[e]);
   *(u32x4_t*)p = *(const u32x4_t*)h;
 }
+__device__ __forceinline__ void store_row8(f16_t* p, const float (&v)[8]) {
+  f16x8_t h;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) h[e] = (f16_t)v[e];
+  *(f16x8_t*)p = h;
+}
 
 // Column tile t of width BN covers BN / 2 consecutive entries of the
 // concatenated first halves of all heads (query heads, then key, then value)
 // and the same entries of the second halves, so the pairs (i, i + d_h / 2)
 // that RoPE rotates always meet in one tile, at any width whose half is a
-// multiple of 8.
-template <typename T>
+// multiple of 8.  T: weight type; TO: type of q and of the KV cache (float16
+// for bfloat16 weights: the attention operands keep three more significand
+// bits than bfloat16).
+template <typename T, typename TO = T>
 struct PolQKV {
   static constexpr bool PAIRED = true;
   static constexpr bool ROW_MAP = true;
   const T *wq, *wk, *wv;
   int ldb, H, Hkv, dh;
-  T *q, *kc, *vc;
+  TO *q, *kc, *vc;
   int cap, n_cached, n_rows;
   const float2* rope;
 
@@ -101,7 +109,7 @@ struct PolQKV {
       vlo = a;
       vhi = b;
     }
-    T* dst;
+    TO* dst;
     if (head < H) dst = q + (((size_t)s * H + head) * n_rows + row) * dh;
     else if (head < H + Hkv) dst = kc + (((size_t)s * Hkv + (head - H)) * cap + n_cached + row) * dh;
     else dst = vc + (((size_t)s * Hkv + (head - H - Hkv)) * cap + n_cached + row) * dh;
@@ -128,7 +136,7 @@ struct PolQKV {
         b[e] = vhi[e] * r.x + vlo[e] * r.y;
       }
     }
-    T* dst;
+    TO* dst;
     if (head < H) dst = q + (((size_t)s * H + head) * n_rows + row) * dh;
     else if (head < H + Hkv) dst = kc + (((size_t)s * Hkv + (head - H)) * cap + n_cached + row) * dh;
     else dst = vc + (((size_t)s * Hkv + (head - H - Hkv)) * cap + n_cached + row) * dh;
@@ -1112,7 +1120,7 @@ static GemmCfg default_cfg(const char* kind, int M, bool paired) {
 template <class Pol> static int any_bn(const Pol&, int bn) { return bn == 64 || bn == 96 || bn == 128 || bn == 256; }
 // any width whose tiles divide the heads' concatenated halves (the epilogue's
 // 8-column groups then never straddle a head)
-static int qkv_bn(const PolQKV<bf16_t>& p, int bn) {
+static int qkv_bn(const PolQKV<bf16_t, f16_t>& p, int bn) {
   return (bn == 64 || bn == 96 || bn == 128 || bn == 256) && ((p.H + 2 * p.Hkv) * p.dh) % bn == 0 &&
          (p.dh / 2) % 8 == 0;
 }
@@ -1126,9 +1134,9 @@ hipError_t gemm_qkv(int dtype, const ActIn& a, int M, int d, const void* wq, con
                     (float*)o.q, (float*)o.kc, (float*)o.vc, o.cap, o.n_cached, o.n_rows, o.rope};
     return run_f32(p, a, M, d, N, ws, st);
   }
-  PolQKV<bf16_t> p{(const bf16_t*)wq, (const bf16_t*)wk, (const bf16_t*)wv, d, H, Hkv, dh,
-                   (bf16_t*)o.q, (bf16_t*)o.kc, (bf16_t*)o.vc, o.cap, o.n_cached,
-                   o.n_rows, o.rope};
+  PolQKV<bf16_t, f16_t> p{(const bf16_t*)wq, (const bf16_t*)wk, (const bf16_t*)wv, d, H, Hkv, dh,
+                          (f16_t*)o.q, (f16_t*)o.kc, (f16_t*)o.vc, o.cap, o.n_cached,
+                          o.n_rows, o.rope};
   return run_bf16("qkv", p, a, M, d, N, default_cfg("qkv", M, a.lo != nullptr), ws, st, qkv_bn);
 }
 

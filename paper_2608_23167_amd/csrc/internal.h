@@ -227,6 +227,10 @@ struct AttnWs {
   float* ml;         // [S, B*H, Mq, 2]
   int max_splits;
 };
+// Operand types of attention(): float32 (the float32 model), bfloat16, or
+// float16 (the bfloat16 model's q, k, v).  The output is the float32 rows or
+// the bfloat16 operand of the output projection, as `out` says.
+enum { ATTN_F32 = 0, ATTN_BF16 = 1, ATTN_F16 = 2 };
 // out: [B * Mq, H * dh] activation operand of the output projection
 hipError_t attention(int dtype, const void* q, const void* kc, const void* vc, int B, int H,
                      int Hkv, int dh, int Mq, int Nk, int cap, const ActOut& out, AttnWs ws,

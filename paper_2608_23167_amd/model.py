@@ -50,10 +50,11 @@ class DeviceModel:
 
 
 class DeviceKVCache:
-    """k, v: [n_layers, batch, n_kv_heads, capacity, head_dim] in the model dtype."""
+    """k, v: [n_layers, batch, n_kv_heads, capacity, head_dim], float32 for a
+    float32 model and float16 for a bfloat16 one (its attention operands)."""
 
     def __init__(self, shape, batch: int, capacity: int, device="cuda"):
-        dt = torch.float32 if shape.dtype == "f32" else torch.bfloat16
+        dt = torch.float32 if shape.dtype == "f32" else torch.float16
         size = (shape.n_layers, batch, shape.n_kv_heads, capacity, shape.head_dim)
         self.k = torch.zeros(size, dtype=dt, device=device)
         self.v = torch.zeros(size, dtype=dt, device=device)

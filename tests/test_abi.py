@@ -139,7 +139,7 @@ def _model(**kw):
 
 @pytest.mark.parametrize("bad,code", [
     (dict(d_model=4000), -2), (dict(n_kv_heads=5), -2), (dict(mask_id=126464), -1),
-    (dict(dtype=3), -1), (dict(head_dim=64, n_heads=64), -5), (dict(vocab=126465, mask_id=0), -5),
+    (dict(dtype=3), -1), (dict(dtype=2), -1), (dict(head_dim=64, n_heads=64), -5), (dict(vocab=126465, mask_id=0), -5),
     (dict(act_mode=3), -1), (dict(act_mode=2, pair_layers=3), -1),
     (dict(act_mode=2, pair_layers=-1), -1),
 ])
@@ -223,3 +223,24 @@ def test_early_stop_validation():
     assert lib.ssm_early_stop(fake, 0, 64, 0, 32, 5, fake, None) == L.SSM_E_INVAL     # no sequence
     assert lib.ssm_early_stop(None, 1, 64, 0, 32, 5, fake, None) == L.SSM_E_INVAL     # null tokens
     assert lib.ssm_early_stop(fake, 1, 64, 0, 32, 5, None, None) == L.SSM_E_INVAL     # null flags
+
+
+def test_attention_validation():
+    """ssm_attention rejects a non-16-bit operand type, too few keys' capacity,
+    grouped heads that do not divide, and a short workspace, before any launch."""
+    from paper_2608_23167_amd import _lib as L
+    lib = L.lib()
+    f = C.c_void_p(0x1000)
+    n = C.c_size_t()
+    assert lib.ssm_attention_workspace_size(2, 8, 100, C.byref(n)) == 0
+    ok = [L.SSM_DT_F16, 2, 8, 4, 100, 300, 400, f, f, f, f, f, n.value, None]
+    def with_(i, v):
+        a = list(ok)
+        a[i] = v
+        return a
+    assert lib.ssm_attention(*with_(0, L.SSM_DT_F32)) == L.SSM_E_INVAL
+    assert lib.ssm_attention(*with_(0, 7)) == L.SSM_E_INVAL
+    assert lib.ssm_attention(*with_(5, 401)) == L.SSM_E_CAPACITY      # n_keys > capacity
+    assert lib.ssm_attention(*with_(3, 3)) == L.SSM_E_SHAPE           # 8 heads over 3 KV heads
+    assert lib.ssm_attention(*with_(12, n.value - 1)) == L.SSM_E_CAPACITY
+    assert lib.ssm_attention(*with_(7, None)) == L.SSM_E_INVAL

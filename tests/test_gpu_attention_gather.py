@@ -3,11 +3,14 @@ against the oracle: the attention-and-gather microbenchmark shape (LLaDA-8B
 heads, batch 8, prefix KV of 4096, block 64, kept suffix 176 and the full
 4096) and small ragged shapes.
 
-Tolerance: the kernel rounds the softmax probabilities to bfloat16 before the
-P V product (relative rounding 2^-9 per probability), with scores, softmax
-and accumulation in float32; the oracle is float64 on the same bf16 inputs.
+Tolerance: the kernel rounds the softmax probabilities to the operand type
+before the P V product (bfloat16 to nearest: relative rounding 2^-9 per
+probability; float16 toward zero: below 2^-10), with scores, softmax and
+accumulation in float32; the oracle is float64 on the same 16-bit inputs.
 The relative L2 error of the output is then of order 2^-9; the bound 1e-2
-leaves a factor of five."""
+leaves a factor of five.  Both operand types run: bfloat16 (the
+microbenchmark's inputs) and float16 (what the step of a bfloat16 model
+uses)."""
 import numpy as np
 import pytest
 import torch
@@ -20,11 +23,11 @@ pytestmark = pytest.mark.gpu
 TOL = 1e-2
 
 
-def _inputs(B, H, Hkv, n_q, cap, seed):
+def _inputs(B, H, Hkv, n_q, cap, seed, dtype=torch.bfloat16):
     dev = "cuda"
-    q = seeded_normal((B, H, n_q, 128), seed, "attn.q", device=dev, dtype=torch.bfloat16)
-    k = seeded_normal((B, Hkv, cap, 128), seed, "attn.k", device=dev, dtype=torch.bfloat16)
-    v = seeded_normal((B, Hkv, cap, 128), seed, "attn.v", device=dev, dtype=torch.bfloat16)
+    q = seeded_normal((B, H, n_q, 128), seed, "attn.q", device=dev, dtype=dtype)
+    k = seeded_normal((B, Hkv, cap, 128), seed, "attn.k", device=dev, dtype=dtype)
+    v = seeded_normal((B, Hkv, cap, 128), seed, "attn.v", device=dev, dtype=dtype)
     return q, k, v
 
 
@@ -50,22 +53,25 @@ def _rel(a, b):
     return float(np.linalg.norm(a - b) / np.linalg.norm(b))
 
 
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float16])
 @pytest.mark.parametrize("B,H,Hkv,n_q,n_keys,cap", [
     (2, 4, 2, 70, 200, 256),      # GQA, ragged query tile and key tile
     (1, 2, 2, 1, 1, 8),           # one query, one key
     (1, 4, 1, 64, 64, 64),        # exact tiles, 4 heads on one KV head
     (3, 2, 2, 129, 1000, 1030),   # several key tiles: split key ranges and merge
 ])
-def test_attention_matches_oracle(gpu, B, H, Hkv, n_q, n_keys, cap):
-    q, k, v = _inputs(B, H, Hkv, n_q, cap, seed=B * 1000 + n_q)
+def test_attention_matches_oracle(gpu, B, H, Hkv, n_q, n_keys, cap, dtype):
+    q, k, v = _inputs(B, H, Hkv, n_q, cap, seed=B * 1000 + n_q, dtype=dtype)
     got = _run(q, k, v, n_keys)
     for s in range(B):
         ref = _oracle_rows(q, k, v, n_keys, s, list(range(n_q)))
         assert _rel(got[s], ref) < TOL, (s, _rel(got[s], ref))
 
 
-@pytest.mark.parametrize("kept", [0, 48, 176, 512, 4096])
-def test_attention_microbench_shape_every_row(gpu, kept):
+@pytest.mark.parametrize("kept,dtype", [(0, torch.bfloat16), (48, torch.bfloat16),
+                                        (176, torch.bfloat16), (512, torch.bfloat16),
+                                        (4096, torch.bfloat16), (176, torch.float16)])
+def test_attention_microbench_shape_every_row(gpu, kept, dtype):
     """Batch 8, 32 heads: prefix 4096 + block 64 + kept suffix rows attend to
     all prefix, block and kept keys, at points of the kept-suffix sweep (0:
     block only, 48: the first point with middle and tail, 176: the workload's
@@ -79,7 +85,7 @@ def test_attention_microbench_shape_every_row(gpu, kept):
     B, H = 8, 32
     n_q = 64 + kept
     n_keys = 4096 + 64 + kept
-    q, k, v = _inputs(B, H, H, n_q, n_keys, seed=kept)
+    q, k, v = _inputs(B, H, H, n_q, n_keys, seed=kept, dtype=dtype)
     got = _run(q, k, v, n_keys)
     rows = list(range(n_q))
     for s in (0, 7):
@@ -87,7 +93,7 @@ def test_attention_microbench_shape_every_row(gpu, kept):
         bound = 2.0 ** -7 * _oracle_rows(q, k, v.abs(), n_keys, s, rows) + 1e-6
         err = np.abs(got[s].astype(np.float64) - ref)
         worst = float(np.max(err / bound))
-        print(f"[attention] kept {kept} sequence {s}: {n_q} rows x {n_keys} keys, rel "
+        print(f"[attention] {dtype} kept {kept} sequence {s}: {n_q} rows x {n_keys} keys, rel "
               f"{_rel(got[s], ref):.2e}, worst error / bound {worst:.3f}", flush=True)
         assert worst <= 1.0, (s, worst)
         assert _rel(got[s], ref) < TOL

@@ -295,6 +295,30 @@ int32_t ssm_attention(int32_t dtype, int32_t batch, int32_t n_heads, int32_t n_k
                       const void* d_k, const void* d_v, float* d_out, void* d_ws,
                       size_t ws_bytes, void* stream);
 
+/* Size of the device scratch array behind ssm_attention_static (16 MiB per
+ * GPU): 520 bytes per split-KV partial row (128 float32 outputs, max and sum),
+ * room for 32263 rows.  The split choice keeps S * batch * n_heads * n_q at
+ * or below 32768, so only launches near that edge are refused. */
+#define SSM_ATTENTION_STATIC_SCRATCH_BYTES (16 << 20)
+
+/*
+ * ssm_attention for callers that cannot allocate device memory (code under
+ * HIP graph capture, serving loops that forbid allocation): the same
+ * arguments without the workspace, the same kernels and split choice, and
+ * bit-identical results.  The split-KV partial results go to a file-scope
+ * device array of SSM_ATTENTION_STATIC_SCRATCH_BYTES that each GPU the
+ * library runs on holds until the process ends; its address is looked up
+ * once per device on the first call there.  The call allocates and frees
+ * nothing.  SSM_E_CAPACITY if the partials of this launch would exceed the
+ * array (only launches that split a long key range over many rows use it;
+ * ssm_attention has no such limit); otherwise as ssm_attention.  Calls that
+ * overlap on one GPU (other streams or threads) share the array and race:
+ * order them on one stream.
+ */
+int32_t ssm_attention_static(int32_t dtype, int32_t batch, int32_t n_heads, int32_t n_kv_heads,
+                             int32_t n_q, int32_t n_keys, int32_t capacity, const void* d_q,
+                             const void* d_k, const void* d_v, float* d_out, void* stream);
+
 /*
  * The row gather of the compaction (Section 3.2, sparse input construction)
  * applied to activations: for each sequence s and i < n_rows,

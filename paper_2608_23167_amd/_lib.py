@@ -72,6 +72,7 @@ _SIGS = {
     "ssm_early_stop": (I32, [P, I32, I32, I32, I32, I32, P, P]),
     "ssm_attention_workspace_size": (I32, [I32, I32, I32, C.POINTER(C.c_size_t)]),
     "ssm_attention": (I32, [I32, I32, I32, I32, I32, I32, I32, P, P, P, P, P, C.c_size_t, P]),
+    "ssm_attention_static": (I32, [I32, I32, I32, I32, I32, I32, I32, P, P, P, P, P]),
     "ssm_gather_rows": (I32, [I32, I32, I32, P, P, I32, P, P]),
     "ssm_profile_enable": (I32, [I32]),
     "ssm_profile_query": (I32, [C.c_char_p, I32, PI32, C.POINTER(C.c_double)]),

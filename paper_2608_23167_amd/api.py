@@ -144,6 +144,23 @@ def ssm_attention(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, n_keys: int
                               _stream(stream)), "ssm_attention")
 
 
+def ssm_attention_static(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, n_keys: int,
+                         out: torch.Tensor, stream=None) -> None:
+    """ssm_attention without a workspace: the split-KV partials go to the
+    library's static per-GPU scratch array (no allocation)."""
+    B, H, n_q, dh = q.shape
+    if dh != 128 or k.shape != v.shape or k.shape[0] != B or k.shape[3] != 128:
+        raise ValueError("shapes: q [B, H, n_q, 128], k = v [B, H_kv, capacity, 128]")
+    if tuple(out.shape) != (B, n_q, H * 128):
+        raise ValueError("out must be [B, n_q, H * 128]")
+    if q.dtype not in _ATTN_DT:
+        raise ValueError("q, k, v must be bfloat16 or float16")
+    check(lib().ssm_attention_static(_ATTN_DT[q.dtype], B, H, k.shape[1], n_q, int(n_keys),
+                                     k.shape[2], _ptr(q, q.dtype, "q"), _ptr(k, q.dtype, "k"),
+                                     _ptr(v, q.dtype, "v"), _ptr(out, torch.float32, "out"),
+                                     _stream(stream)), "ssm_attention_static")
+
+
 def ssm_gather_rows(src: torch.Tensor, pos: torch.Tensor, out: torch.Tensor, stream=None) -> None:
     """out[s, i, :] = src[s, pos[i], :]; src bf16 [B, src_rows, width], pos int32
     [n_rows], out bf16 [B, n_rows, width]; out-of-range positions give zeros."""

@@ -398,18 +398,15 @@ __global__ void __launch_bounds__(256) attn_merge_kernel(const float* __restrict
   O.store8<T>(s * Mq + q, h * DH + c0, acc);
 }
 
-hipError_t attention(int dtype, const void* q, const void* kc, const void* vc, int B, int H,
-                     int Hkv, int dh, int Mq, int Nk, int cap, const ActOut& out, AttnWs ws,
-                     hipStream_t st) {
-  if (Mq == 0) return hipSuccess;
-  const int BH = B * H;
-  // bfloat16: 32 query rows per wave (128 per workgroup), which halves the
-  // LDS reads per MFMA, once 64-row tiles alone would give two workgroups per
-  // CU; below that 16 per wave, twice the workgroups for a launch that is
-  // bound by latency rather than by MFMA or HBM.  float32: 64 rows per block.
+// Query rows per wave (16 QB) and split count of a launch (see attention()).
+static int attention_qb(int dtype, int BH, int Mq) {
   const bool mfma = dtype == ATTN_BF16 || dtype == ATTN_F16;
-  const int QB = mfma && Mq > 64 && ceil_div(Mq, 64) * BH >= 512 ? 2 : 1;
-  const int qtiles = ceil_div(Mq, 64 * QB);
+  return mfma && Mq > 64 && ceil_div(Mq, 64) * BH >= 512 ? 2 : 1;
+}
+
+int attention_splits(int dtype, int B, int H, int Mq, int Nk, int max_splits, int* keys_per_split) {
+  const int BH = B * H;
+  const int qtiles = ceil_div(Mq, 64 * attention_qb(dtype, BH, Mq));
   // split the key range (whole 64-key tiles) until every split has about two
   // tiles or the grid reaches two workgroups per CU: each workgroup walks its
   // tiles in sequence and hides only the next tile's load, so long ranges
@@ -419,11 +416,29 @@ hipError_t attention(int dtype, const void* q, const void* kc, const void* vc, i
   // the merge kernel would cost more than the shorter walk saves.
   const int key_tiles = ceil_div(Nk, 64);
   int S = key_tiles <= 10 ? 1 : key_tiles / 2;
-  if (S > ws.max_splits) S = ws.max_splits;
+  if (S > max_splits) S = max_splits;
   if (S > 512 / (qtiles * BH)) S = 512 / (qtiles * BH);
   if (S < 1) S = 1;
-  int kps = ceil_div(key_tiles, S) * 64;
-  S = ceil_div(Nk, kps);
+  const int kps = ceil_div(key_tiles, S) * 64;
+  if (keys_per_split) *keys_per_split = kps;
+  return ceil_div(Nk, kps);           // every split holds at least one key
+}
+
+hipError_t attention(int dtype, const void* q, const void* kc, const void* vc, int B, int H,
+                     int Hkv, int dh, int Mq, int Nk, int cap, const ActOut& out, AttnWs ws,
+                     hipStream_t st) {
+  if (Mq == 0) return hipSuccess;
+  const int BH = B * H;
+  // bfloat16 / float16: 32 query rows per wave (128 per workgroup), which
+  // halves the LDS reads per MFMA, once 64-row tiles alone would give two
+  // workgroups per CU; below that 16 per wave, twice the workgroups for a
+  // launch that is bound by latency rather than by MFMA or HBM.  float32: 64
+  // rows per block.
+  const bool mfma = dtype == ATTN_BF16 || dtype == ATTN_F16;
+  const int QB = attention_qb(dtype, BH, Mq);
+  const int qtiles = ceil_div(Mq, 64 * QB);
+  int kps = 0;
+  const int S = attention_splits(dtype, B, H, Mq, Nk, ws.max_splits, &kps);
   const float scale_log2 = LOG2E / sqrtf((float)dh);
   float* opart = S > 1 ? ws.opart : nullptr;
   if (mfma) {

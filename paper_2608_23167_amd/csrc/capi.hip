@@ -4,6 +4,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
 #include <string>
 #include <utility>
 #include <vector>
@@ -142,6 +143,18 @@ int32_t check_model(const ssm_model* m) {
 }
 
 constexpr int ATTN_MAX_SPLITS = 16;
+
+// Scratch memory of ssm_attention_static: the split-KV partial results,
+// SSM_ATTENTION_STATIC_SCRATCH_BYTES in a file-scope device array, one copy
+// per GPU, held until the process ends.  In host code `scratch` is only a
+// stand-in for the symbol: its device address comes from
+// hipGetSymbolAddress, once per device with that device current, and only
+// that address is handed to kernels.
+__device__ __align__(256) unsigned char scratch[SSM_ATTENTION_STATIC_SCRATCH_BYTES];
+
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[MAX_DEVICES] = {};
 
 // ---- launch profiling: HIP events around each launcher, per tag ----------
 struct ProfRec {
@@ -478,6 +491,59 @@ int32_t ssm_attention(int32_t dtype, int32_t batch, int32_t n_heads, int32_t n_k
   HIP_TRY(attention(dtype == SSM_DT_F16 ? ATTN_F16 : ATTN_BF16, d_q, d_k, d_v, batch, n_heads,
                     n_kv_heads, 128, n_q, n_keys,
                     capacity, out, aws, st));
+  return ok();
+}
+
+// Bytes of split-KV partial results an attention launch of these sizes uses
+// (0 when it does not split the key range).
+static size_t attn_partial_bytes(int dtype, int32_t batch, int32_t n_heads, int32_t n_q,
+                                 int32_t n_keys, int max_splits) {
+  const int S = attention_splits(dtype, batch, n_heads, n_q, n_keys, max_splits, nullptr);
+  if (S <= 1) return 0;
+  const size_t rows = (size_t)S * batch * n_heads * n_q;
+  return align256(rows * 128 * 4) + align256(rows * 2 * 4);
+}
+
+int32_t ssm_attention_static(int32_t dtype, int32_t batch, int32_t n_heads, int32_t n_kv_heads,
+                             int32_t n_q, int32_t n_keys, int32_t capacity, const void* d_q,
+                             const void* d_k, const void* d_v, float* d_out, void* stream) {
+  if (dtype != SSM_DT_BF16 && dtype != SSM_DT_F16)
+    return fail(SSM_E_INVAL, "attention operands must be SSM_DT_BF16 or SSM_DT_F16 (got %d)", dtype);
+  if (batch < 1 || n_heads < 1 || n_kv_heads < 1 || n_q < 0 || n_keys < 1 || capacity < 1)
+    return fail(SSM_E_INVAL, "bad sizes");
+  if (n_heads % n_kv_heads) return fail(SSM_E_SHAPE, "n_heads %d not a multiple of n_kv_heads %d", n_heads, n_kv_heads);
+  if (n_keys > capacity) return fail(SSM_E_CAPACITY, "n_keys %d > capacity %d", n_keys, capacity);
+  if (!d_q || !d_k || !d_v || !d_out) return fail(SSM_E_INVAL, "null device pointer");
+  // the split count of ssm_attention, so both give identical results
+  const int ad = dtype == SSM_DT_F16 ? ATTN_F16 : ATTN_BF16;
+  const int max_splits = attn_max_splits(batch, n_heads, n_q);
+  const size_t need = attn_partial_bytes(ad, batch, n_heads, n_q, n_keys, max_splits);
+  if (need > SSM_ATTENTION_STATIC_SCRATCH_BYTES)
+    return fail(SSM_E_CAPACITY, "split-KV partials need %zu bytes, above the %d-byte static scratch "
+                "(ssm_attention with a workspace has no such limit)", need,
+                SSM_ATTENTION_STATIC_SCRATCH_BYTES);
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev < 0 || dev >= MAX_DEVICES) return fail(SSM_E_UNSUPPORTED, "device %d beyond %d", dev, MAX_DEVICES);
+  void* base = nullptr;
+  {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+      void* p = nullptr;
+      HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+      g_scratch_ptr[dev] = p;
+    }
+    base = g_scratch_ptr[dev];
+  }
+  // partial outputs first, then the (max, sum) pairs, as attn_partial_bytes
+  // counts them; every entry is written by its split before the merge reads
+  // it, so nothing needs clearing between calls
+  const int S = attention_splits(ad, batch, n_heads, n_q, n_keys, max_splits, nullptr);
+  const size_t rows = (size_t)S * batch * n_heads * n_q;
+  const AttnWs aws{(float*)base, (float*)((char*)base + align256(rows * 128 * 4)), max_splits};
+  const ActOut out{d_out, nullptr, n_heads * 128, 0, 1};
+  HIP_TRY(attention(ad, d_q, d_k, d_v, batch, n_heads, n_kv_heads, 128, n_q, n_keys, capacity, out,
+                    aws, (hipStream_t)stream));
   return ok();
 }
 

@@ -231,6 +231,11 @@ struct AttnWs {
 // float16 (the bfloat16 model's q, k, v).  The output is the float32 rows or
 // the bfloat16 operand of the output projection, as `out` says.
 enum { ATTN_F32 = 0, ATTN_BF16 = 1, ATTN_F16 = 2 };
+// Number of key-range splits attention() uses for these sizes (at most
+// max_splits); with more than one, ws receives S * B * H * Mq float32 rows of
+// dh partial outputs and S * B * H * Mq (max, sum) pairs, each written before
+// the merge reads it.  keys_per_split (may be null) receives the split width.
+int attention_splits(int dtype, int B, int H, int Mq, int Nk, int max_splits, int* keys_per_split);
 // out: [B * Mq, H * dh] activation operand of the output projection
 hipError_t attention(int dtype, const void* q, const void* kc, const void* vc, int B, int H,
                      int Hkv, int dh, int Mq, int Nk, int cap, const ActOut& out, AttnWs ws,

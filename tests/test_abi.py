@@ -244,3 +244,22 @@ def test_attention_validation():
     assert lib.ssm_attention(*with_(3, 3)) == L.SSM_E_SHAPE           # 8 heads over 3 KV heads
     assert lib.ssm_attention(*with_(12, n.value - 1)) == L.SSM_E_CAPACITY
     assert lib.ssm_attention(*with_(7, None)) == L.SSM_E_INVAL
+
+
+def test_attention_static_rejects_partials_beyond_its_scratch():
+    """ssm_attention_static checks the split-KV partials of the launch against
+    its static scratch on the host, before it touches the device: 8 heads of
+    4096 query rows over 4096 keys split the key range in two, 65536 partial
+    rows (about 34 MB) against 32 MiB.  The same launch with fewer rows fits."""
+    from paper_2608_23167_amd import _lib as L
+    lib = L.lib()
+    f = C.c_void_p(0x1000)
+    assert lib.ssm_attention_static(L.SSM_DT_F16, 1, 32, 32, 64, 4096, 4096, f, f, f, f, None) \
+        == L.SSM_E_CAPACITY
+    assert b"static scratch" in lib.ssm_last_error()
+    assert lib.ssm_attention_static(L.SSM_DT_F32, 1, 8, 8, 100, 300, 400, f, f, f, f, None) \
+        == L.SSM_E_INVAL
+    assert lib.ssm_attention_static(L.SSM_DT_F16, 1, 8, 3, 100, 300, 400, f, f, f, f, None) \
+        == L.SSM_E_SHAPE
+    assert lib.ssm_attention_static(L.SSM_DT_F16, 1, 8, 8, 100, 401, 400, f, f, f, f, None) \
+        == L.SSM_E_CAPACITY

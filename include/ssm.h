@@ -29,8 +29,20 @@
  *     a message available from ssm_last_error() (thread-local).
  *   - No C++ exception crosses the ABI.  Results are deterministic: no
  *     floating-point reduction depends on scheduling order.
- *   - Batched sequences share prompt length, generation length and block
- *     schedule, hence one position list for the whole batch.
+ *   - Batched sequences share generation length, block size, budgets and
+ *     block schedule.  Their prompts may differ in length: the calls then take
+ *     `pad`, a HOST array [batch] (at most 64 sequences) in which pad[s] is
+ *     how many tokens shorter sequence s's prompt is than the longest one
+ *     (pad = NULL: all prompts equally long).  The batch shares the row
+ *     layout of its longest prompt, and sequence s sits pad[s] positions to
+ *     the left in it: row r is position pos[r] - pad[s] of sequence s, and
+ *     prefix rows whose position falls below zero are padding (embedded as
+ *     [MASK], computed, never read as keys).  This is exact rather than an
+ *     approximation: with a shared generation length each sequence's suffix
+ *     regions (Eq. 1) and retained set R_t are those of the longest prompt
+ *     shifted by pad[s], so pos[r] - pad[s] is sequence s's own position
+ *     list.  Token and prediction-state arrays keep a stride of the longest
+ *     sequence; sequence s uses its first seq_len - pad[s] positions.
  *   - Element types: token ids and positions int32; region tags int8;
  *     probabilities and the residual stream float32; weights and embeddings
  *     in the model's dtype (float32 or bfloat16); the KV cache in float32
@@ -147,16 +159,19 @@ int32_t ssm_select_positions_host(const ssm_select_params* p, int32_t* pos, int8
  * Builds the compacted row list of the sparse input [P; B_t; R_t]: for row r,
  * d_pos[r] is its absolute position (ascending within prefix, block and R_t),
  * d_region[r] its SSM_REGION_* tag, and d_tok_c[s*cap + r] the token id of
- * sequence s at that position (gathered from d_tokens[s*seq_len + pos]).
+ * sequence s at that position (gathered from d_tokens[s*seq_len + pos -
+ * pad[s]]; -1 for padding rows).
  *   d_tokens  [batch, seq_len] int32, seq_len == prompt_len + gen_len
+ *             (prompt_len: the longest prompt when pad is given)
+ *   pad       HOST [batch] or NULL, each in [0, prompt_len]
  *   d_pos     [cap] int32, d_region [cap] int8 (may be NULL), d_tok_c [batch, cap] int32
  * The row counts are returned synchronously (as ssm_select_count).
  * SSM_E_CAPACITY if cap < n_rows.
  */
 int32_t ssm_select_suffix(const ssm_select_params* p, int32_t batch, int32_t seq_len,
-                          const int32_t* d_tokens, int32_t* d_pos, int32_t* d_tok_c,
-                          int8_t* d_region, int32_t cap, int32_t* n_rows, int32_t* n_suffix,
-                          int32_t* first_out_row, void* stream);
+                          const int32_t* pad, const int32_t* d_tokens, int32_t* d_pos,
+                          int32_t* d_tok_c, int8_t* d_region, int32_t cap, int32_t* n_rows,
+                          int32_t* n_suffix, int32_t* first_out_row, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* Model description.                                                       */
@@ -224,10 +239,12 @@ typedef struct ssm_kv_cache {
  *   d_tok_c [batch, tok_stride] int32 (tok_stride >= n_rows: the `cap` of
  *   ssm_select_suffix); d_pos, d_region [n_rows];
  *   d_pred_ids [batch, seq_len, k] int32, d_pred_w [batch, seq_len, k] float32,
- *   d_pred_step [batch, seq_len] int32.
+ *   d_pred_step [batch, seq_len] int32 (indexed by each sequence's own
+ *   position pos[r] - pad[s]; pad HOST [batch] or NULL, each in [0, seq_len]).
+ * Padding rows (position below zero) are E[mask].
  * k in [1, 8]; alpha in [0, 1].
  */
-int32_t ssm_embed_suffix(const ssm_model* m, int32_t batch, int32_t seq_len,
+int32_t ssm_embed_suffix(const ssm_model* m, int32_t batch, int32_t seq_len, const int32_t* pad,
                          const int32_t* d_tok_c, int32_t tok_stride, const int32_t* d_pos,
                          const int8_t* d_region, int32_t n_rows, const int32_t* d_pred_ids,
                          const float* d_pred_w, const int32_t* d_pred_step, int32_t prev_step,
@@ -258,13 +275,17 @@ int32_t ssm_workspace_size(const ssm_model* m, int32_t batch, int32_t max_rows, 
  * and values go to slots [n_cached, n_cached + n_rows), so capacity >=
  * n_cached + n_rows.  Attention of every row reads all n_cached + n_rows keys.
  * d_ws: workspace of ws_bytes >= ssm_workspace_size(batch, n_rows).
+ * pad (HOST [batch] or NULL): sequence s rotates row r at position pos[r] -
+ * pad[s] and its keys start at slot pad[s] (its padding rows and slots are
+ * never attended to); each pad[s] is at most the prefix it pads: n_cached
+ * for SSM_CACHE_READ, first_out_row otherwise (SSM_E_INVAL).
  * k in [1, 8].  The bfloat16 path needs d_model and ffn_dim to be multiples of
  * 256, vocab a multiple of 128 and head_dim == 128; otherwise SSM_E_UNSUPPORTED.
  */
 int32_t ssm_denoise_step(const ssm_model* m, const ssm_kv_cache* cache, int32_t cache_mode,
-                         int32_t n_cached, int32_t batch, const int32_t* d_pos, int32_t n_rows,
-                         const float* d_x, int32_t first_out_row, int32_t k, int32_t* d_argmax,
-                         float* d_conf, int32_t* d_topk_ids, float* d_topk_w,
+                         int32_t n_cached, int32_t batch, const int32_t* pad, const int32_t* d_pos,
+                         int32_t n_rows, const float* d_x, int32_t first_out_row, int32_t k,
+                         int32_t* d_argmax, float* d_conf, int32_t* d_topk_ids, float* d_topk_w,
                          float* d_logits_dbg, float* d_hidden_dbg, void* d_ws, size_t ws_bytes,
                          void* stream);
 
@@ -349,10 +370,12 @@ int32_t ssm_gather_rows(int32_t batch, int32_t src_rows, int32_t width, const vo
  * d_pred_step[s, pos] = step.
  * d_selected (uint8 [batch, block_size], may be NULL) receives the decoded
  * positions, d_masked_left (int32 [batch], may be NULL) the masks left in the block.
+ * pad (HOST [batch] or NULL, each in [0, block_start]): sequence s's block
+ * starts at block_start - pad[s] and its suffix rows are at d_pos_out[i] - pad[s].
  */
-int32_t ssm_unmask(int32_t* d_tokens, int32_t batch, int32_t seq_len, int32_t block_start,
-                   int32_t block_size, int32_t mask_id, int32_t rule, int32_t n_per_step,
-                   float threshold, const int32_t* d_argmax, const float* d_conf,
+int32_t ssm_unmask(int32_t* d_tokens, int32_t batch, int32_t seq_len, const int32_t* pad,
+                   int32_t block_start, int32_t block_size, int32_t mask_id, int32_t rule,
+                   int32_t n_per_step, float threshold, const int32_t* d_argmax, const float* d_conf,
                    const int32_t* d_topk_ids, const float* d_topk_w, int32_t k, int32_t n_out,
                    const int32_t* d_pos_out, int32_t step, int32_t* d_pred_ids, float* d_pred_w,
                    int32_t* d_pred_step, uint8_t* d_selected, int32_t* d_masked_left,
@@ -371,11 +394,14 @@ int32_t ssm_unmask(int32_t* d_tokens, int32_t batch, int32_t seq_len, int32_t bl
  *   d_tokens [batch, seq_len] int32 (in place), d_done [batch] int32, zeroed by
  *   the caller at the start of a generation.
  * The generation can stop once every d_done[s] is 1 (the caller copies
- * d_done to the host to find out).  SSM_E_INVAL for a block outside the
- * sequence, eos_id < 0 or a null pointer.
+ * d_done to the host to find out).  With pad (HOST [batch] or NULL, each in
+ * [0, block_start]) sequence s's block starts pad[s] to the left and its
+ * sequence ends at seq_len - pad[s].  SSM_E_INVAL for a block outside the
+ * sequence, eos_id < 0, a pad out of range or a null pointer.
  */
-int32_t ssm_early_stop(int32_t* d_tokens, int32_t batch, int32_t seq_len, int32_t block_start,
-                       int32_t block_size, int32_t eos_id, int32_t* d_done, void* stream);
+int32_t ssm_early_stop(int32_t* d_tokens, int32_t batch, int32_t seq_len, const int32_t* pad,
+                       int32_t block_start, int32_t block_size, int32_t eos_id, int32_t* d_done,
+                       void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* Launch timing (tracing aid; off by default).                             */

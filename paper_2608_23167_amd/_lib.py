@@ -61,15 +61,16 @@ PI32 = C.POINTER(C.c_int32)
 _SIGS = {
     "ssm_select_count": (I32, [C.POINTER(SelectParams), PI32, PI32, PI32]),
     "ssm_select_positions_host": (I32, [C.POINTER(SelectParams), PI32, C.POINTER(C.c_int8), I32, PI32]),
-    "ssm_select_suffix": (I32, [C.POINTER(SelectParams), I32, I32, P, P, P, P, I32, PI32, PI32, PI32, P]),
-    "ssm_embed_suffix": (I32, [C.POINTER(Model), I32, I32, P, I32, P, P, I32, P, P, P, I32, I32,
-                               C.c_float, P, P]),
+    "ssm_select_suffix": (I32, [C.POINTER(SelectParams), I32, I32, PI32, P, P, P, P, I32, PI32, PI32,
+                                PI32, P]),
+    "ssm_embed_suffix": (I32, [C.POINTER(Model), I32, I32, PI32, P, I32, P, P, I32, P, P, P, I32,
+                               I32, C.c_float, P, P]),
     "ssm_workspace_size": (I32, [C.POINTER(Model), I32, I32, C.POINTER(C.c_size_t)]),
-    "ssm_denoise_step": (I32, [C.POINTER(Model), C.POINTER(KVCache), I32, I32, I32, P, I32, P, I32,
-                               I32, P, P, P, P, P, P, P, C.c_size_t, P]),
-    "ssm_unmask": (I32, [P, I32, I32, I32, I32, I32, I32, I32, C.c_float, P, P, P, P, I32, I32, P,
-                         I32, P, P, P, P, P, P]),
-    "ssm_early_stop": (I32, [P, I32, I32, I32, I32, I32, P, P]),
+    "ssm_denoise_step": (I32, [C.POINTER(Model), C.POINTER(KVCache), I32, I32, I32, PI32, P, I32, P,
+                               I32, I32, P, P, P, P, P, P, P, C.c_size_t, P]),
+    "ssm_unmask": (I32, [P, I32, I32, PI32, I32, I32, I32, I32, I32, C.c_float, P, P, P, P, I32, I32,
+                         P, I32, P, P, P, P, P, P]),
+    "ssm_early_stop": (I32, [P, I32, I32, PI32, I32, I32, I32, P, P]),
     "ssm_attention_workspace_size": (I32, [I32, I32, I32, C.POINTER(C.c_size_t)]),
     "ssm_attention": (I32, [I32, I32, I32, I32, I32, I32, I32, P, P, P, P, P, C.c_size_t, P]),
     "ssm_attention_static": (I32, [I32, I32, I32, I32, I32, I32, I32, P, P, P, P, P]),

@@ -33,6 +33,16 @@ def _ptr(t: Optional[torch.Tensor], dtype=None, name="tensor") -> C.c_void_p:
     return C.c_void_p(t.data_ptr())
 
 
+def _pad(pad, batch: int):
+    """Host int32 array of per-sequence left padding (None: no padding)."""
+    if pad is None:
+        return None
+    a = (C.c_int32 * batch)(*[int(v) for v in pad])
+    if len(pad) != batch:
+        raise ValueError(f"pad has {len(pad)} entries for a batch of {batch}")
+    return a
+
+
 def select_params(prompt_len, gen_len, block_size, block_idx, local_budget, middle_budget,
                   middle_mode, tail_budget, include_prefix, tail_mode=0) -> L.SelectParams:
     return L.SelectParams(prompt_len, gen_len, block_size, block_idx, local_budget, middle_budget,
@@ -58,14 +68,15 @@ def ssm_select_positions_host(p: L.SelectParams) -> Tuple[np.ndarray, np.ndarray
 
 
 def ssm_select_suffix(p: L.SelectParams, tokens: torch.Tensor, pos: torch.Tensor,
-                      tok_c: torch.Tensor, region: Optional[torch.Tensor], stream=None
-                      ) -> Tuple[int, int, int]:
+                      tok_c: torch.Tensor, region: Optional[torch.Tensor], stream=None,
+                      pad=None) -> Tuple[int, int, int]:
     B, seq_len = tokens.shape
     cap = pos.numel()
     if tok_c.shape != (B, cap):
         raise ValueError("tok_c must be [batch, cap]")
     n, s, f = C.c_int32(), C.c_int32(), C.c_int32()
-    rc = lib().ssm_select_suffix(C.byref(p), B, seq_len, _ptr(tokens, torch.int32, "tokens"),
+    rc = lib().ssm_select_suffix(C.byref(p), B, seq_len, _pad(pad, B),
+                                 _ptr(tokens, torch.int32, "tokens"),
                                  _ptr(pos, torch.int32, "pos"), _ptr(tok_c, torch.int32, "tok_c"),
                                  _ptr(region, torch.int8, "region"), cap, C.byref(n), C.byref(s),
                                  C.byref(f), _stream(stream))
@@ -76,9 +87,9 @@ def ssm_select_suffix(p: L.SelectParams, tokens: torch.Tensor, pos: torch.Tensor
 def ssm_embed_suffix(model, tok_c: torch.Tensor, pos: torch.Tensor, region: torch.Tensor,
                      n_rows: int, pred_ids: torch.Tensor, pred_w: torch.Tensor,
                      pred_step: torch.Tensor, prev_step: int, k: int, alpha: float,
-                     x: torch.Tensor, stream=None) -> None:
+                     x: torch.Tensor, stream=None, pad=None) -> None:
     B, seq_len = pred_step.shape
-    rc = lib().ssm_embed_suffix(C.byref(model.c_model), B, seq_len,
+    rc = lib().ssm_embed_suffix(C.byref(model.c_model), B, seq_len, _pad(pad, B),
                                 _ptr(tok_c, torch.int32, "tok_c"), tok_c.shape[1],
                                 _ptr(pos, torch.int32, "pos"), _ptr(region, torch.int8, "region"),
                                 n_rows, _ptr(pred_ids, torch.int32, "pred_ids"),
@@ -100,10 +111,10 @@ def ssm_denoise_step(model, cache, cache_mode: int, n_cached: int, pos: torch.Te
                      argmax: torch.Tensor, conf: torch.Tensor, topk_ids: torch.Tensor,
                      topk_w: torch.Tensor, ws: torch.Tensor,
                      logits: Optional[torch.Tensor] = None, hidden: Optional[torch.Tensor] = None,
-                     stream=None) -> None:
+                     stream=None, pad=None) -> None:
     B = x.shape[0]
     rc = lib().ssm_denoise_step(C.byref(model.c_model), C.byref(cache.c_cache), cache_mode,
-                                n_cached, B, _ptr(pos, torch.int32, "pos"), n_rows,
+                                n_cached, B, _pad(pad, B), _ptr(pos, torch.int32, "pos"), n_rows,
                                 _ptr(x, torch.float32, "x"), first_out_row, k,
                                 _ptr(argmax, torch.int32, "argmax"),
                                 _ptr(conf, torch.float32, "conf"),
@@ -178,9 +189,9 @@ def ssm_unmask(tokens: torch.Tensor, block_start: int, block_size: int, mask_id:
                topk_ids: torch.Tensor, topk_w: torch.Tensor, k: int, n_out: int,
                pos_out: torch.Tensor, step: int, pred_ids: torch.Tensor, pred_w: torch.Tensor,
                pred_step: torch.Tensor, selected: Optional[torch.Tensor] = None,
-               masked_left: Optional[torch.Tensor] = None, stream=None) -> None:
+               masked_left: Optional[torch.Tensor] = None, stream=None, pad=None) -> None:
     B, seq_len = tokens.shape
-    rc = lib().ssm_unmask(_ptr(tokens, torch.int32, "tokens"), B, seq_len, block_start,
+    rc = lib().ssm_unmask(_ptr(tokens, torch.int32, "tokens"), B, seq_len, _pad(pad, B), block_start,
                           block_size, mask_id, rule, n_per_step, float(threshold),
                           _ptr(argmax, torch.int32, "argmax"), _ptr(conf, torch.float32, "conf"),
                           _ptr(topk_ids, torch.int32, "topk_ids"),
@@ -195,12 +206,13 @@ def ssm_unmask(tokens: torch.Tensor, block_start: int, block_size: int, mask_id:
 
 
 def ssm_early_stop(tokens: torch.Tensor, block_start: int, block_size: int, eos_id: int,
-                   done: torch.Tensor, stream=None) -> None:
+                   done: torch.Tensor, stream=None, pad=None) -> None:
     B, seq_len = tokens.shape
     if done.numel() != B:
         raise ValueError("done must hold one int32 per sequence")
-    rc = lib().ssm_early_stop(_ptr(tokens, torch.int32, "tokens"), B, seq_len, block_start,
-                              block_size, eos_id, _ptr(done, torch.int32, "done"), _stream(stream))
+    rc = lib().ssm_early_stop(_ptr(tokens, torch.int32, "tokens"), B, seq_len, _pad(pad, B),
+                              block_start, block_size, eos_id, _ptr(done, torch.int32, "done"),
+                              _stream(stream))
     check(rc, "ssm_early_stop")
 
 

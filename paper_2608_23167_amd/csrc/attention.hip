@@ -86,7 +86,7 @@ template <int QB, typename E>
 __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(
     const E* __restrict__ Q, const E* __restrict__ Kc, const E* __restrict__ Vc,
     int H, int Hkv, int Mq, int Nk, int cap, int keys_per_split, float scale_log2,
-    ActOut O, float* __restrict__ Opart, float* __restrict__ ML, int qtiles, int BH) {
+    ActOut O, float* __restrict__ Opart, float* __restrict__ ML, int qtiles, int BH, Pads pads) {
   typedef AttnOps<E> Ops;
   typedef typename Ops::vec vec;
   constexpr int DH = 128, KT = 64, TBUF = KT * DH;
@@ -98,10 +98,26 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(
   int qt, bh, split;
   attn_tile_of(blockIdx.x, gridDim.x, qtiles, BH, qt, bh, split);
   const int s = bh / H, h = bh % H, kvh = h / (H / Hkv);
-  const int kb = split * keys_per_split, ke = min(Nk, kb + keys_per_split);
-  const int ntile = (ke - kb + KT - 1) / KT;   // >= 1: every split holds a key
+  // a padded sequence's keys start after its padding slots
+  const int kb = pads.of(s) + split * keys_per_split, ke = min(Nk, kb + keys_per_split);
   // query block b of the wave: rows q0 + 16 b .. + 15; this lane's query in it
   const int q0 = (qt * 4 + wave) * 16 * QB;
+  if (kb >= ke) {
+    // a split past the end of a padded sequence's shorter key range: an empty
+    // partial (sum 0), which the merge skips (the host keeps split 0 non-empty)
+    if (Opart != nullptr && g == 0) {
+#pragma unroll
+      for (int b = 0; b < QB; ++b) {
+        const int q = q0 + 16 * b + c16;
+        if (q >= Mq) continue;
+        const size_t row = ((size_t)split * BH + bh) * Mq + q;
+        ML[row * 2] = -INFINITY;
+        ML[row * 2 + 1] = 0.f;
+      }
+    }
+    return;
+  }
+  const int ntile = (ke - kb + KT - 1) / KT;   // >= 1
 
   const E* Qh = Q + (size_t)bh * Mq * DH;
   vec qf[QB][4];
@@ -327,10 +343,10 @@ template <int DH>
 __global__ void __launch_bounds__(64) attn_f32_kernel(
     const float* __restrict__ Q, const float* __restrict__ Kc, const float* __restrict__ Vc,
     int H, int Hkv, int Mq, int Nk, int cap, int keys_per_split, float scale_log2,
-    ActOut O, float* __restrict__ Opart, float* __restrict__ ML) {
+    ActOut O, float* __restrict__ Opart, float* __restrict__ ML, Pads pads) {
   const int bh = blockIdx.y, s = bh / H, h = bh % H, kvh = h / (H / Hkv);
   const int split = blockIdx.z;
-  const int kb = split * keys_per_split, ke = min(Nk, kb + keys_per_split);
+  const int kb = pads.of(s) + split * keys_per_split, ke = min(Nk, kb + keys_per_split);
   const int q = blockIdx.x * 64 + threadIdx.x;
   if (q >= Mq) return;
   const float* qp = Q + ((size_t)bh * Mq + q) * DH;
@@ -426,7 +442,7 @@ int attention_splits(int dtype, int B, int H, int Mq, int Nk, int max_splits, in
 
 hipError_t attention(int dtype, const void* q, const void* kc, const void* vc, int B, int H,
                      int Hkv, int dh, int Mq, int Nk, int cap, const ActOut& out, AttnWs ws,
-                     hipStream_t st) {
+                     const Pads& pads, hipStream_t st) {
   if (Mq == 0) return hipSuccess;
   const int BH = B * H;
   // bfloat16 / float16: 32 query rows per wave (128 per workgroup), which
@@ -447,18 +463,18 @@ hipError_t attention(int dtype, const void* q, const void* kc, const void* vc, i
       const f16_t *qh = (const f16_t*)q, *kh = (const f16_t*)kc, *vh = (const f16_t*)vc;
       if (QB == 2)
         launch(attn_bf16_kernel<2, f16_t>, grid, dim3(256), 0, st, qh, kh, vh, H, Hkv, Mq, Nk, cap,
-               kps, scale_log2, out, opart, ws.ml, qtiles, BH);
+               kps, scale_log2, out, opart, ws.ml, qtiles, BH, pads);
       else
         launch(attn_bf16_kernel<1, f16_t>, grid, dim3(256), 0, st, qh, kh, vh, H, Hkv, Mq, Nk, cap,
-               kps, scale_log2, out, opart, ws.ml, qtiles, BH);
+               kps, scale_log2, out, opart, ws.ml, qtiles, BH, pads);
     } else {
       const bf16_t *qh = (const bf16_t*)q, *kh = (const bf16_t*)kc, *vh = (const bf16_t*)vc;
       if (QB == 2)
         launch(attn_bf16_kernel<2, bf16_t>, grid, dim3(256), 0, st, qh, kh, vh, H, Hkv, Mq, Nk,
-               cap, kps, scale_log2, out, opart, ws.ml, qtiles, BH);
+               cap, kps, scale_log2, out, opart, ws.ml, qtiles, BH, pads);
       else
         launch(attn_bf16_kernel<1, bf16_t>, grid, dim3(256), 0, st, qh, kh, vh, H, Hkv, Mq, Nk,
-               cap, kps, scale_log2, out, opart, ws.ml, qtiles, BH);
+               cap, kps, scale_log2, out, opart, ws.ml, qtiles, BH, pads);
     }
   } else {
     const dim3 grid(qtiles, BH, S);
@@ -468,13 +484,13 @@ hipError_t attention(int dtype, const void* q, const void* kc, const void* vc, i
     const ActOut& of = out;
     if (dh == 32)
       launch(attn_f32_kernel<32>, grid, dim3(64), 0, st, qf, kf, vf, H, Hkv, Mq, Nk,
-                         cap, kps, scale_log2, of, opart, ws.ml);
+                         cap, kps, scale_log2, of, opart, ws.ml, pads);
     else if (dh == 64)
       launch(attn_f32_kernel<64>, grid, dim3(64), 0, st, qf, kf, vf, H, Hkv, Mq, Nk,
-                         cap, kps, scale_log2, of, opart, ws.ml);
+                         cap, kps, scale_log2, of, opart, ws.ml, pads);
     else
       launch(attn_f32_kernel<128>, grid, dim3(64), 0, st, qf, kf, vf, H, Hkv, Mq, Nk,
-                         cap, kps, scale_log2, of, opart, ws.ml);
+                         cap, kps, scale_log2, of, opart, ws.ml, pads);
   }
   if (S > 1) {
     const dim3 mgrid(ceil_div(BH * Mq * (dh / 8), 256));

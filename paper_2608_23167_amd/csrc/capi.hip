@@ -142,6 +142,22 @@ int32_t check_model(const ssm_model* m) {
   return SSM_OK;
 }
 
+// Host array of per-sequence left padding (null: none) -> the kernels' Pads,
+// each entry in [0, max_pad].
+int32_t pads_of(const int32_t* pad, int batch, int max_pad, Pads& P) {
+  memset(&P, 0, sizeof(P));
+  if (!pad) return SSM_OK;
+  if (batch > MAX_PAD_BATCH)
+    return fail(SSM_E_UNSUPPORTED, "padded batches hold at most %d sequences (got %d)", MAX_PAD_BATCH, batch);
+  for (int s = 0; s < batch; ++s) {
+    if (pad[s] < 0 || pad[s] > max_pad)
+      return fail(SSM_E_INVAL, "pad[%d] = %d not in [0, %d]", s, pad[s], max_pad);
+    P.v[s] = pad[s];
+    P.any |= pad[s] != 0;
+  }
+  return SSM_OK;
+}
+
 constexpr int ATTN_MAX_SPLITS = 16;
 
 // Scratch memory of ssm_attention_static: the split-KV partial results,
@@ -252,7 +268,7 @@ WsLayout ws_layout(const ssm_model* m, int batch, int max_rows) {
   w.attn_lo = take(Mp * H * dh * lo_es);
   w.act = take(Mp * F * es);
   w.act_lo = take(Mp * F * lo_es);
-  w.rope = take((size_t)max_rows * (dh / 2) * 8);
+  w.rope = take((size_t)batch * max_rows * (dh / 2) * 8);   // one table per sequence when padded
   w.opart = take((size_t)ATTN_MAX_SPLITS * Mt * H * dh * 4);
   w.ml = take((size_t)ATTN_MAX_SPLITS * Mt * H * 2 * 4);
   w.part_floats = gemm_split_ws_floats((int)Mt, (int)maxn);
@@ -298,13 +314,15 @@ int32_t ssm_select_positions_host(const ssm_select_params* p, int32_t* pos, int8
 }
 
 int32_t ssm_select_suffix(const ssm_select_params* p, int32_t batch, int32_t seq_len,
-                          const int32_t* d_tokens, int32_t* d_pos, int32_t* d_tok_c,
-                          int8_t* d_region, int32_t cap, int32_t* n_rows, int32_t* n_suffix,
-                          int32_t* first_out_row, void* stream) {
+                          const int32_t* pad, const int32_t* d_tokens, int32_t* d_pos,
+                          int32_t* d_tok_c, int8_t* d_region, int32_t cap, int32_t* n_rows,
+                          int32_t* n_suffix, int32_t* first_out_row, void* stream) {
   SelectLayout L;
   int32_t rc = layout_of(p, L);
   if (rc) return rc;
   if (batch < 1) return fail(SSM_E_INVAL, "batch %d < 1", batch);
+  Pads pads;
+  if ((rc = pads_of(pad, batch, p->prompt_len, pads))) return rc;
   if (seq_len != p->prompt_len + p->gen_len)
     return fail(SSM_E_INVAL, "seq_len %d != prompt_len + gen_len", seq_len);
   if (!d_tokens || !d_pos || !d_tok_c) return fail(SSM_E_INVAL, "null device pointer");
@@ -313,11 +331,11 @@ int32_t ssm_select_suffix(const ssm_select_params* p, int32_t batch, int32_t seq
   if (n_suffix) *n_suffix = L.n_suffix;
   if (first_out_row) *first_out_row = L.n_prefix;
   hipStream_t st = (hipStream_t)stream;
-  PROF_TRY("select", launch_select(L, batch, seq_len, d_tokens, d_pos, d_tok_c, d_region, cap, st));
+  PROF_TRY("select", launch_select(L, batch, seq_len, d_tokens, d_pos, d_tok_c, d_region, cap, pads, st));
   return ok();
 }
 
-int32_t ssm_embed_suffix(const ssm_model* m, int32_t batch, int32_t seq_len,
+int32_t ssm_embed_suffix(const ssm_model* m, int32_t batch, int32_t seq_len, const int32_t* pad,
                          const int32_t* d_tok_c, int32_t tok_stride, const int32_t* d_pos,
                          const int8_t* d_region, int32_t n_rows, const int32_t* d_pred_ids,
                          const float* d_pred_w, const int32_t* d_pred_step, int32_t prev_step,
@@ -332,10 +350,13 @@ int32_t ssm_embed_suffix(const ssm_model* m, int32_t batch, int32_t seq_len,
   if (!(alpha >= 0.f && alpha <= 1.f)) return fail(SSM_E_INVAL, "alpha not in [0, 1]");
   if (!d_tok_c || !d_pos || !d_region || !d_pred_ids || !d_pred_w || !d_pred_step || !d_x)
     return fail(SSM_E_INVAL, "null device pointer");
+  Pads pads;
+  int32_t rc = pads_of(pad, batch, seq_len, pads);
+  if (rc) return rc;
   hipStream_t st = (hipStream_t)stream;
   PROF_TRY("embed", launch_embed(m->dtype, m->tok_emb, m->d_model, m->vocab, m->mask_id, batch,
                                  seq_len, d_tok_c, tok_stride, d_pos, d_region, n_rows, d_pred_ids,
-                                 d_pred_w, d_pred_step, prev_step, k, alpha, d_x, st));
+                                 d_pred_w, d_pred_step, prev_step, k, alpha, d_x, pads, st));
   return ok();
 }
 
@@ -348,9 +369,9 @@ int32_t ssm_workspace_size(const ssm_model* m, int32_t batch, int32_t max_rows, 
 }
 
 int32_t ssm_denoise_step(const ssm_model* m, const ssm_kv_cache* cache, int32_t cache_mode,
-                         int32_t n_cached, int32_t batch, const int32_t* d_pos, int32_t n_rows,
-                         const float* d_x, int32_t first_out_row, int32_t k, int32_t* d_argmax,
-                         float* d_conf, int32_t* d_topk_ids, float* d_topk_w,
+                         int32_t n_cached, int32_t batch, const int32_t* pad, const int32_t* d_pos,
+                         int32_t n_rows, const float* d_x, int32_t first_out_row, int32_t k,
+                         int32_t* d_argmax, float* d_conf, int32_t* d_topk_ids, float* d_topk_w,
                          float* d_logits_dbg, float* d_hidden_dbg, void* d_ws, size_t ws_bytes,
                          void* stream) {
   int32_t rc = check_model(m);
@@ -373,6 +394,10 @@ int32_t ssm_denoise_step(const ssm_model* m, const ssm_kv_cache* cache, int32_t 
     return fail(SSM_E_CAPACITY, "cache capacity %d < n_cached %d + n_rows %d", cache->capacity, n_cached, n_rows);
   const WsLayout w = ws_layout(m, batch, n_rows);
   if (ws_bytes < w.total) return fail(SSM_E_CAPACITY, "workspace %zu < %zu bytes", ws_bytes, w.total);
+  // padding lies in the prefix: the cached slots, or the prefix rows
+  Pads pads;
+  if ((rc = pads_of(pad, batch, cache_mode == SSM_CACHE_READ ? n_cached : first_out_row, pads)))
+    return rc;
 
   hipStream_t st = (hipStream_t)stream;
   const int dt = m->dtype;
@@ -402,7 +427,7 @@ int32_t ssm_denoise_step(const ssm_model* m, const ssm_kv_cache* cache, int32_t 
   float* logits = d_logits_dbg ? d_logits_dbg : (float*)(ws + w.logits);
   const size_t layer_kv = (size_t)batch * Hkv * cache->capacity * dh * es;
 
-  PROF_TRY("rope_table", launch_rope_table(d_pos, n_rows, dh, m->rope_base, rope, st));
+  PROF_TRY("rope_table", launch_rope_table(d_pos, n_rows, dh, m->rope_base, rope, batch, pads, st));
   HIP_TRY(hipMemcpyAsync(resid, d_x, (size_t)Mt * d * 4, hipMemcpyDeviceToDevice, st));
   // the attention norm of layer 0 runs alone; every later norm follows the
   // residual projection before it (fused with its split-K completion)
@@ -421,11 +446,11 @@ int32_t ssm_denoise_step(const ssm_model* m, const ssm_kv_cache* cache, int32_t 
     char* kc = (char*)cache->k + l * layer_kv;
     char* vc = (char*)cache->v + l * layer_kv;
     // attention block (its input norm is in xn)
-    QKVOut qo{qb, kc, vc, cache->capacity, n_cached, n_rows, rope};
+    QKVOut qo{qb, kc, vc, cache->capacity, n_cached, n_rows, rope, pads.any};
     PROF_TRY("gemm_qkv", gemm_qkv(dt, xn_in, Mt, d, y.wq, y.wk, y.wv, H, Hkv, dh, qo, sws, st));
     PROF_TRY("attention", attention(dt == SSM_DT_BF16 ? ATTN_F16 : ATTN_F32, qb, kc, vc, batch, H,
-                                    Hkv, dh, n_rows, Nk,
-                                    cache->capacity, attn_out, aws, st));
+                                    Hkv, dh, n_rows, Nk, cache->capacity, attn_out, aws, pads,
+                                    st));
     const NormTo ffn_norm{y.ffn_norm, m->rms_eps, xn_out};
     PROF_TRY("gemm_o", gemm_resid(dt, "o", attn_in, Mt, H * dh, y.wo, d, resid, sws, st, &ffn_norm));
     // feed-forward block
@@ -489,8 +514,7 @@ int32_t ssm_attention(int32_t dtype, int32_t batch, int32_t n_heads, int32_t n_k
   const ActOut out{d_out, nullptr, n_heads * 128, 0, 1};
   hipStream_t st = (hipStream_t)stream;
   HIP_TRY(attention(dtype == SSM_DT_F16 ? ATTN_F16 : ATTN_BF16, d_q, d_k, d_v, batch, n_heads,
-                    n_kv_heads, 128, n_q, n_keys,
-                    capacity, out, aws, st));
+                    n_kv_heads, 128, n_q, n_keys, capacity, out, aws, Pads{}, st));
   return ok();
 }
 
@@ -543,7 +567,7 @@ int32_t ssm_attention_static(int32_t dtype, int32_t batch, int32_t n_heads, int3
   const AttnWs aws{(float*)base, (float*)((char*)base + align256(rows * 128 * 4)), max_splits};
   const ActOut out{d_out, nullptr, n_heads * 128, 0, 1};
   HIP_TRY(attention(ad, d_q, d_k, d_v, batch, n_heads, n_kv_heads, 128, n_q, n_keys, capacity, out,
-                    aws, (hipStream_t)stream));
+                    aws, Pads{}, (hipStream_t)stream));
   return ok();
 }
 
@@ -557,9 +581,9 @@ int32_t ssm_gather_rows(int32_t batch, int32_t src_rows, int32_t width, const vo
   return ok();
 }
 
-int32_t ssm_unmask(int32_t* d_tokens, int32_t batch, int32_t seq_len, int32_t block_start,
-                   int32_t block_size, int32_t mask_id, int32_t rule, int32_t n_per_step,
-                   float threshold, const int32_t* d_argmax, const float* d_conf,
+int32_t ssm_unmask(int32_t* d_tokens, int32_t batch, int32_t seq_len, const int32_t* pad,
+                   int32_t block_start, int32_t block_size, int32_t mask_id, int32_t rule,
+                   int32_t n_per_step, float threshold, const int32_t* d_argmax, const float* d_conf,
                    const int32_t* d_topk_ids, const float* d_topk_w, int32_t k, int32_t n_out,
                    const int32_t* d_pos_out, int32_t step, int32_t* d_pred_ids, float* d_pred_w,
                    int32_t* d_pred_step, uint8_t* d_selected, int32_t* d_masked_left,
@@ -577,24 +601,31 @@ int32_t ssm_unmask(int32_t* d_tokens, int32_t batch, int32_t seq_len, int32_t bl
   if (!d_tokens || !d_argmax || !d_conf || !d_topk_ids || !d_topk_w) return fail(SSM_E_INVAL, "null device pointer");
   if (n_out > block_size && (!d_pos_out || !d_pred_ids || !d_pred_w || !d_pred_step))
     return fail(SSM_E_INVAL, "null prediction-state pointer");
+  Pads pads;
+  int32_t rc = pads_of(pad, batch, block_start, pads);
+  if (rc) return rc;
   hipStream_t st = (hipStream_t)stream;
   PROF_TRY("unmask", launch_unmask(d_tokens, batch, seq_len, block_start, block_size, mask_id,
                                    rule, n_per_step, threshold, d_argmax, d_conf, d_topk_ids,
                                    d_topk_w, k, n_out, d_pos_out, step, d_pred_ids, d_pred_w,
-                                   d_pred_step, d_selected, d_masked_left, st));
+                                   d_pred_step, d_selected, d_masked_left, pads, st));
   return ok();
 }
 
-int32_t ssm_early_stop(int32_t* d_tokens, int32_t batch, int32_t seq_len, int32_t block_start,
-                       int32_t block_size, int32_t eos_id, int32_t* d_done, void* stream) {
+int32_t ssm_early_stop(int32_t* d_tokens, int32_t batch, int32_t seq_len, const int32_t* pad,
+                       int32_t block_start, int32_t block_size, int32_t eos_id, int32_t* d_done,
+                       void* stream) {
   if (batch < 1 || seq_len < 1) return fail(SSM_E_INVAL, "bad batch / seq_len");
   if (block_size < 1 || block_start < 0 || block_start + block_size > seq_len)
     return fail(SSM_E_INVAL, "block [%d, %d) outside the sequence", block_start, block_start + block_size);
   if (eos_id < 0) return fail(SSM_E_INVAL, "eos_id %d < 0", eos_id);
   if (!d_tokens || !d_done) return fail(SSM_E_INVAL, "null device pointer");
+  Pads pads;
+  int32_t rc = pads_of(pad, batch, block_start, pads);
+  if (rc) return rc;
   hipStream_t st = (hipStream_t)stream;
   PROF_TRY("early_stop", launch_early_stop(d_tokens, batch, seq_len, block_start, block_size,
-                                           eos_id, d_done, st));
+                                           eos_id, d_done, pads, st));
   return ok();
 }
 

@@ -79,6 +79,7 @@ struct PolQKV {
   TO *q, *kc, *vc;
   int cap, n_cached, n_rows;
   const float2* rope;
+  int rope_per_seq;    // 1: RoPE table [B, n_rows, d_h / 2] (padded batch), 0: [n_rows, d_h / 2]
 
   __device__ __forceinline__ const T* head_rows(int head) const {
     if (head < H) return wq + (size_t)head * dh * ldb;
@@ -103,7 +104,7 @@ struct PolQKV {
     const int half = dh / 2, j = t * (BN / 2) + c, head = j / half, i = j - head * half;
     const int s = m / n_rows, row = m % n_rows;
     if (head < H + Hkv) {
-      const float2 cs = rope[(size_t)row * half + i];
+      const float2 cs = rope[((size_t)(rope_per_seq ? s : 0) * n_rows + row) * half + i];
       const float a = vlo * cs.x - vhi * cs.y;
       const float b = vhi * cs.x + vlo * cs.y;
       vlo = a;
@@ -128,7 +129,7 @@ struct PolQKV {
       b[e] = vhi[e];
     }
     if (head < H + Hkv) {
-      const float2* cs = rope + (size_t)row * half + i0;
+      const float2* cs = rope + ((size_t)(rope_per_seq ? s : 0) * n_rows + row) * half + i0;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const float2 r = cs[e];
@@ -1131,12 +1132,13 @@ hipError_t gemm_qkv(int dtype, const ActIn& a, int M, int d, const void* wq, con
   const int N = (H + 2 * Hkv) * dh;
   if (dtype == 0) {
     PolQKV<float> p{(const float*)wq, (const float*)wk, (const float*)wv, d, H, Hkv, dh,
-                    (float*)o.q, (float*)o.kc, (float*)o.vc, o.cap, o.n_cached, o.n_rows, o.rope};
+                    (float*)o.q, (float*)o.kc, (float*)o.vc, o.cap, o.n_cached, o.n_rows, o.rope,
+                    o.rope_per_seq};
     return run_f32(p, a, M, d, N, ws, st);
   }
   PolQKV<bf16_t, f16_t> p{(const bf16_t*)wq, (const bf16_t*)wk, (const bf16_t*)wv, d, H, Hkv, dh,
                           (f16_t*)o.q, (f16_t*)o.kc, (f16_t*)o.vc, o.cap, o.n_cached,
-                          o.n_rows, o.rope};
+                          o.n_rows, o.rope, o.rope_per_seq};
   return run_bf16("qkv", p, a, M, d, N, default_cfg("qkv", M, a.lo != nullptr), ws, st, qkv_bn);
 }
 

@@ -32,6 +32,22 @@ inline void launch(void (*kernel)(KArgs...), dim3 grid, dim3 block, uint32_t shm
   if (timed) hipEventRecord(b, st);
 }
 
+// Left padding of each sequence of a batch whose prompts differ in length.
+// The batch shares one row layout, that of its longest prompt; sequence s,
+// whose prompt is pad[s] tokens shorter, sits pad[s] positions to the left
+// in it: row r of the layout is position pos[r] - pad[s] of that sequence,
+// and rows whose position falls below zero are padding (embedded as [MASK],
+// never read as keys).  The retained suffix of every sequence is that of the
+// longest prompt shifted by pad[s] (its suffix regions are measured from its
+// own block), so one position list serves the whole batch.  Passed to the
+// kernels by value; `any` = 0 for a batch without padding.
+constexpr int MAX_PAD_BATCH = 64;
+struct Pads {
+  int32_t v[MAX_PAD_BATCH];
+  int32_t any;
+  __host__ __device__ __forceinline__ int of(int s) const { return any ? v[s] : 0; }
+};
+
 // Closed-form layout of the compacted rows of one step (Section 3.2, Eq. 1-5).
 struct SelectLayout {
   int n_prefix;      // prefix rows included (0 on a cached step)
@@ -79,7 +95,8 @@ __host__ __device__ inline void row_position(const SelectLayout& L, int r, int& 
 }
 
 hipError_t launch_select(const SelectLayout& L, int batch, int seq_len, const int32_t* tokens,
-                         int32_t* pos, int32_t* tok_c, int8_t* region, int cap, hipStream_t st);
+                         int32_t* pos, int32_t* tok_c, int8_t* region, int cap, const Pads& pads,
+                         hipStream_t st);
 
 // out[s, i, :] = src[s, pos[i], :] for bfloat16 rows of `width` elements.
 hipError_t launch_gather_rows(int batch, int src_rows, int width, const bf16_t* src,
@@ -89,11 +106,13 @@ hipError_t launch_embed(int dtype, const void* E, int d, int vocab, int mask_id,
                         int seq_len, const int32_t* tok_c, int tok_stride, const int32_t* pos,
                         const int8_t* region, int n_rows, const int32_t* pred_ids,
                         const float* pred_w, const int32_t* pred_step, int prev_step, int k,
-                        float alpha, float* x, hipStream_t st);
+                        float alpha, float* x, const Pads& pads, hipStream_t st);
 
-// cos/sin of pos[r] * base^(-2i/dh) computed in float64, stored as float2.
+// cos/sin of pos[r] * base^(-2i/dh) computed in float64, stored as float2
+// [n_rows, dh / 2]; with padding, one table per sequence ([batch, n_rows,
+// dh / 2]) at positions pos[r] - pad[s] (padding rows at position 0).
 hipError_t launch_rope_table(const int32_t* pos, int n_rows, int dh, float base, float2* tab,
-                             hipStream_t st);
+                             int batch, const Pads& pads, hipStream_t st);
 
 // Per-row statistics of float32 logits [rows, ldl]: argmax, max probability,
 // top-k ids and their renormalised weights, [MASK] excluded.
@@ -108,6 +127,7 @@ struct QKVOut {
   void* vc;
   int cap, n_cached, n_rows;
   const float2* rope;
+  int rope_per_seq;  // 1: one RoPE table per sequence (padded batch)
 };
 
 // Workspace for split-K partial sums, float32.
@@ -237,9 +257,10 @@ enum { ATTN_F32 = 0, ATTN_BF16 = 1, ATTN_F16 = 2 };
 // the merge reads it.  keys_per_split (may be null) receives the split width.
 int attention_splits(int dtype, int B, int H, int Mq, int Nk, int max_splits, int* keys_per_split);
 // out: [B * Mq, H * dh] activation operand of the output projection
+// Sequence s reads keys [pads.of(s), Nk): its first pads.of(s) slots are padding.
 hipError_t attention(int dtype, const void* q, const void* kc, const void* vc, int B, int H,
                      int Hkv, int dh, int Mq, int Nk, int cap, const ActOut& out, AttnWs ws,
-                     hipStream_t st);
+                     const Pads& pads, hipStream_t st);
 
 // ---- unmasking ------------------------------------------------------------
 hipError_t launch_unmask(int32_t* tokens, int batch, int seq_len, int block_start, int b,
@@ -247,8 +268,8 @@ hipError_t launch_unmask(int32_t* tokens, int batch, int seq_len, int block_star
                          const int32_t* argmax, const float* conf, const int32_t* topk_ids,
                          const float* topk_w, int k, int n_out, const int32_t* pos_out, int step,
                          int32_t* pred_ids, float* pred_w, int32_t* pred_step, uint8_t* selected,
-                         int32_t* masked_left, hipStream_t st);
+                         int32_t* masked_left, const Pads& pads, hipStream_t st);
 hipError_t launch_early_stop(int32_t* tokens, int batch, int seq_len, int block_start, int b,
-                             int eos_id, int32_t* done, hipStream_t st);
+                             int eos_id, int32_t* done, const Pads& pads, hipStream_t st);
 
 }  // namespace ssm

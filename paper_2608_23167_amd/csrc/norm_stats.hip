@@ -115,22 +115,25 @@ hipError_t launch_norm(int dtype, const float* x, int d, const void* g, float ep
 }
 
 // ---- RoPE table (rotate-half form), float64 arithmetic -------------------
+// Table t (blockIdx.y) holds the angles of sequence t's positions pos[r] -
+// pad[t]; padding rows (negative positions) take position 0.
 __global__ void rope_table_kernel(const int32_t* __restrict__ pos, int n_rows, int half, int dh,
-                                  double base, float2* __restrict__ tab) {
+                                  double base, float2* __restrict__ tab, Pads pads) {
   const int idx = blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= n_rows * half) return;
-  const int r = idx / half, i = idx % half;
+  const int r = idx / half, i = idx % half, t = blockIdx.y;
+  const int p = pos[r] - pads.of(t);
   const double inv_freq = 1.0 / pow(base, (2.0 * i) / (double)dh);
-  const double a = (double)pos[r] * inv_freq;
-  tab[idx] = make_float2((float)cos(a), (float)sin(a));
+  const double a = (double)(p < 0 ? 0 : p) * inv_freq;
+  tab[(size_t)t * n_rows * half + idx] = make_float2((float)cos(a), (float)sin(a));
 }
 
 hipError_t launch_rope_table(const int32_t* pos, int n_rows, int dh, float base, float2* tab,
-                             hipStream_t st) {
+                             int batch, const Pads& pads, hipStream_t st) {
   const int half = dh / 2, n = n_rows * half;
   if (n == 0) return hipSuccess;
-  launch(rope_table_kernel, dim3(ceil_div(n, 256)), dim3(256), 0, st, pos, n_rows,
-                     half, dh, (double)base, tab);
+  launch(rope_table_kernel, dim3(ceil_div(n, 256), pads.any ? batch : 1), dim3(256), 0, st, pos,
+         n_rows, half, dh, (double)base, tab, pads);
   return hipGetLastError();
 }
 

@@ -4,10 +4,12 @@
 
 namespace ssm {
 
+// Row r of sequence s gathers the token at its own position pos[r] - pad[s]
+// (-1 for padding rows, whose position is negative).
 __global__ void __launch_bounds__(256) select_kernel(SelectLayout L, const int32_t* __restrict__ tokens,
                                                      int seq_len, int32_t* __restrict__ pos,
                                                      int32_t* __restrict__ tok_c,
-                                                     int8_t* __restrict__ region, int cap) {
+                                                     int8_t* __restrict__ region, int cap, Pads pads) {
   const int r = blockIdx.x * blockDim.x + threadIdx.x;
   if (r >= L.n_rows) return;
   int p, g;
@@ -17,36 +19,40 @@ __global__ void __launch_bounds__(256) select_kernel(SelectLayout L, const int32
     pos[r] = p;
     if (region) region[r] = (int8_t)g;
   }
-  tok_c[(size_t)s * cap + r] = (p >= 0 && p < seq_len) ? tokens[(size_t)s * seq_len + p] : -1;
+  const int q = p - pads.of(s);
+  tok_c[(size_t)s * cap + r] = (q >= 0 && q < seq_len) ? tokens[(size_t)s * seq_len + q] : -1;
 }
 
 hipError_t launch_select(const SelectLayout& L, int batch, int seq_len, const int32_t* tokens,
-                         int32_t* pos, int32_t* tok_c, int8_t* region, int cap, hipStream_t st) {
+                         int32_t* pos, int32_t* tok_c, int8_t* region, int cap, const Pads& pads,
+                         hipStream_t st) {
   if (L.n_rows == 0) return hipSuccess;
   dim3 grid(ceil_div(L.n_rows, 256), batch);
   launch(select_kernel, grid, dim3(256), 0, st, L, tokens, seq_len, pos, tok_c,
-                     region, cap);
+                     region, cap, pads);
   return hipGetLastError();
 }
 
 // One workgroup per (row, sequence).  An out-of-range id or position makes
-// the row NaN instead of reading outside the tables.
+// the row NaN instead of reading outside the tables; a padding row (its
+// position pos[r] - pad[s] below zero) is the [MASK] embedding.
 template <typename T>
 __global__ void __launch_bounds__(256) embed_kernel(
     const T* __restrict__ E, int d, int vocab, int mask_id, int seq_len,
     const int32_t* __restrict__ tok_c, int tok_stride, const int32_t* __restrict__ pos,
     const int8_t* __restrict__ region, int n_rows, const int32_t* __restrict__ pred_ids,
     const float* __restrict__ pred_w, const int32_t* __restrict__ pred_step, int prev_step, int k,
-    float alpha, float* __restrict__ x) {
+    float alpha, float* __restrict__ x, Pads pads) {
   const int r = blockIdx.x, s = blockIdx.y;
   float* out = x + ((size_t)s * n_rows + r) * d;
-  const int p = pos[r];
+  const int p = pos[r] - pads.of(s);
+  const bool pad = pos[r] >= 0 && p < 0;
   const bool pos_ok = p >= 0 && p < seq_len;
   const size_t sp = (size_t)s * seq_len + (pos_ok ? p : 0);
   const bool soft = pos_ok && region[r] >= 2 && prev_step >= 0 && pred_step[sp] == prev_step;
   if (!soft) {
-    const int tok = tok_c[(size_t)s * tok_stride + r];
-    const bool ok = pos_ok && tok >= 0 && tok < vocab;
+    const int tok = pad ? mask_id : tok_c[(size_t)s * tok_stride + r];
+    const bool ok = (pos_ok || pad) && tok >= 0 && tok < vocab;
     const T* e = E + (size_t)(ok ? tok : 0) * d;
     for (int c = threadIdx.x; c < d; c += blockDim.x) out[c] = ok ? ldf(e + c) : __builtin_nanf("");
     return;
@@ -99,17 +105,18 @@ __global__ void __launch_bounds__(256) embed8_kernel(
     const int32_t* __restrict__ tok_c, int tok_stride, const int32_t* __restrict__ pos,
     const int8_t* __restrict__ region, int n_rows, const int32_t* __restrict__ pred_ids,
     const float* __restrict__ pred_w, const int32_t* __restrict__ pred_step, int prev_step, int k,
-    float alpha, float* __restrict__ x) {
+    float alpha, float* __restrict__ x, Pads pads) {
   const int r = blockIdx.x, s = blockIdx.y, d8 = d >> 3;
   float* out = x + ((size_t)s * n_rows + r) * d;
-  const int p = pos[r];
+  const int p = pos[r] - pads.of(s);
+  const bool pad = pos[r] >= 0 && p < 0;
   const bool pos_ok = p >= 0 && p < seq_len;
   const size_t sp = (size_t)s * seq_len + (pos_ok ? p : 0);
   const bool soft = pos_ok && region[r] >= 2 && prev_step >= 0 && pred_step[sp] == prev_step;
   const float qnan = __builtin_nanf("");
   if (!soft) {
-    const int tok = tok_c[(size_t)s * tok_stride + r];
-    const bool ok = pos_ok && tok >= 0 && tok < vocab;
+    const int tok = pad ? mask_id : tok_c[(size_t)s * tok_stride + r];
+    const bool ok = (pos_ok || pad) && tok >= 0 && tok < vocab;
     const T* e = E + (size_t)(ok ? tok : 0) * d;
     for (int c = threadIdx.x; c < d8; c += blockDim.x) {
       float v[8];
@@ -161,26 +168,26 @@ hipError_t launch_embed(int dtype, const void* E, int d, int vocab, int mask_id,
                         int seq_len, const int32_t* tok_c, int tok_stride, const int32_t* pos,
                         const int8_t* region, int n_rows, const int32_t* pred_ids,
                         const float* pred_w, const int32_t* pred_step, int prev_step, int k,
-                        float alpha, float* x, hipStream_t st) {
+                        float alpha, float* x, const Pads& pads, hipStream_t st) {
   if (n_rows == 0) return hipSuccess;
   dim3 grid(n_rows, batch);
   const bool vec = d % 8 == 0 && ((uintptr_t)E & 15) == 0 && ((uintptr_t)x & 15) == 0;
   if (vec && dtype == 0)
     launch(embed8_kernel<float>, grid, dim3(256), 0, st, (const float*)E, d, vocab, mask_id,
            seq_len, tok_c, tok_stride, pos, region, n_rows, pred_ids, pred_w, pred_step,
-           prev_step, k, alpha, x);
+           prev_step, k, alpha, x, pads);
   else if (vec)
     launch(embed8_kernel<bf16_t>, grid, dim3(256), 0, st, (const bf16_t*)E, d, vocab, mask_id,
            seq_len, tok_c, tok_stride, pos, region, n_rows, pred_ids, pred_w, pred_step,
-           prev_step, k, alpha, x);
+           prev_step, k, alpha, x, pads);
   else if (dtype == 0)
     launch(embed_kernel<float>, grid, dim3(256), 0, st, (const float*)E, d, vocab,
                        mask_id, seq_len, tok_c, tok_stride, pos, region, n_rows, pred_ids, pred_w,
-                       pred_step, prev_step, k, alpha, x);
+                       pred_step, prev_step, k, alpha, x, pads);
   else
     launch(embed_kernel<bf16_t>, grid, dim3(256), 0, st, (const bf16_t*)E, d, vocab,
                        mask_id, seq_len, tok_c, tok_stride, pos, region, n_rows, pred_ids, pred_w,
-                       pred_step, prev_step, k, alpha, x);
+                       pred_step, prev_step, k, alpha, x, pads);
   return hipGetLastError();
 }
 

@@ -14,13 +14,15 @@ __global__ void __launch_bounds__(256) unmask_kernel(
     const float* __restrict__ topk_w, int k, int n_out, const int32_t* __restrict__ pos_out,
     int step, int32_t* __restrict__ pred_ids, float* __restrict__ pred_w,
     int32_t* __restrict__ pred_step, uint8_t* __restrict__ selected,
-    int32_t* __restrict__ masked_left) {
+    int32_t* __restrict__ masked_left, Pads pads) {
   __shared__ float score[1024];
   __shared__ uint8_t cand[1024];
   __shared__ uint8_t sel[1024];
   __shared__ int n_cand, n_sel, best;
   const int s = blockIdx.x, tid = threadIdx.x;
-  int32_t* tok = tokens + (size_t)s * seq_len + block_start;
+  // a padded sequence's block and suffix positions sit pad[s] to the left
+  const int shift = pads.of(s);
+  int32_t* tok = tokens + (size_t)s * seq_len + (block_start - shift);
   const size_t ro = (size_t)s * n_out;
   if (tid == 0) { n_cand = 0; n_sel = 0; best = -1; }
   for (int i = tid; i < b; i += blockDim.x) {
@@ -64,7 +66,7 @@ __global__ void __launch_bounds__(256) unmask_kernel(
   }
   // prediction state of the retained suffix rows
   for (int r = b + tid; r < n_out; r += blockDim.x) {
-    const int p = pos_out[r];
+    const int p = pos_out[r] - shift;
     if (p < 0 || p >= seq_len) continue;
     const size_t sp = (size_t)s * seq_len + p;
     for (int i = 0; i < k; ++i) {
@@ -80,24 +82,29 @@ hipError_t launch_unmask(int32_t* tokens, int batch, int seq_len, int block_star
                          const int32_t* argmax, const float* conf, const int32_t* topk_ids,
                          const float* topk_w, int k, int n_out, const int32_t* pos_out, int step,
                          int32_t* pred_ids, float* pred_w, int32_t* pred_step, uint8_t* selected,
-                         int32_t* masked_left, hipStream_t st) {
+                         int32_t* masked_left, const Pads& pads, hipStream_t st) {
   launch(unmask_kernel, dim3(batch), dim3(256), 0, st, tokens, seq_len, block_start, b,
                      mask_id, rule, n_per_step, threshold, argmax, conf, topk_ids, topk_w, k,
-                     n_out, pos_out, step, pred_ids, pred_w, pred_step, selected, masked_left);
+                     n_out, pos_out, step, pred_ids, pred_w, pred_step, selected, masked_left,
+                     pads);
   return hipGetLastError();
 }
 
 // Early termination after a block (Section 3.2, "Early Termination"; the fill
 // rule of Section 4.4).  One workgroup per sequence: a sequence not yet done
 // whose block holds eos_id gets every later position set to eos_id and is
-// marked done.
+// marked done.  A padded sequence's block starts pad[s] to the left and its
+// sequence ends pad[s] before seq_len.
 __global__ void __launch_bounds__(256) early_stop_kernel(int32_t* __restrict__ tokens, int seq_len,
                                                          int block_start, int b, int eos_id,
-                                                         int32_t* __restrict__ done) {
+                                                         int32_t* __restrict__ done, Pads pads) {
   __shared__ int found;
   const int s = blockIdx.x, tid = threadIdx.x;
   if (done[s]) return;                        // uniform over the workgroup
   int32_t* tok = tokens + (size_t)s * seq_len;
+  const int shift = pads.of(s);
+  block_start -= shift;
+  seq_len -= shift;
   if (tid == 0) found = 0;
   __syncthreads();
   int hit = 0;
@@ -110,9 +117,9 @@ __global__ void __launch_bounds__(256) early_stop_kernel(int32_t* __restrict__ t
 }
 
 hipError_t launch_early_stop(int32_t* tokens, int batch, int seq_len, int block_start, int b,
-                             int eos_id, int32_t* done, hipStream_t st) {
+                             int eos_id, int32_t* done, const Pads& pads, hipStream_t st) {
   launch(early_stop_kernel, dim3(batch), dim3(256), 0, st, tokens, seq_len, block_start, b, eos_id,
-         done);
+         done, pads);
   return hipGetLastError();
 }
 

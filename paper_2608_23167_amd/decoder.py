@@ -4,6 +4,10 @@ Per step: ssm_select_suffix -> ssm_embed_suffix -> ssm_denoise_step ->
 ssm_unmask, all enqueued on the current stream.  The fixed top-n rule knows
 its step count up front and never synchronises; the threshold and margin
 rules read the number of masks left in the block once per step.
+
+A batch whose prompts differ in length (`prompt_lens`) shares the row layout
+of its longest prompt (the workload's prompt_len); every call gets each
+sequence's left padding, the longest prompt length minus its own.
 """
 from __future__ import annotations
 
@@ -37,8 +41,13 @@ class StepInfo:
 
 
 class Decoder:
-    def __init__(self, wl, model: DeviceModel, device="cuda"):
+    def __init__(self, wl, model: DeviceModel, device="cuda", prompt_lens=None):
         self.wl, self.model, self.device = wl, model, device
+        self.pad = None
+        if prompt_lens is not None:
+            if len(prompt_lens) != wl.batch or max(prompt_lens) != wl.prompt_len or min(prompt_lens) < 0:
+                raise ValueError("prompt_lens: one per sequence, the longest equal to the workload's")
+            self.pad = [wl.prompt_len - int(p) for p in prompt_lens]
         shape = wl.model
         B, Lt, k = wl.batch, wl.total_len, wl.topk
         self.max_rows, self.max_kv = 1, 1
@@ -86,9 +95,10 @@ class Decoder:
         wl, m = self.wl, self.model
         include_prefix = (not wl.cache) or first_in_block
         n_rows, n_suffix, first_out = ssm_select_suffix(
-            self.params(block_idx, include_prefix), self.tokens, self.pos, self.tok_c, self.region)
+            self.params(block_idx, include_prefix), self.tokens, self.pos, self.tok_c, self.region,
+            pad=self.pad)
         ssm_embed_suffix(m, self.tok_c, self.pos, self.region, n_rows, self.pred_ids, self.pred_w,
-                         self.pred_step, self.step_idx - 1, wl.topk, wl.alpha, self.x)
+                         self.pred_step, self.step_idx - 1, wl.topk, wl.alpha, self.x, pad=self.pad)
         P = wl.prompt_len + block_idx * wl.block_size
         if not wl.cache:
             mode, n_cached = L.SSM_CACHE_OFF, 0
@@ -98,13 +108,14 @@ class Decoder:
             mode, n_cached = L.SSM_CACHE_READ, P
         ssm_denoise_step(m, self.cache, mode, n_cached, self.pos, n_rows, self.x.view(wl.batch, -1),
                          first_out, wl.topk, self.argmax, self.conf, self.topk_ids, self.topk_w,
-                         self.ws, logits, hidden)
+                         self.ws, logits, hidden, pad=self.pad)
         n_out = n_rows - first_out
         if unmask:
             ssm_unmask(self.tokens, P, wl.block_size, wl.model.mask_id, RULES[wl.rule],
                        wl.n_per_step, wl.threshold, self.argmax, self.conf, self.topk_ids,
                        self.topk_w, wl.topk, n_out, self.pos[first_out:], self.step_idx,
-                       self.pred_ids, self.pred_w, self.pred_step, self.selected, self.masked_left)
+                       self.pred_ids, self.pred_w, self.pred_step, self.selected, self.masked_left,
+                       pad=self.pad)
         info = StepInfo(block_idx, self.step_idx, include_prefix, n_rows, n_suffix, first_out,
                         n_cached)
         self.step_idx += 1
@@ -142,5 +153,5 @@ class Decoder:
         sequences that produced the end token; True once every sequence has."""
         wl = self.wl
         ssm_early_stop(self.tokens, wl.prompt_len + block_idx * wl.block_size, wl.block_size,
-                       wl.eos_id, self.done)
+                       wl.eos_id, self.done, pad=self.pad)
         return bool(int(self.done.min().item()) == 1)

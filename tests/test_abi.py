@@ -112,14 +112,21 @@ def test_select_suffix_validation_before_launch():
     p = _params()
     n = C.c_int32()
     fake = C.c_void_p(0x1000)   # never dereferenced: validation fails first
-    rc = lib.ssm_select_suffix(C.byref(p), 1, 160, fake, fake, fake, None, 10, C.byref(n), None, None, None)
+    rc = lib.ssm_select_suffix(C.byref(p), 1, 160, None, fake, fake, fake, None, 10, C.byref(n), None, None, None)
     assert rc == L.SSM_E_CAPACITY and b"cap" in lib.ssm_last_error()
-    rc = lib.ssm_select_suffix(C.byref(p), 1, 161, fake, fake, fake, None, 500, None, None, None, None)
+    rc = lib.ssm_select_suffix(C.byref(p), 1, 161, None, fake, fake, fake, None, 500, None, None, None, None)
     assert rc == L.SSM_E_INVAL
-    rc = lib.ssm_select_suffix(C.byref(p), 0, 160, fake, fake, fake, None, 500, None, None, None, None)
+    rc = lib.ssm_select_suffix(C.byref(p), 0, 160, None, fake, fake, fake, None, 500, None, None, None, None)
     assert rc == L.SSM_E_INVAL
-    rc = lib.ssm_select_suffix(C.byref(p), 1, 160, None, fake, fake, None, 500, None, None, None, None)
+    rc = lib.ssm_select_suffix(C.byref(p), 1, 160, None, None, fake, fake, None, 500, None, None, None, None)
     assert rc == L.SSM_E_INVAL
+    # a pad beyond the longest prompt (32), and a padded batch beyond 64 sequences
+    rc = lib.ssm_select_suffix(C.byref(p), 1, 160, (C.c_int32 * 1)(33), fake, fake, fake, None, 500,
+                               None, None, None, None)
+    assert rc == L.SSM_E_INVAL
+    rc = lib.ssm_select_suffix(C.byref(p), 65, 160, (C.c_int32 * 65)(), fake, fake, fake, None, 500,
+                               None, None, None, None)
+    assert rc == L.SSM_E_UNSUPPORTED
 
 
 def _model(**kw):
@@ -177,8 +184,8 @@ def test_workspace_size_and_step_validation():
     assert n.value > 376 * 126464 * 4
     fake = C.c_void_p(0x1000)
     cache = L.KVCache(0x1000, 0x1000, 400)
-    args = lambda mode, n_cached, rows, k=5, ws=n.value, first=0: (
-        C.byref(m), C.byref(cache), mode, n_cached, 1, fake, rows, fake, first, k, fake, fake,
+    args = lambda mode, n_cached, rows, k=5, ws=n.value, first=0, pad=None: (
+        C.byref(m), C.byref(cache), mode, n_cached, 1, pad, fake, rows, fake, first, k, fake, fake,
         fake, fake, None, None, fake, ws, None)
     assert lib.ssm_denoise_step(*args(L.SSM_CACHE_READ, 100, 376)) == L.SSM_E_CAPACITY
     assert lib.ssm_denoise_step(*args(L.SSM_CACHE_WRITE, 10, 120)) == L.SSM_E_INVAL
@@ -187,30 +194,39 @@ def test_workspace_size_and_step_validation():
     assert lib.ssm_denoise_step(*args(0, 0, 120, k=9)) == L.SSM_E_INVAL
     assert lib.ssm_denoise_step(*args(0, 0, 120, ws=1000)) == L.SSM_E_CAPACITY
     assert lib.ssm_denoise_step(*args(0, 0, 120, first=120)) == L.SSM_E_INVAL
+    # padding must lie in the prefix: the cached slots, or the prefix rows
+    pad = lambda v: (C.c_int32 * 1)(v)
+    assert lib.ssm_denoise_step(*args(L.SSM_CACHE_READ, 100, 120, pad=pad(101))) == L.SSM_E_INVAL
+    assert lib.ssm_denoise_step(*args(L.SSM_CACHE_WRITE, 0, 120, first=40, pad=pad(41))) == L.SSM_E_INVAL
+    assert lib.ssm_denoise_step(*args(L.SSM_CACHE_WRITE, 0, 120, first=40, pad=pad(-1))) == L.SSM_E_INVAL
 
 
 def test_unmask_and_embed_validation():
     from paper_2608_23167_amd import _lib as L
     lib = L.lib()
     f = C.c_void_p(0x1000)
-    base = [f, 1, 200, 64, 32, 999, 0, 1, 0.9, f, f, f, f, 4, 40, f, 3, f, f, f, None, None, None]
+    base = [f, 1, 200, None, 64, 32, 999, 0, 1, 0.9, f, f, f, f, 4, 40, f, 3, f, f, f, None, None,
+            None]
     def with_(**kw):
         a = list(base)
-        idx = dict(batch=1, seq_len=2, block_start=3, block_size=4, rule=6, n_per_step=7, k=13, n_out=14)
+        idx = dict(batch=1, seq_len=2, pad=3, block_start=4, block_size=5, rule=7, n_per_step=8,
+                   k=14, n_out=15)
         for k, v in kw.items():
             a[idx[k]] = v
         return a
     for kw in (dict(block_size=0), dict(block_start=180), dict(rule=5), dict(n_per_step=0),
-               dict(k=9), dict(n_out=10), dict(rule=2, k=1)):
+               dict(k=9), dict(n_out=10), dict(rule=2, k=1), dict(pad=(C.c_int32 * 1)(65))):
         assert lib.ssm_unmask(*with_(**kw)) == L.SSM_E_INVAL, kw
     m = _model()
-    e = [C.byref(m), 1, 100, f, 50, f, f, 50, f, f, f, 3, 5, 0.4, f, None]
-    e2 = list(e); e2[12] = 0
+    e = [C.byref(m), 1, 100, None, f, 50, f, f, 50, f, f, f, 3, 5, 0.4, f, None]
+    e2 = list(e); e2[13] = 0
     assert lib.ssm_embed_suffix(*e2) == L.SSM_E_INVAL
-    e3 = list(e); e3[13] = 1.5
+    e3 = list(e); e3[14] = 1.5
     assert lib.ssm_embed_suffix(*e3) == L.SSM_E_INVAL
-    e4 = list(e); e4[4] = 10
+    e4 = list(e); e4[5] = 10
     assert lib.ssm_embed_suffix(*e4) == L.SSM_E_INVAL
+    e5 = list(e); e5[3] = (C.c_int32 * 1)(101)
+    assert lib.ssm_embed_suffix(*e5) == L.SSM_E_INVAL
 
 
 def test_early_stop_validation():
@@ -218,11 +234,13 @@ def test_early_stop_validation():
     from paper_2608_23167_amd import _lib as L
     lib = L.lib()
     fake = C.c_void_p(0x1000)
-    assert lib.ssm_early_stop(fake, 1, 64, 32, 32, -1, fake, None) == L.SSM_E_INVAL   # eos < 0
-    assert lib.ssm_early_stop(fake, 1, 64, 48, 32, 5, fake, None) == L.SSM_E_INVAL    # past the end
-    assert lib.ssm_early_stop(fake, 0, 64, 0, 32, 5, fake, None) == L.SSM_E_INVAL     # no sequence
-    assert lib.ssm_early_stop(None, 1, 64, 0, 32, 5, fake, None) == L.SSM_E_INVAL     # null tokens
-    assert lib.ssm_early_stop(fake, 1, 64, 0, 32, 5, None, None) == L.SSM_E_INVAL     # null flags
+    assert lib.ssm_early_stop(fake, 1, 64, None, 32, 32, -1, fake, None) == L.SSM_E_INVAL   # eos < 0
+    assert lib.ssm_early_stop(fake, 1, 64, None, 48, 32, 5, fake, None) == L.SSM_E_INVAL    # past the end
+    assert lib.ssm_early_stop(fake, 0, 64, None, 0, 32, 5, fake, None) == L.SSM_E_INVAL     # no sequence
+    assert lib.ssm_early_stop(None, 1, 64, None, 0, 32, 5, fake, None) == L.SSM_E_INVAL     # null tokens
+    assert lib.ssm_early_stop(fake, 1, 64, None, 0, 32, 5, None, None) == L.SSM_E_INVAL     # null flags
+    pad = (C.c_int32 * 1)(33)                                                               # pad > block start
+    assert lib.ssm_early_stop(fake, 1, 64, pad, 32, 32, 5, fake, None) == L.SSM_E_INVAL
 
 
 def test_attention_validation():

@@ -118,6 +118,9 @@ def main():
                          "generation of length 1024)")
     ap.add_argument("--cpu-layers", type=int, default=None,
                     help="layers of the CPU oracle sample (default: all; fewer are extrapolated)")
+    ap.add_argument("--no-cpu-samples", action="store_true",
+                    help="skip the further oracle samples (tiny generation, long-workload steps, "
+                         "microbenchmark attention)")
     ap.add_argument("--cpu-reps", type=int, default=4,
                     help="repetitions of each layer of the CPU oracle sample")
     args = ap.parse_args()
@@ -156,16 +159,46 @@ def main():
     dm = DeviceModel(shape, mw)
     dec = Decoder(wl, dm, device=dev)
     tok0 = initial_tokens(wl, device=dev)
-    sched = dec.schedule()
+    # fixed top-n rules know their schedule; confidence-driven rules (threshold,
+    # margin) run whole generations through Decoder.generate, which reads the
+    # masks left in the block after every step
+    fixed = wl.steps_per_block() is not None
+
+    def schedule_of(d):
+        if fixed:
+            return d.schedule()
+        rec = []
+        d.generate(tok0, pre_step=lambda j, first: rec.append((j, first)))
+        torch.cuda.synchronize()
+        return rec
+
+    sched = schedule_of(dec)
     K = args.steps or len(sched)
+    if not fixed:
+        K = min(K, len(sched))
     W = args.warmup
 
-    def run(n, events=None, d=dec):
+    def run(n, events=None, d=dec, sch=None):
         """n steps of the schedule from a fresh generation, wrapping around."""
+        sch = sch or sched
+        if not fixed:
+            # the first n steps of a generation, as generate() runs them
+            i = [0]
+
+            def pre(j, first):
+                if events is not None:
+                    events[i[0]][0].record()
+
+            def post(j, first):
+                if events is not None:
+                    events[i[0]][1].record()
+                i[0] += 1
+            d.generate(tok0, max_steps=n, pre_step=pre, post_step=post)
+            return
         d.reset(tok0)
         for i in range(n):
-            j, first = sched[i % len(sched)]
-            if i and i % len(sched) == 0:
+            j, first = sch[i % len(sch)]
+            if i and i % len(sch) == 0:
                 d.reset(tok0)
             if events is not None:
                 events[i][0].record()
@@ -173,18 +206,20 @@ def main():
             if events is not None:
                 events[i][1].record()
 
-    def timed(d):
+    def timed(d, sch=None):
         """W warm-up steps, then K timed steps: (wall s, per-step ms, step kinds)."""
-        run(W, d=d)
+        sch = sch or sched
+        k = K if fixed else min(K, len(sch))
+        run(W, d=d, sch=sch)
         torch.cuda.synchronize()
         ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-              for _ in range(K)]
+              for _ in range(k)]
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        run(K, ev, d=d)
+        run(k, ev, d=d, sch=sch)
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
-        return wall, [a.elapsed_time(b) for a, b in ev], [sched[i % len(sched)][1] for i in range(K)]
+        return wall, [a.elapsed_time(b) for a, b in ev], [sch[i % len(sch)][1] for i in range(k)], k
 
     def medians(step_ms, kinds):
         start_ms = [t for t, f in zip(step_ms, kinds) if f]
@@ -193,8 +228,10 @@ def main():
                 "cached_median": round(statistics.median(cached_ms), 4) if cached_ms else None}
 
     print(f"[bench] warmup {W} steps", file=sys.stderr, flush=True)
-    wall, step_ms, kinds = timed(dec)
-    tokens = K * wl.n_per_step * wl.batch
+    wall, step_ms, kinds, _ = timed(dec)
+    # tokens decoded in the timed steps: n per step for top-n; a confidence
+    # rule decodes a whole generation in its len(sched) steps
+    tokens = K * wl.n_per_step * wl.batch if fixed else wl.gen_len * wl.batch * K / len(sched)
     value = tokens / wall
     print(f"[bench] {K} steps in {wall:.3f} s -> {value:.1f} tokens/s", file=sys.stderr, flush=True)
 
@@ -270,13 +307,15 @@ def main():
         # local row (the unpruned decoder SSM is measured against)
         wl_full = wl.replace(local_budget=wl.gen_len, middle_budget=0, tail_budget=0)
         dec_full = Decoder(wl_full, dm, device=dev)
-        fwall, fstep_ms, fkinds = timed(dec_full)
-        fvalue = tokens / fwall
+        fsched = schedule_of(dec_full)
+        fwall, fstep_ms, fkinds, fk = timed(dec_full, fsched)
+        ftokens = tokens if fixed else wl.gen_len * wl.batch * fk / len(fsched)
+        fvalue = ftokens / fwall
         del dec_full
         print(f"[bench] full suffix: {K} steps in {fwall:.3f} s -> {fvalue:.1f} tokens/s",
               file=sys.stderr, flush=True)
         result["full_suffix"] = {"value": round(fvalue, 2), "unit": "tokens/s",
-                                 "ms_per_step": round(fwall / K * 1e3, 4),
+                                 "steps": fk, "ms_per_step": round(fwall / fk * 1e3, 4),
                                  "step_latency_ms": medians(fstep_ms, fkinds),
                                  "ssm_speedup": round(value / fvalue, 3)}
 
@@ -287,6 +326,8 @@ def main():
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, mw, dec, args.cpu_layers or wl.model.n_layers,
                                               args.cpu_reps)
+        if shape == WORKLOADS["llada_long2048"].model and not args.no_cpu_samples:
+            result["cpu_baseline"]["samples"] = cpu_samples(mw)
     print(json.dumps(result), flush=True)
 
 
@@ -680,7 +721,102 @@ def cpu_baseline(wl, mw, dec, n_layers_sample, reps):
                        f"{n_layers_sample} of {shape.n_layers} layers (each timed {reps}x, mean) "
                        f"+ LM head and row statistics in float32 NumPy ({sample_s:.1f} s of CPU "
                        f"work) -> {step_s:.2f} s per step"),
-            "step_seconds": round(step_s, 3)}
+            "step_seconds": round(step_s, 3), **host_info()}
+
+
+def host_info():
+    """CPU model and the BLAS library NumPy runs on (threadpoolctl)."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    blas = None
+    try:
+        from threadpoolctl import threadpool_info
+        for p in threadpool_info():
+            if p.get("user_api") == "blas":
+                blas = f"{p.get('internal_api')} {p.get('version')} ({p.get('num_threads')} threads)"
+                break
+    except Exception:
+        pass
+    return {"cpu_model": model, "blas": blas, "nproc": os.cpu_count()}
+
+
+def cpu_samples(mw_llada):
+    """Further oracle samples on the host cores (bounded, about 10-30 s):
+      * the tiny float32 workload: one whole generation (32 steps);
+      * the long LLaDA-8B workload (prompt 1024, gen 2048, block 64, budgets
+        128/32/16, prefix cache): a block-start and a cached step at the first,
+        a middle and the last block, each as one decoder layer (extrapolated to
+        32 layers) plus the LM head and row statistics of its output rows;
+      * the attention microbenchmark (LLaDA-8B heads, batch 8, prefix 4096,
+        block 64, 176 kept suffix rows): the oracle's attention of one layer.
+    Inputs are synthetic rows of the step's shape; the LLaDA-shaped weights are
+    those of the bench model (same shape and seed)."""
+    import numpy as np
+    import oracle.generate as OG
+    import oracle.model as OM
+    import oracle.selection as OS
+    from synthetic import WORKLOADS, make_weights
+    out = []
+    tiny = WORKLOADS["tiny"]
+    wt = OG.NumpyWeights(make_weights(tiny.model, seed=tiny.seed))
+    t0 = time.perf_counter()
+    _, recs = OG.generate(tiny, wt, initial_tokens_np(tiny))
+    dt = time.perf_counter() - t0
+    out.append({"workload": "tiny", "sample": f"whole generation ({len(recs)} steps)",
+                "seconds": round(dt, 3), "tokens_per_s": round(tiny.gen_len / dt, 2)})
+    print(f"[bench] cpu sample {out[-1]}", file=sys.stderr, flush=True)
+
+    wl = WORKLOADS["llada_long2048"]
+    sh = wl.model
+    w = OG.NumpyWeights(mw_llada, dtype=np.float32, keep_layers=False)
+    lw = w.layers[0]
+    rng = np.random.default_rng(0)
+    for j in (0, wl.n_blocks // 2, wl.n_blocks - 1):
+        t_head = None
+        for kind, incl in (("block_start", True), ("cached", False)):
+            rows = OS.compacted_rows(wl.prompt_len, wl.gen_len, wl.block_size, j, wl.local_budget,
+                                     wl.middle_budget, wl.middle_mode, wl.tail_budget, incl)
+            n = len(rows.pos)
+            x = (0.02 * rng.standard_normal((n, sh.d_model))).astype(np.float32)
+            kp = vp = None
+            if not incl:
+                P = wl.prompt_len + j * wl.block_size
+                kp = rng.standard_normal((P, sh.n_kv_heads, sh.head_dim)).astype(np.float32)
+                vp = rng.standard_normal((P, sh.n_kv_heads, sh.head_dim)).astype(np.float32)
+            t0 = time.perf_counter()
+            y = OM.layer_forward(x, rows.pos, lw, sh, kp, vp).x
+            t_layer = time.perf_counter() - t0
+            if t_head is None:
+                t0 = time.perf_counter()
+                OM.output_stats(y[rows.first_out_row:], w, sh, wl.topk)
+                t_head = time.perf_counter() - t0
+            step_s = t_layer * sh.n_layers + t_head
+            out.append({"workload": wl.name, "block": j, "step": kind, "rows": n,
+                        "layer_seconds": round(t_layer, 3), "lm_head_seconds": round(t_head, 3),
+                        "step_seconds_extrapolated": round(step_s, 2)})
+            print(f"[bench] cpu sample {out[-1]}", file=sys.stderr, flush=True)
+
+    B, H, dh, n_q, n_k = 8, 32, 128, 64 + 176, 4096 + 64 + 176
+    q = rng.standard_normal((n_q, H, dh)).astype(np.float32)
+    k = rng.standard_normal((n_k, H, dh)).astype(np.float32)
+    v = rng.standard_normal((n_k, H, dh)).astype(np.float32)
+    t0 = time.perf_counter()
+    for _ in range(B):
+        OM.attention(q, k, v)
+    dt = time.perf_counter() - t0
+    out.append({"workload": "attn_micro", "sample": f"one layer: batch {B}, {n_q} queries x {n_k} keys, "
+                                                   f"{H} heads of {dh}",
+                "seconds": round(dt, 3),
+                "gflops": round(4.0 * B * n_q * n_k * H * dh / dt / 1e9, 1)})
+    print(f"[bench] cpu sample {out[-1]}", file=sys.stderr, flush=True)
+    return out
 
 
 def initial_tokens_np(wl):

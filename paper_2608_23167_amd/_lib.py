@@ -81,16 +81,26 @@ _SIGS = {
 }
 
 _lib = None
+_path = LIB_PATH
+
+
+def use_library(path: str) -> None:
+    """Loads the C ABI from `path` instead of the package's libssm.so (e.g. a
+    host-only build instrumented with sanitizers); only before the first call."""
+    global _path
+    if _lib is not None:
+        raise RuntimeError("the library is already loaded")
+    _path = path
 
 
 def lib() -> C.CDLL:
     """The loaded library; raises if it has not been built."""
     global _lib
     if _lib is None:
-        if not os.path.exists(LIB_PATH):
-            raise ImportError(f"{LIB_PATH} is missing: build it with "
+        if not os.path.exists(_path):
+            raise ImportError(f"{_path} is missing: build it with "
                               "`python -m paper_2608_23167_amd.build` (no CPU fallback exists)")
-        l = C.CDLL(LIB_PATH)
+        l = C.CDLL(_path)
         for name, (res, args) in _SIGS.items():
             f = getattr(l, name)
             f.restype = res

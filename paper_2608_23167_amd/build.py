@@ -4,6 +4,11 @@ Usage: python -m paper_2608_23167_amd.build   (or __graft_entry__.build()).
 Objects go to _build/ next to this file; the library is written in place
 (paper_2608_23167_amd/libssm.so) so that it travels with the source tree.
 
+`--hostsan DIR` builds DIR/libssm_hostsan.so: the same library with its host
+code instrumented by AddressSanitizer and UndefinedBehaviorSanitizer (device
+code as usual, uninstrumented), for the CPU tests of the C ABI's validation
+and closed-form host paths.
+
 `--tuning` builds a separate library (libssm_tuning.so, objects in
 _build_tuning/) with SSM_TUNING defined: its GEMM launch choices can be
 overridden through the SSM_GEMM_CFG / SSM_GEMM_KROT environment variables
@@ -59,6 +64,42 @@ def build(verbose: bool = False, tuning: bool = False) -> str:
     return out
 
 
+# Sanitizer build: each -fsanitize= applies to the host compilation only.
+HOSTSAN_FLAGS = [
+    "--offload-arch=gfx950", "-O1", "-g", "-std=c++17", "-fPIC",
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-fno-omit-frame-pointer", "-Wno-unused-result",
+    *"-Xarch_host -fsanitize=address -Xarch_host -fsanitize=undefined".split(),
+    *"-Xarch_host -fno-sanitize-recover=undefined".split(),
+]
+
+
+def build_hostsan(out_dir: str) -> str:
+    """Builds out_dir/libssm_hostsan.so (see the module docstring)."""
+    os.makedirs(out_dir, exist_ok=True)
+    srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
+
+    def one(src):
+        obj = os.path.join(out_dir, os.path.basename(src) + ".o")
+        r = subprocess.run([HIPCC, *HOSTSAN_FLAGS, "-c", src, "-o", obj], capture_output=True,
+                           text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"hipcc failed on {src}:\n{r.stdout}\n{r.stderr}")
+        return obj
+    with cf.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
+        objs = list(ex.map(one, srcs))
+    out = os.path.join(out_dir, "libssm_hostsan.so")
+    r = subprocess.run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-shared-libsan",
+                        *"-Xarch_host -fsanitize=address -Xarch_host -fsanitize=undefined".split(),
+                        "-o", out, *objs], capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")
+    return out
+
+
 if __name__ == "__main__":
+    if "--hostsan" in sys.argv[1:]:
+        print("built", build_hostsan(sys.argv[sys.argv.index("--hostsan") + 1]))
+        sys.exit(0)
     build(verbose=True, tuning="--tuning" in sys.argv[1:])
     sys.exit(0)

@@ -127,7 +127,11 @@ class Decoder:
         assert spb is not None
         return [(j, i == 0) for j in range(self.wl.n_blocks) for i in range(spb)]
 
-    def generate(self, tokens0: torch.Tensor, max_steps: Optional[int] = None) -> torch.Tensor:
+    def generate(self, tokens0: torch.Tensor, max_steps: Optional[int] = None,
+                 pre_step=None, post_step=None) -> torch.Tensor:
+        """Whole generation from tokens0.  pre_step / post_step (optional) are
+        called with (block, first_in_block) around every step, e.g. to record
+        the schedule of a confidence-driven rule or to place timing events."""
         self.reset(tokens0)
         wl = self.wl
         spb = wl.steps_per_block()
@@ -137,7 +141,11 @@ class Decoder:
             while True:
                 if spb is not None and i >= spb:
                     break
+                if pre_step is not None:
+                    pre_step(j, i == 0)
                 self.step(j, i == 0)
+                if post_step is not None:
+                    post_step(j, i == 0)
                 i += 1
                 n += 1
                 if max_steps is not None and n >= max_steps:

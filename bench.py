@@ -113,6 +113,9 @@ def main():
                     help="skip the unpruned (full-suffix) decoder run of the same schedule")
     ap.add_argument("--no-profile", action="store_true",
                     help="skip the profiled replay (per-kernel times and roofline), e.g. under counter collection")
+    ap.add_argument("--no-gen-sweep", action="store_true",
+                    help="skip the generation-length sweep (whole generations at 256 .. 2048, SSM and "
+                         "unpruned) that the default run reports")
     ap.add_argument("--no-mfma", action="store_true",
                     help="skip the MFMA report (projections and attention of the LLaDA-8B-shaped "
                          "generation of length 1024)")
@@ -323,6 +326,12 @@ def main():
         result["mfma"] = mfma_report(dm, dev)
         print(f"[bench] mfma: {result['mfma']}", file=sys.stderr, flush=True)
 
+    if not args.no_gen_sweep and shape == WORKLOADS["llada_long2048"].model:
+        result["gen_sweep"] = {
+            "workload": "LLaDA-8B shape, prompt 1024, block 64, top-8, budgets 128/32/16, prefix "
+                        "cache; whole generations, SSM and unpruned",
+            "points": gen_sweep(dm, dev, emit=False)}
+
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, mw, dec, args.cpu_layers or wl.model.n_layers,
                                               args.cpu_reps)
@@ -394,20 +403,22 @@ def mfma_report(dm, dev, reps=3):
     return out
 
 
-def gen_sweep():
+def gen_sweep(dm=None, dev=None, emit=True):
     """Tokens/s and step latency of whole generations vs generation length, SSM
     and the unpruned decoder (every suffix token kept), on one set of LLaDA-8B
     weights: prompt 1024, block 64, top-8 per step, budgets 128/32/16, prefix
-    cache, batch 1.  One warm-up generation per point; one JSON line."""
+    cache, batch 1.  One warm-up generation per point.  Standalone it prints
+    one JSON line; inside the default bench its points are returned."""
     import torch
     from synthetic import WORKLOADS, initial_tokens, make_weights
     from paper_2608_23167_amd.decoder import Decoder
     from paper_2608_23167_amd.model import DeviceModel
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
     base = WORKLOADS["llada_long2048"]
-    mw = make_weights(base.model, seed=base.seed, device=dev)
-    dm = DeviceModel(base.model, mw)
+    if dm is None:
+        dev = torch.device("cuda:0")
+        torch.cuda.set_device(dev)
+        mw = make_weights(base.model, seed=base.seed, device=dev)
+        dm = DeviceModel(base.model, mw)
     points = []
     for G in (256, 512, 1024, 2048):
         wl = base.replace(gen_len=G)
@@ -435,6 +446,8 @@ def gen_sweep():
         pt["ssm_speedup"] = round(pt["full"]["seconds"] / pt["ssm"]["seconds"], 3)
         print(f"[bench] gen sweep {pt}", file=sys.stderr, flush=True)
         points.append(pt)
+    if not emit:
+        return points
     print(json.dumps({"metric": "whole-generation tokens/s vs generation length, SSM and unpruned "
                                 "(LLaDA-8B shape, prompt 1024, block 64, top-8, budgets 128/32/16)",
                       "unit": "tokens/s", "n_gpus": 1, "dtype": "bf16",

@@ -147,3 +147,14 @@ def test_dream_last_block_uncached(gpu, dream):
     """The last block of the Dream-7B workload (no cache): prefix 992 + block
     32 = 1024 rows, no suffix left."""
     _run(WORKLOADS["dream_gen512"], dream, 15, True, 9, False)
+
+
+@pytest.mark.parametrize("gen,block,first,seed", [(256, 1, True, 10), (512, 3, False, 11)])
+def test_llada_gen_sweep_lengths(gpu, llada, gen, block, first, seed):
+    """The generation-length sweep's workloads (prompt 1024, block 64, top-8,
+    budgets 128/32/16, prefix cache) at the lengths no other full-depth test
+    covers: gen 256 (block-start step of block 1: prefix 1088, the two
+    remaining suffix blocks all local) and gen 512 (cached step of block 3,
+    prefix 1216 cached).  Gen 1024 and 2048 are the long workloads above."""
+    wl = WORKLOADS["llada_long2048"].replace(gen_len=gen)
+    _run(wl, llada, block, first, seed, not first)

@@ -18,9 +18,11 @@ class DeviceModel:
 
     # Leading layers whose projection inputs keep the bfloat16 pair by default.
     # Rounding them once in layer 0 alone gives most of the error of rounding
-    # them in every layer (the residual stream is smallest there); from about
-    # layer 4 on a rounding barely shows in the output.
-    PAIR_LAYERS = 4
+    # them in every layer (the residual stream is smallest there).  With the
+    # attention operands in float16, two pair layers keep the full-depth
+    # relative error of the 8B shapes at or below 1.0e-2 (half the bound);
+    # none gives up to 2.9e-2, one up to 1.3e-2.
+    PAIR_LAYERS = 2
 
     def __init__(self, shape, weights, act_mode: int = L.SSM_ACT_BF16X2_FIRST,
                  pair_layers: int = PAIR_LAYERS):

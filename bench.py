@@ -38,18 +38,16 @@ METRIC = "denoised tokens/sec + step latency per GPU (LLaDA-8B shape); % MFMA/HB
 # for the kernel sources it was measured on (sha256 of the GEMM sources).
 TRAFFIC = {
     # rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE over `bench.py --steps 32 --warmup 1
-    # --no-profile --no-cpu-baseline --no-full-suffix --no-mfma`; per-dispatch means
-    # of the block-start launches (grid 393216: 135884.1 / 9024.0 KiB for the 28
-    # one-pass layers, 189382.0 / 18048.0 KiB for the 4 layers with the bf16
-    # pair) and the cached ones (grid 131072: 104448.6 / 2880.0 and 110536.1 /
-    # 5760.0 KiB), weighted 28:4 over the layers and 1:31 over the steps as in the
-    # generation schedule; copy kernel: 268435456 bytes read and written per
-    # launch read as 131085.2 KiB fetched and 262144.0 KiB written
+    # --no-profile --no-cpu-baseline --no-full-suffix --no-mfma --no-gen-sweep`:
+    # per-dispatch means of the block-start launches (grid 393216, 376 rows) and
+    # the cached ones (grid 131072, 120 rows), for the one-pass layers and the
+    # layers that keep the bfloat16 pair; copy kernel: 268435456 bytes read and
+    # written per launch read as 131085.0 KiB fetched and 262144.0 KiB written
     ("llada_gen256", "gemm_gate_up"): {
-        "sources_sha256": "c479fea4753f0445a58138058de7a98d2c4306fab3b3d6d546c0dee67691913f",
-        "fetch_kib": ((28 * 135884.1 + 4 * 189382.0) / 32 + 31 * (28 * 104448.6 + 4 * 110536.1) / 32) / 32,
-        "write_kib": ((28 * 9024.0 + 4 * 18048.0) / 32 + 31 * (28 * 2880.0 + 4 * 5760.0) / 32) / 32,
-        "fetch_scale": 262144.0 / 131085.2, "write_scale": 1.0},
+        "sources_sha256": "15a8380c93a852e25edea5f5411810a94c5c9c9db3ea73eafd72a06229ce6c8c",
+        "fetch_kib": {"start": (135919.9, 189386.0), "cached": (104448.5, 110536.9)},
+        "write_kib": {"start": (9024.0, 18048.0), "cached": (2880.0, 5760.0)},
+        "fetch_scale": 262144.0 / 131085.0, "write_scale": 1.0},
 }
 GEMM_SOURCES = ("gemm.hip", "internal.h", "common.h")
 
@@ -62,11 +60,28 @@ def gemm_sources_sha256():
     return h.hexdigest()
 
 
-def measured_traffic(workload, kernel):
+def measured_traffic(workload, kernel, n_layers, n_pair, start_frac):
+    """Bytes per launch: the counters weighted n_pair : n_layers - n_pair over
+    the layers and start_frac : 1 - start_frac over block-start and cached
+    steps, as in the timed schedule; None if the sources changed since."""
     t = TRAFFIC.get((workload, kernel))
     if not t or t["sources_sha256"] != gemm_sources_sha256():
         return None
-    return round((t["fetch_kib"] * t["fetch_scale"] + t["write_kib"] * t["write_scale"]) * 1024)
+
+    def mix(table):
+        by_kind = {k: ((n_layers - n_pair) * one + n_pair * pair) / n_layers
+                   for k, (one, pair) in table.items()}
+        return start_frac * by_kind["start"] + (1.0 - start_frac) * by_kind["cached"]
+    return round((mix(t["fetch_kib"]) * t["fetch_scale"] + mix(t["write_kib"]) * t["write_scale"])
+                 * 1024)
+
+
+def n_pair_layers(dm):
+    """Layers whose projection inputs keep the bfloat16 pair (two MFMA passes)."""
+    from paper_2608_23167_amd import _lib as L
+    cm = dm.c_model
+    return {L.SSM_ACT_BF16X2: cm.n_layers,
+            L.SSM_ACT_BF16X2_FIRST: min(cm.pair_layers, cm.n_layers)}.get(cm.act_mode, 0)
 
 
 def gemm_work(shape, tag, M):
@@ -278,7 +293,9 @@ def main():
                     "unit": "TFLOP/s", "frac": round(tfl / BF16_PEAK_TFLOPS, 4)}
         roof.update({"kernel": dom, "launches": n_launch, "avg_launch_us": round(dom_ms / n_launch * 1e3, 2),
                      "algorithmic_bytes_per_launch": round(tot_bytes / n_launch),
-                     "mfma_tflops": round(tfl, 1), "traffic": measured_traffic(wl.name, dom)})
+                     "mfma_tflops": round(tfl, 1),
+                     "traffic": measured_traffic(wl.name, dom, shape.n_layers, n_pair_layers(dm),
+                                                 sum(1 for i in range(K) if sched[i % len(sched)][1]) / K)})
 
     result = {
         "metric": METRIC,
@@ -364,10 +381,7 @@ def mfma_report(dm, dev, reps=3):
     d_, H, Hkv, dh, F = sh.d_model, sh.n_heads, sh.n_kv_heads, sh.head_dim, sh.ffn_dim
     # MFMA passes per projection, averaged over the layers: two where a layer
     # keeps the bfloat16 pair (hi and lo parts), one where it rounds once
-    cm = dm.c_model
-    n_pair = {L.SSM_ACT_BF16X2: sh.n_layers,
-              L.SSM_ACT_BF16X2_FIRST: min(cm.pair_layers, sh.n_layers)}.get(cm.act_mode, 0)
-    passes = 1.0 + n_pair / sh.n_layers
+    passes = 1.0 + n_pair_layers(dm) / sh.n_layers
     dec = Decoder(wl, dm, device=dev)
     tok = initial_tokens(wl, device=dev)
     j = wl.n_blocks // 2

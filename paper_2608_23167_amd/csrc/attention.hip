@@ -82,30 +82,43 @@ __device__ __forceinline__ void attn_tile_of(int w, int total, int qtiles, int B
   split = v / (qtiles * BH);
 }
 
-template <int QB, typename E>
-__global__ void __launch_bounds__(256, 2) attn_bf16_kernel(
+// NG key groups per workgroup.  NG = 1: 4 waves walk the workgroup's key
+// range.  NG = 2 (small grids of decode steps, one workgroup per CU): two
+// groups of 4 waves take the query rows of the tile each, over the first and
+// the second half of the key tiles, with buffers of their own; group 1 then
+// hands its (output, maximum, sum) to group 0 through LDS, which merges and
+// writes.  Both groups pass the same barriers: a group with fewer tiles idles
+// through the missing steps.  Two waves per SIMD and half the tile chain per
+// wave: a decode launch is bound by the dependent chain of each tile step.
+template <int QB, typename E, int NG>
+__global__ void __launch_bounds__(256 * NG, NG == 1 ? 2 : 1) attn_bf16_kernel(
     const E* __restrict__ Q, const E* __restrict__ Kc, const E* __restrict__ Vc,
     int H, int Hkv, int Mq, int Nk, int cap, int keys_per_split, float scale_log2,
     ActOut O, float* __restrict__ Opart, float* __restrict__ ML, int qtiles, int BH, Pads pads) {
   typedef AttnOps<E> Ops;
   typedef typename Ops::vec vec;
   constexpr int DH = 128, KT = 64, TBUF = KT * DH;
-  // two buffers per tile kind
-  __shared__ __attribute__((aligned(1024))) E Ks[2 * TBUF];
-  __shared__ __attribute__((aligned(1024))) E Vs[2 * TBUF];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  static_assert(NG == 1 || (NG == 2 && QB == 1), "two key groups with 16 query rows per wave");
+  // two buffers per tile kind and group
+  __shared__ __attribute__((aligned(1024))) E Ks_all[NG * 2 * TBUF];
+  __shared__ __attribute__((aligned(1024))) E Vs_all[NG * 2 * TBUF];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int grp = NG == 1 ? 0 : __builtin_amdgcn_readfirstlane(tid >> 8);
+  const int wave = (tid >> 6) & 3;           // wave within its group
+  E* const Ks = Ks_all + grp * 2 * TBUF;
+  E* const Vs = Vs_all + grp * 2 * TBUF;
   const int g = lane >> 4, c16 = lane & 15;
   int qt, bh, split;
   attn_tile_of(blockIdx.x, gridDim.x, qtiles, BH, qt, bh, split);
   const int s = bh / H, h = bh % H, kvh = h / (H / Hkv);
   // a padded sequence's keys start after its padding slots
-  const int kb = pads.of(s) + split * keys_per_split, ke = min(Nk, kb + keys_per_split);
+  const int kb_wg = pads.of(s) + split * keys_per_split, ke_wg = min(Nk, kb_wg + keys_per_split);
   // query block b of the wave: rows q0 + 16 b .. + 15; this lane's query in it
   const int q0 = (qt * 4 + wave) * 16 * QB;
-  if (kb >= ke) {
+  if (kb_wg >= ke_wg) {
     // a split past the end of a padded sequence's shorter key range: an empty
     // partial (sum 0), which the merge skips (the host keeps split 0 non-empty)
-    if (Opart != nullptr && g == 0) {
+    if (Opart != nullptr && g == 0 && grp == 0) {
 #pragma unroll
       for (int b = 0; b < QB; ++b) {
         const int q = q0 + 16 * b + c16;
@@ -117,7 +130,10 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(
     }
     return;
   }
-  const int ntile = (ke - kb + KT - 1) / KT;   // >= 1
+  // this group's part of the range: whole tiles, the first group's part first
+  const int steps = (ke_wg - kb_wg + KT * NG - 1) / (KT * NG);          // tiles per group, >= 1
+  const int kb = kb_wg + grp * steps * KT, ke = min(ke_wg, kb + steps * KT);
+  const int ntile = ke > kb ? (ke - kb + KT - 1) / KT : 0;              // this group's tiles
 
   const E* Qh = Q + (size_t)bh * Mq * DH;
   vec qf[QB][4];
@@ -272,30 +288,64 @@ __global__ void __launch_bounds__(256, 2) attn_bf16_kernel(
     // the softmax of tile t runs (VALU).  In step t the waves read K of tile
     // t + 1 and V of tile t while K of tile t + 2 and V of tile t + 1 are
     // copied into the buffers read in step t - 1; one barrier per step.
-    copy_k(0, 0);
-    copy_v(0, 0);
-    if (ntile > 1) copy_k(1, 1);
+    if (ntile > 0) {
+      copy_k(0, 0);
+      copy_v(0, 0);
+      if (ntile > 1) copy_k(1, 1);
+    }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
     f32x4_t sa[QB][4], sb[QB][4];
-    qk(0, sa);
+    if (ntile > 0) qk(0, sa);
     __syncthreads();                                       // K buffer 0 is refilled next
     auto step = [&](int t, f32x4_t (&cur)[QB][4], f32x4_t (&nxt)[QB][4]) {
-      if (t + 2 < ntile) copy_k(t + 2, t & 1);
-      if (t + 1 < ntile) copy_v(t + 1, (t + 1) & 1);
-      softmax_max(t, cur);
-      // one branch-free block: the next tile's score MFMAs interleave with
-      // this tile's exponentials
-      if (t + 1 < ntile) qk((t + 1) & 1, nxt);
-      vec pb[QB][2];
-      softmax_exp(cur, pb);
-      pv(t & 1, pb);
+      if (t < ntile) {
+        if (t + 2 < ntile) copy_k(t + 2, t & 1);
+        if (t + 1 < ntile) copy_v(t + 1, (t + 1) & 1);
+        softmax_max(t, cur);
+        // one branch-free block: the next tile's score MFMAs interleave with
+        // this tile's exponentials
+        if (t + 1 < ntile) qk((t + 1) & 1, nxt);
+        vec pb[QB][2];
+        softmax_exp(cur, pb);
+        pv(t & 1, pb);
+      }
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       __syncthreads();
     };
-    for (int t = 0; t < ntile; t += 2) {
+    for (int t = 0; t < steps; t += 2) {
       step(t, sa, sb);
-      if (t + 1 < ntile) step(t + 1, sb, sa);
+      if (t + 1 < steps) step(t + 1, sb, sa);
+    }
+  }
+
+  if constexpr (NG == 2) {
+    // group 1 hands over its state (the loop has drained every copy and
+    // read): outputs at Ks_all's second half, (maximum, sum) at Vs_all's
+    float* xo = (float*)(Ks_all + 2 * TBUF) + (wave * 64 + lane) * (8 * 4 * QB);
+    float* xm = (float*)(Vs_all + 2 * TBUF) + (wave * 64 + lane) * (2 * QB);
+    if (grp == 1) {
+#pragma unroll
+      for (int b = 0; b < QB; ++b) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) *(f32x4_t*)(xo + (b * 8 + i) * 4) = o[b][i];
+        xm[2 * b] = m_run[b];
+        xm[2 * b + 1] = ol[b][0];
+      }
+    }
+    __syncthreads();
+    if (grp == 1) return;
+#pragma unroll
+    for (int b = 0; b < QB; ++b) {
+      const float m1 = xm[2 * b], l1 = xm[2 * b + 1];
+      const float m = fmaxf(m_run[b], m1);
+      // a group without keys has m = -inf and l = 0; its weight is 0
+      const float w0 = ol[b][0] > 0.f ? __builtin_amdgcn_exp2f(m_run[b] - m) : 0.f;
+      const float w1 = l1 > 0.f ? __builtin_amdgcn_exp2f(m1 - m) : 0.f;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) o[b][i] = o[b][i] * w0 + *(const f32x4_t*)(xo + (b * 8 + i) * 4) * w1;
+      ol[b][0] = ol[b][0] * w0 + l1 * w1;
+      m_run[b] = m;
     }
   }
 
@@ -459,22 +509,23 @@ hipError_t attention(int dtype, const void* q, const void* kc, const void* vc, i
   float* opart = S > 1 ? ws.opart : nullptr;
   if (mfma) {
     const dim3 grid(qtiles * BH * S);
+    // small grids (at most one workgroup per CU) whose splits hold two tiles or
+    // more: two key groups per workgroup
+    const bool groups = QB == 1 && qtiles * BH * S <= 256 && kps >= 2 * 64;
+    auto go = [&](auto kernel, int threads, auto* qh, auto* kh, auto* vh) {
+      launch(kernel, grid, dim3(threads), 0, st, qh, kh, vh, H, Hkv, Mq, Nk, cap, kps, scale_log2,
+             out, opart, ws.ml, qtiles, BH, pads);
+    };
     if (dtype == ATTN_F16) {
       const f16_t *qh = (const f16_t*)q, *kh = (const f16_t*)kc, *vh = (const f16_t*)vc;
-      if (QB == 2)
-        launch(attn_bf16_kernel<2, f16_t>, grid, dim3(256), 0, st, qh, kh, vh, H, Hkv, Mq, Nk, cap,
-               kps, scale_log2, out, opart, ws.ml, qtiles, BH, pads);
-      else
-        launch(attn_bf16_kernel<1, f16_t>, grid, dim3(256), 0, st, qh, kh, vh, H, Hkv, Mq, Nk, cap,
-               kps, scale_log2, out, opart, ws.ml, qtiles, BH, pads);
+      if (QB == 2) go(attn_bf16_kernel<2, f16_t, 1>, 256, qh, kh, vh);
+      else if (groups) go(attn_bf16_kernel<1, f16_t, 2>, 512, qh, kh, vh);
+      else go(attn_bf16_kernel<1, f16_t, 1>, 256, qh, kh, vh);
     } else {
       const bf16_t *qh = (const bf16_t*)q, *kh = (const bf16_t*)kc, *vh = (const bf16_t*)vc;
-      if (QB == 2)
-        launch(attn_bf16_kernel<2, bf16_t>, grid, dim3(256), 0, st, qh, kh, vh, H, Hkv, Mq, Nk,
-               cap, kps, scale_log2, out, opart, ws.ml, qtiles, BH, pads);
-      else
-        launch(attn_bf16_kernel<1, bf16_t>, grid, dim3(256), 0, st, qh, kh, vh, H, Hkv, Mq, Nk,
-               cap, kps, scale_log2, out, opart, ws.ml, qtiles, BH, pads);
+      if (QB == 2) go(attn_bf16_kernel<2, bf16_t, 1>, 256, qh, kh, vh);
+      else if (groups) go(attn_bf16_kernel<1, bf16_t, 2>, 512, qh, kh, vh);
+      else go(attn_bf16_kernel<1, bf16_t, 1>, 256, qh, kh, vh);
     }
   } else {
     const dim3 grid(qtiles, BH, S);

@@ -4,6 +4,11 @@ Usage: python -m paper_2608_23167_amd.build   (or __graft_entry__.build()).
 Objects go to _build/ next to this file; the library is written in place
 (paper_2608_23167_amd/libssm.so) so that it travels with the source tree.
 
+`--debug` builds libssm_debug.so next to libssm.so (objects in _build_debug/)
+with SSM_DEBUG defined: the kernels then check on the device the invariants
+the host validation promises (positions, capacities, ids, k) and abort with
+the failed condition instead of skipping a write or producing a NaN row.
+
 `--hostsan DIR` builds DIR/libssm_hostsan.so: the same library with its host
 code instrumented by AddressSanitizer and UndefinedBehaviorSanitizer (device
 code as usual, uninstrumented), for the CPU tests of the C ABI's validation
@@ -45,10 +50,11 @@ def _compile(src: str, obj_dir: str, extra) -> str:
     return obj
 
 
-def build(verbose: bool = False, tuning: bool = False) -> str:
-    obj_dir = OBJ + "_tuning" if tuning else OBJ
-    out = os.path.join(HERE, "libssm_tuning.so") if tuning else OUT
-    extra = ["-DSSM_TUNING"] if tuning else []
+def build(verbose: bool = False, tuning: bool = False, debug: bool = False) -> str:
+    variant = "_tuning" if tuning else "_debug" if debug else ""
+    obj_dir = OBJ + variant
+    out = os.path.join(HERE, f"libssm{variant}.so")
+    extra = ["-DSSM_TUNING"] if tuning else ["-DSSM_DEBUG"] if debug else []
     os.makedirs(obj_dir, exist_ok=True)
     srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
     with cf.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
@@ -101,5 +107,5 @@ if __name__ == "__main__":
     if "--hostsan" in sys.argv[1:]:
         print("built", build_hostsan(sys.argv[sys.argv.index("--hostsan") + 1]))
         sys.exit(0)
-    build(verbose=True, tuning="--tuning" in sys.argv[1:])
+    build(verbose=True, tuning="--tuning" in sys.argv[1:], debug="--debug" in sys.argv[1:])
     sys.exit(0)

@@ -14,6 +14,7 @@
 // at small row counts; a merge kernel combines the per-split (max, sum,
 // output) triples in split order.
 #include "internal.h"
+#include "dcheck.h"
 
 namespace ssm {
 
@@ -134,6 +135,7 @@ __global__ void __launch_bounds__(256 * NG, NG == 1 ? 2 : 1) attn_bf16_kernel(
   const int steps = (ke_wg - kb_wg + KT * NG - 1) / (KT * NG);          // tiles per group, >= 1
   const int kb = kb_wg + grp * steps * KT, ke = min(ke_wg, kb + steps * KT);
   const int ntile = ke > kb ? (ke - kb + KT - 1) / KT : 0;              // this group's tiles
+  SSM_DCHECK(ke_wg <= cap);
 
   const E* Qh = Q + (size_t)bh * Mq * DH;
   vec qf[QB][4];

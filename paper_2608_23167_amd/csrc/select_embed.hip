@@ -1,6 +1,7 @@
 // Compacted row list of the sparse input (Section 3.2, Eq. 1-5) and the
 // soft suffix embedding of its rows (Section 3.2, Eq. 6-8).
 #include "internal.h"
+#include "dcheck.h"
 
 namespace ssm {
 
@@ -14,6 +15,7 @@ __global__ void __launch_bounds__(256) select_kernel(SelectLayout L, const int32
   if (r >= L.n_rows) return;
   int p, g;
   row_position(L, r, p, g);
+  SSM_DCHECK(r < cap && p >= 0 && p < seq_len);
   const int s = blockIdx.y;
   if (s == 0) {
     pos[r] = p;
@@ -50,9 +52,11 @@ __global__ void __launch_bounds__(256) embed_kernel(
   const bool pos_ok = p >= 0 && p < seq_len;
   const size_t sp = (size_t)s * seq_len + (pos_ok ? p : 0);
   const bool soft = pos_ok && region[r] >= 2 && prev_step >= 0 && pred_step[sp] == prev_step;
+  SSM_DCHECK(k >= 1 && k <= 8 && (pos_ok || pad));
   if (!soft) {
     const int tok = pad ? mask_id : tok_c[(size_t)s * tok_stride + r];
     const bool ok = (pos_ok || pad) && tok >= 0 && tok < vocab;
+    SSM_DCHECK(ok);
     const T* e = E + (size_t)(ok ? tok : 0) * d;
     for (int c = threadIdx.x; c < d; c += blockDim.x) out[c] = ok ? ldf(e + c) : __builtin_nanf("");
     return;
@@ -70,6 +74,7 @@ __global__ void __launch_bounds__(256) embed_kernel(
       ok = ok && ids[i] >= 0 && ids[i] < vocab;
     }
   }
+  SSM_DCHECK(ok);
   const T* em = E + (size_t)mask_id * d;
   for (int c = threadIdx.x; c < d; c += blockDim.x) {
     float acc = 0.f;  // Eq. 7: sum_i w_i e_{id_i}, in the stored order
@@ -114,9 +119,11 @@ __global__ void __launch_bounds__(256) embed8_kernel(
   const size_t sp = (size_t)s * seq_len + (pos_ok ? p : 0);
   const bool soft = pos_ok && region[r] >= 2 && prev_step >= 0 && pred_step[sp] == prev_step;
   const float qnan = __builtin_nanf("");
+  SSM_DCHECK(k >= 1 && k <= 8 && (pos_ok || pad));
   if (!soft) {
     const int tok = pad ? mask_id : tok_c[(size_t)s * tok_stride + r];
     const bool ok = (pos_ok || pad) && tok >= 0 && tok < vocab;
+    SSM_DCHECK(ok);
     const T* e = E + (size_t)(ok ? tok : 0) * d;
     for (int c = threadIdx.x; c < d8; c += blockDim.x) {
       float v[8];
@@ -143,6 +150,7 @@ __global__ void __launch_bounds__(256) embed8_kernel(
       ok = ok && ids[i] >= 0 && ids[i] < vocab;
     }
   }
+  SSM_DCHECK(ok);
   const T* em = E + (size_t)mask_id * d;
   for (int c = threadIdx.x; c < d8; c += blockDim.x) {
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};   // Eq. 7, in the stored order

@@ -3,6 +3,7 @@
 // rule) and the update of the per-position prediction state that the next
 // step's soft suffix embedding reads (Section 3.2, Eq. 6).
 #include "internal.h"
+#include "dcheck.h"
 
 namespace ssm {
 
@@ -20,6 +21,7 @@ __global__ void __launch_bounds__(256) unmask_kernel(
   __shared__ uint8_t sel[1024];
   __shared__ int n_cand, n_sel, best;
   const int s = blockIdx.x, tid = threadIdx.x;
+  SSM_DCHECK(b <= 1024 && k >= 1 && k <= 8 && n_out >= b);
   // a padded sequence's block and suffix positions sit pad[s] to the left
   const int shift = pads.of(s);
   int32_t* tok = tokens + (size_t)s * seq_len + (block_start - shift);
@@ -67,6 +69,7 @@ __global__ void __launch_bounds__(256) unmask_kernel(
   // prediction state of the retained suffix rows
   for (int r = b + tid; r < n_out; r += blockDim.x) {
     const int p = pos_out[r] - shift;
+    SSM_DCHECK(p >= 0 && p < seq_len);
     if (p < 0 || p >= seq_len) continue;
     const size_t sp = (size_t)s * seq_len + p;
     for (int i = 0; i < k; ++i) {

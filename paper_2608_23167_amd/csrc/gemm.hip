@@ -382,12 +382,13 @@ __device__ __forceinline__ void lds_written_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-// Warp-specialised workgroup of 8 waves, BM = 128 rows x BN columns.
+// Warp-specialised workgroup of 8 waves, BM rows (64, 128, 192 or 256) x BN
+// columns.
 //  * Waves 4-7 ("staging") stream the weight tile of each K-step (BN rows x 64
 //    k, the HBM-bound stream) through a ring of 4 register stages into a ring
 //    of 3 or 4 LDS buffers, 2 or 3 K-steps ahead.  A staging thread holds only BN / 32
 //    x 16 bytes per stage, so the ring is deep at little register cost.
-//  * Waves 0-3 ("compute") each own 32 rows x all BN columns.  They load
+//  * Waves 0-3 ("compute") each own BM / 4 rows x all BN columns.  They load
 //    their activation fragments (bfloat16 hi and optionally lo, L2-resident)
 //    straight from global memory into registers in the MFMA operand layout,
 //    two K-steps ahead, read the weight fragments from LDS one half-step
@@ -403,9 +404,10 @@ __global__ void __launch_bounds__(512) gemm_bf16_kernel(Pol pol, const bf16_t* _
                                                         int M, int k_per_split, int mt,
                                                         int n_split, float* __restrict__ part,
                                                         int ldp, int krot) {
-  static_assert(BM == 128, "4 compute waves of 32 rows");
+  static_assert(BM == 64 || BM == 128 || BM == 192 || BM == 256, "4 compute waves of BM / 4 rows");
   constexpr int BK = 64, LS = BK + 8;            // LDS row stride (elements), 144 B
-  constexpr int FM = 2, FN = BN / 16;            // per compute wave: 32 rows x BN columns
+  constexpr int FM = BM / 64, FN = BN / 16;      // per compute wave: 16 FM rows x BN columns
+  constexpr int RW = 16 * FM;
   constexpr int NA = SPLIT ? 2 : 1;
   constexpr int WR = BN / 32;                    // weight rows per staging thread per stage
   // LDS weight buffers: 4 (three K-steps ahead) for the 96-column tiles, 3
@@ -449,7 +451,7 @@ __global__ void __launch_bounds__(512) gemm_bf16_kernel(Pol pol, const bf16_t* _
 #pragma unroll
     for (int i = 0; i < FM; ++i)
       a_off[i] = (size_t)(kbeg >> 6) * a_kstep +
-                 (size_t)min((m0 + 32 * wave + 16 * i) >> 4, G - 1) * 1024 + lane * 8;
+                 (size_t)min((m0 + RW * wave + 16 * i) >> 4, G - 1) * 1024 + lane * 8;
     // weight fragment j, half kk: LDS row 16 j + lane % 16, column 32 kk + 8 (lane / 16)
     const int wfrag = (lane & 15) * LS + (lane >> 4) * 8;
     f32x4_t acc[FM][FN];
@@ -496,7 +498,7 @@ __global__ void __launch_bounds__(512) gemm_bf16_kernel(Pol pol, const bf16_t* _
     lds_handover_barrier();                                                           \
   } while (0)
 
-    if (m0 + 32 * wave >= M) {
+    if (m0 + RW * wave >= M) {
       // every row of this wave is padding (few rows, e.g. the LM head's
       // block rows): no loads or MFMAs, only the barrier schedule
       __syncthreads();
@@ -510,14 +512,14 @@ __global__ void __launch_bounds__(512) gemm_bf16_kernel(Pol pol, const bf16_t* _
         CSTEP(kt, a0);
         CSTEP(kt + 1, a1);
       }
-      // accumulators -> LDS tile: acc[i][j][r] = C[32 wave + 16i + 4*(lane/16) + r][16j + lane%16]
+      // accumulators -> LDS tile: acc[i][j][r] = C[RW wave + 16i + 4*(lane/16) + r][16j + lane%16]
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j)
 #pragma unroll
           for (int r = 0; r < 4; ++r)
-            Cs[(32 * wave + i * 16 + (lane >> 4) * 4 + r) * CS + j * 16 + (lane & 15)] = acc[i][j][r];
+            Cs[(RW * wave + i * 16 + (lane >> 4) * 4 + r) * CS + j * 16 + (lane & 15)] = acc[i][j][r];
     }
 #undef LOAD_A
 #undef READ_W
@@ -852,7 +854,8 @@ size_t gemm_split_ws_floats(int M, int max_n) {
 // register ring of weight loads.
 struct GemmCfg {
   int bn, s, pw;
-  int big = 0;    // gemm_big_kernel tile: 1 = 256 x 128, 2 = 128 x 256 (8 waves, 2-stage ring),
+  int big = 0;
+  int bm = 128;   // row tile of gemm_bf16_kernel (see launch_bf16_bm)    // gemm_big_kernel tile: 1 = 256 x 128, 2 = 128 x 256 (8 waves, 2-stage ring),
                   // 3 = 256 x 256 (16 waves, 3-stage ring), 4 = 128 x 256 (8 waves, 3-stage
                   // ring), 5 = 256 x 256 (8 waves of 64 x 128, 3-stage ring), 6 = 256 x 128
                   // (8 waves, 3-stage ring); 0 = gemm_bf16_kernel; -1 = automatic
@@ -861,8 +864,8 @@ static int big_rows(int big) { return big == 1 || big == 3 || big == 5 || big ==
 static int big_cols(int big) { return big == 1 || big == 6 ? 128 : 256; }
 
 // Tuning override, compiled only into a tuning build (SSM_TUNING defined):
-// SSM_GEMM_CFG="kind:bn:s:pw[:big],..." with kind one of qkv, o, gate_up,
-// down, lm (big as in GemmCfg); read once per process.  The product build
+// SSM_GEMM_CFG="kind:bn:s:pw[:big[:bm]],..." with kind one of qkv, o, gate_up,
+// down, lm (big and bm as in GemmCfg); read once per process.  The product build
 // always takes the measured defaults.
 static GemmCfg cfg_override(const char* kind, GemmCfg c) {
 #ifdef SSM_TUNING
@@ -871,9 +874,9 @@ static GemmCfg cfg_override(const char* kind, GemmCfg c) {
   const size_t kl = strlen(kind);
   for (const char* p = env; p && *p;) {
     if (strncmp(p, kind, kl) == 0 && p[kl] == ':') {
-      int bn, s, pw, big = -1;
-      const int n = sscanf(p + kl + 1, "%d:%d:%d:%d", &bn, &s, &pw, &big);
-      if (n >= 3) return GemmCfg{bn, s, pw, n == 4 ? big : c.big};
+      int bn, s, pw, big = -1, bm = 128;
+      const int n = sscanf(p + kl + 1, "%d:%d:%d:%d:%d", &bn, &s, &pw, &big, &bm);
+      if (n >= 3) return GemmCfg{bn, s, pw, n >= 4 ? big : c.big, n == 5 ? bm : c.bm};
     }
     p = strchr(p, ',');
     if (p) ++p;
@@ -911,10 +914,9 @@ static int big_split(int tiles, int big, int M, int K, int N, size_t ws_floats) 
   return best;
 }
 
-template <int BN, int PW, bool SPLIT, class Pol>
+template <int BM, int BN, int PW, bool SPLIT, class Pol>
 static hipError_t launch_bf16(const Pol& pol, const ActIn& a, int M, int K, int N, int S,
                               SplitWs ws, hipStream_t st, bool reduce) {
-  constexpr int BM = 128;
   const int ntiles = N / BN, mt = ceil_div(M, BM);
   const dim3 grid(ntiles * mt * S);
   launch((gemm_bf16_kernel<BM, BN, PW, SPLIT, Pol>), grid, dim3(512), 0, st, pol,
@@ -926,17 +928,31 @@ static hipError_t launch_bf16(const Pol& pol, const ActIn& a, int M, int K, int 
   return hipGetLastError();
 }
 
-template <int BN, class Pol>
+template <int BM, int BN, class Pol>
 static hipError_t launch_bf16_pw(const Pol& pol, const ActIn& a, int M, int K, int N, int S,
-                                 int pw, SplitWs ws, hipStream_t st, bool reduce = true) {
+                                 int pw, SplitWs ws, hipStream_t st, bool reduce) {
   const bool split = a.lo != nullptr;
   // the staging loop is unrolled by the ring depth: nk = K / S / 64 must be a
   // multiple of it (of 4 always, host-checked)
   if (pw >= 8 && (K / S / 64) % 8 == 0)
-    return split ? launch_bf16<BN, 8, true>(pol, a, M, K, N, S, ws, st, reduce)
-                 : launch_bf16<BN, 8, false>(pol, a, M, K, N, S, ws, st, reduce);
-  return split ? launch_bf16<BN, 4, true>(pol, a, M, K, N, S, ws, st, reduce)
-               : launch_bf16<BN, 4, false>(pol, a, M, K, N, S, ws, st, reduce);
+    return split ? launch_bf16<BM, BN, 8, true>(pol, a, M, K, N, S, ws, st, reduce)
+                 : launch_bf16<BM, BN, 8, false>(pol, a, M, K, N, S, ws, st, reduce);
+  return split ? launch_bf16<BM, BN, 4, true>(pol, a, M, K, N, S, ws, st, reduce)
+               : launch_bf16<BM, BN, 4, false>(pol, a, M, K, N, S, ws, st, reduce);
+}
+
+// Row tile of gemm_bf16_kernel: 128 (default), 64 (two row tiles share each
+// weight tile through L2 on small row counts), 192 or 256 (one-pass layers,
+// tiles up to 96 columns: the register budget of a compute wave).
+template <int BN, class Pol>
+static hipError_t launch_bf16_bm(const Pol& pol, const ActIn& a, int M, int K, int N, int S,
+                                 int pw, int bm, SplitWs ws, hipStream_t st, bool reduce) {
+  if (bm == 64) return launch_bf16_pw<64, BN>(pol, a, M, K, N, S, pw, ws, st, reduce);
+  if constexpr (BN <= 96) {
+    if (bm == 192 && a.lo == nullptr) return launch_bf16_pw<192, BN>(pol, a, M, K, N, S, pw, ws, st, reduce);
+    if (bm == 256 && a.lo == nullptr) return launch_bf16_pw<256, BN>(pol, a, M, K, N, S, pw, ws, st, reduce);
+  }
+  return launch_bf16_pw<128, BN>(pol, a, M, K, N, S, pw, ws, st, reduce);
 }
 
 // Launch plan of one projection: the configuration with a valid tile width
@@ -953,7 +969,9 @@ static GemmCfg plan_bf16(const char* kind, const Pol& pol, int M, int K, int N, 
     c.big = 0;
   if (c.big) c.bn = big_bn;
   else if (c.bn > 128 || !bn_ok(pol, c.bn) || N % c.bn) c.bn = bn_ok(pol, 128) && N % 128 == 0 ? 128 : 64;
-  const int tiles = (N / c.bn) * ceil_div(M, c.big ? big_rows(c.big) : 128);
+  if (c.big || (c.bm != 64 && c.bm != 192 && c.bm != 256) || ((c.bm == 192 || c.bm == 256) && c.bn > 96))
+    c.bm = 128;
+  const int tiles = (N / c.bn) * ceil_div(M, c.big ? big_rows(c.big) : c.bm);
   int S = c.s > 0 ? c.s : c.big ? big_split(tiles, c.big, M, K, N, ws.floats)
                                  : auto_split(tiles, M, K, ws.floats, N);
   while (S > 1 && (K % (256 * S) != 0 || (size_t)S * M * N > ws.floats)) S /= 2;
@@ -990,9 +1008,9 @@ static hipError_t launch_plan(const Pol& pol, const ActIn& a, int M, int K, int 
   if (c.big == 4) return launch_big<128, 256, 2, 4, 3>(pol, a, M, K, N, c.s, ws, st, reduce);
   if (c.big == 5) return launch_big<256, 256, 4, 2, 3>(pol, a, M, K, N, c.s, ws, st, reduce);
   if (c.big == 6) return launch_big<256, 128, 4, 2, 3>(pol, a, M, K, N, c.s, ws, st, reduce);
-  if (c.bn == 96) return launch_bf16_pw<96>(pol, a, M, K, N, c.s, c.pw, ws, st, reduce);
-  if (c.bn == 64) return launch_bf16_pw<64>(pol, a, M, K, N, c.s, c.pw, ws, st, reduce);
-  return launch_bf16_pw<128>(pol, a, M, K, N, c.s, c.pw, ws, st, reduce);
+  if (c.bn == 96) return launch_bf16_bm<96>(pol, a, M, K, N, c.s, c.pw, c.bm, ws, st, reduce);
+  if (c.bn == 64) return launch_bf16_bm<64>(pol, a, M, K, N, c.s, c.pw, c.bm, ws, st, reduce);
+  return launch_bf16_bm<128>(pol, a, M, K, N, c.s, c.pw, c.bm, ws, st, reduce);
 }
 
 template <class Pol>
@@ -1085,6 +1103,10 @@ static hipError_t run_f32(const Pol& pol, const ActIn& a, int M, int K, int N, S
 // MFMA-bound and want wide tiles.  `paired`: the activations carry the lo part
 // (twice the MFMA work per operand byte, so the wide 3-stage tiles pay more).
 // Measured choices:
+//  * row tiles of gemm_bf16_kernel: 128 rows, except 256 for the one-pass QKV
+//    from 257 to 511 rows (two row tiles instead of three or four) and the
+//    one-pass gate/up from 129 to 256 rows (one row tile instead of two); 64-
+//    and 192-row tiles and the 256-row tiles elsewhere measured slower;
 //  * QKV: 96-column tiles below 512 rows (128 column tiles at d = 4096 with
 //    32 + 2 x 32 heads: with the automatic split-K, 2 ways up to 128 rows,
 //    256 workgroups where 128-column tiles left 64 CUs idle); 256 x 128 tiles
@@ -1105,11 +1127,19 @@ static hipError_t run_f32(const Pol& pol, const ActIn& a, int M, int K, int N, S
 static GemmCfg default_cfg(const char* kind, int M, bool paired) {
   const bool small = M <= 256;
   if (!strcmp(kind, "qkv")) {
-    if (M < 512) return GemmCfg{96, 0, 4, 0};
+    if (M < 512) {
+      GemmCfg c{96, 0, 4, 0};
+      if (!paired && M > 256) c.bm = 256;   // two 256-row tiles: 7-17% faster at 376-504 rows
+      return c;
+    }
     return GemmCfg{128, 1, 3, paired ? 1 : (M >= 1024 ? 6 : 0)};
   }
   if (!strcmp(kind, "gate_up")) {
-    if (M < 512) return GemmCfg{96, 1, 4, 0};
+    if (M < 512) {
+      GemmCfg c{96, 1, 4, 0};
+      if (!paired && M > 128 && M <= 256) c.bm = 256;   // one row tile: 9% faster at 240 rows
+      return c;
+    }
     return GemmCfg{128, 1, 3, M >= 1024 ? 3 : (paired ? 2 : 6)};
   }
   if (!strcmp(kind, "lm")) return GemmCfg{128, 1, 4, 0};
@@ -1285,7 +1315,7 @@ hipError_t lm_head_stats(const ActIn& a, int M, int K, const void* w, int N, int
   PolLMStats<bf16_t> p{(const bf16_t*)w, K, N, mask_id, (LMPartial*)stats_ws, 2 * ntiles, logits, N};
   const GemmCfg c = cfg_override("lm", default_cfg("lm", M, a.lo != nullptr));
   SplitWs none{nullptr, 0};
-  hipError_t e = launch_bf16_pw<BN>(p, a, M, K, N, 1, c.pw, none, st);
+  hipError_t e = launch_bf16_pw<128, BN>(p, a, M, K, N, 1, c.pw, none, st, true);
   if (e != hipSuccess) return e;
   launch(lm_merge_kernel, dim3(M), dim3(256), 0, st, (const LMPartial*)stats_ws,
                      2 * ntiles, k, argmax, conf, topk_ids, topk_w);

@@ -390,6 +390,193 @@ __global__ void __launch_bounds__(256 * NG, NG == 1 ? 2 : 1) attn_bf16_kernel(
   }
 }
 
+// Decode launches (few query rows, a short key range, no split): one
+// workgroup of 8 waves per (sequence, head, block of 16 query rows), so the
+// grid holds one workgroup per CU where the 64-row workgroups above would
+// leave three CUs in four idle.  All 8 waves take the same 16 query rows;
+// wave w takes key tiles w, w + 8, ... of the range.  The K fragments of a
+// tile are loaded straight into registers (the A layout of S^T = K Q^T: 16
+// bytes of one key row per lane); its V tile goes into the wave's own LDS
+// buffer (global_load_lds) and is read back transposed, as above.  No wave
+// waits for another until the end, where the (output, maximum, row sum)
+// triples meet in LDS and wave w merges them, in wave order, for head
+// dimensions 16 w .. 16 w + 15.
+template <typename E>
+__global__ void __launch_bounds__(512, 1) attn_dec_kernel(
+    const E* __restrict__ Q, const E* __restrict__ Kc, const E* __restrict__ Vc,
+    int H, int Hkv, int Mq, int Nk, int cap, float scale_log2, ActOut O, int qblocks, int BH,
+    Pads pads) {
+  typedef AttnOps<E> Ops;
+  typedef typename Ops::vec vec;
+  constexpr int DH = 128, KT = 64, TBUF = KT * DH, NW = 8;
+  __shared__ __attribute__((aligned(1024))) E Vs_all[NW * TBUF];   // 16 KB per wave
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int g = lane >> 4, c16 = lane & 15;
+  int qb, bh, split;
+  attn_tile_of(blockIdx.x, gridDim.x, qblocks, BH, qb, bh, split);
+  const int s = bh / H, h = bh % H, kvh = h / (H / Hkv);
+  const int kb = pads.of(s), ke = Nk;
+  const int ntile = ke > kb ? (ke - kb + KT - 1) / KT : 0;
+  SSM_DCHECK(ke <= cap);
+  const int q = qb * 16 + c16;
+
+  const E* Qh = Q + (size_t)bh * Mq * DH;
+  vec qf[4];
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) {
+    if (q < Mq) qf[kk] = *(const vec*)(Qh + (size_t)q * DH + 32 * kk + 8 * g);
+    else qf[kk] = __builtin_bit_cast(vec, u32x4_t{0u, 0u, 0u, 0u});
+  }
+  const E* Kh = Kc + (size_t)(s * Hkv + kvh) * cap * DH;
+  const E* Vh = Vc + (size_t)(s * Hkv + kvh) * cap * DH;
+  E* const Vs = Vs_all + wave * TBUF;
+
+  f32x4_t o[8], ol = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int i = 0; i < 8; ++i) o[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY;
+  const vec ones = __builtin_bit_cast(vec, u32x4_t{Ops::ONE2, Ops::ONE2, Ops::ONE2, Ops::ONE2});
+  constexpr float RESCALE = 8.0f;   // lazy maximum, as in attn_bf16_kernel
+  const int tr_r = c16 >> 2, tr_q = c16 & 3;
+
+  for (int t = wave; t < ntile; t += NW) {
+    const int k0 = kb + t * KT;
+    // the previous tile's transposing reads of this buffer have completed
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    // V tile: 16 copies of 4 rows x 256 bytes; row r = 4 i + lane / 16, whose
+    // 32-byte block j goes to block position j ^ (r % 8).  Keys past the
+    // range repeat the last key; their scores are masked below.
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int r = 4 * i + g, key = min(k0 + r, ke - 1);
+      const int vc = (((c16 >> 1) ^ (r & 7)) << 1) | (c16 & 1);
+      __builtin_amdgcn_global_load_lds((const void*)(Vh + (size_t)key * DH + vc * 8),
+                                       (__attribute__((address_space(3))) void*)((char*)Vs + i * 1024),
+                                       16, 0, 0);
+    }
+    // K fragments: key 16 nb + c16, dimensions 32 kk + 8 g .. + 7
+    vec kf[4][4];
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb) {
+      const int key = min(k0 + 16 * nb + c16, ke - 1);
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) kf[nb][kk] = *(const vec*)(Kh + (size_t)key * DH + 32 * kk + 8 * g);
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+
+    // scores S^T: sc[nb][r] = score(key k0 + 16 nb + 4 g + r, query q)
+    f32x4_t sc[4];
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb) {
+      sc[nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) sc[nb] = Ops::mfma(kf[nb][kk], qf[kk], sc[nb]);
+    }
+    if (k0 + KT > ke) {
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (k0 + 16 * nb + 4 * g + r >= ke) sc[nb][r] = -INFINITY;
+    }
+    float mt = sc[0][0];
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) mt = fmaxf(mt, sc[nb][r]);
+    const float m_tile = max_lanes_16_32(mt) * scale_log2;
+    if (__builtin_amdgcn_ballot_w64(m_tile > m_run + RESCALE) != 0) {
+      const float m_new = fmaxf(m_run, m_tile);
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      ol *= alpha;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) o[i] *= alpha;
+      m_run = m_new;
+    }
+    // P^T operand: slot e of lane group g holds key 32 h2 + 16 (e / 4) + 4 g + e % 4
+    vec pb[2];
+#pragma unroll
+    for (int h2 = 0; h2 < 2; ++h2) {
+      float p[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        p[e] = __builtin_amdgcn_exp2f(fmaf(sc[2 * h2 + (e >> 2)][e & 3], scale_log2, -m_run));
+      pb[h2] = __builtin_bit_cast(vec, u32x4_t{Ops::pack(p[0], p[1]), Ops::pack(p[2], p[3]),
+                                               Ops::pack(p[4], p[5]), Ops::pack(p[6], p[7])});
+    }
+    // O^T += V^T P^T, the V^T operand read transposed from this wave's buffer
+    const char* vd = (const char*)Vs;
+#pragma unroll
+    for (int h2 = 0; h2 < 2; ++h2) {
+      ol = Ops::mfma(ones, pb[h2], ol);
+#pragma unroll
+      for (int db = 0; db < 8; ++db) {
+        const int r0 = 32 * h2 + 4 * g + tr_r, r1 = r0 + 16;
+        const v4i16_t t0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) v4i16_t*)(vd + v_byte(r0, db) + tr_q * 8));
+        const v4i16_t t1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) v4i16_t*)(vd + v_byte(r1, db) + tr_q * 8));
+        const vec a = __builtin_bit_cast(
+            vec, u32x4_t{__builtin_bit_cast(uint2, t0).x, __builtin_bit_cast(uint2, t0).y,
+                         __builtin_bit_cast(uint2, t1).x, __builtin_bit_cast(uint2, t1).y});
+        o[db] = Ops::mfma(a, pb[h2], o[db]);
+      }
+    }
+  }
+
+  // merge: every wave leaves its triple in LDS (over the V buffers, which all
+  // waves have finished reading), outputs as [wave][db][lane] f32x4 and
+  // (maximum, sum) as [wave][lane]; wave w then combines dimension block w
+  // of the 8 waves in wave order.  A wave without keys has m = -inf and
+  // l = 0 and weight 0.
+  __syncthreads();
+  f32x4_t* xo = (f32x4_t*)Vs_all;
+  float2* xm = (float2*)(xo + NW * 8 * 64);
+#pragma unroll
+  for (int db = 0; db < 8; ++db) xo[(wave * 8 + db) * 64 + lane] = o[db];
+  xm[wave * 64 + lane] = make_float2(m_run, ol[0]);   // every row of the ones block holds the sum
+  __syncthreads();
+  float2 ml[NW];
+  f32x4_t ov[NW];
+#pragma unroll
+  for (int v = 0; v < NW; ++v) {
+    ml[v] = xm[v * 64 + lane];
+    ov[v] = xo[(v * 8 + wave) * 64 + lane];
+  }
+  float M = -INFINITY;
+#pragma unroll
+  for (int v = 0; v < NW; ++v) M = fmaxf(M, ml[v].y > 0.f ? ml[v].x : -INFINITY);
+  f32x4_t acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  float L = 0.f;
+#pragma unroll
+  for (int v = 0; v < NW; ++v) {
+    const float w = ml[v].y > 0.f ? __builtin_amdgcn_exp2f(ml[v].x - M) : 0.f;
+    acc += ov[v] * w;
+    L += ml[v].y * w;
+  }
+  if (q >= Mq) return;
+  // acc[r] = O[query q][head dimension 16 wave + 4 g + r] before the division
+  const float inv = 1.0f / L;
+  const int row = s * Mq + q, col = h * DH + 16 * wave + 4 * g;
+  float v[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) v[e] = acc[e] * inv;
+  if (O.f32) {
+    *(float4*)((float*)O.hi + (size_t)row * O.ld + col) = make_float4(v[0], v[1], v[2], v[3]);
+    return;
+  }
+  const size_t idx = frag_index(row, col, O.G);   // 4 columns, one chunk
+  const uint2 hw = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+  *(uint2*)((bf16_t*)O.hi + idx) = hw;
+  if (O.lo) {
+    float r[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) r[e] = v[e] - bf2f((bf16_t)((e >> 1 ? hw.y : hw.x) >> (16 * (e & 1))));
+    *(uint2*)(O.lo + idx) = uint2{pack_bf16x2(r[0], r[1]), pack_bf16x2(r[2], r[3])};
+  }
+}
+
 // float32 path: one thread per query row, keys read through the cache.
 template <int DH>
 __global__ void __launch_bounds__(64) attn_f32_kernel(
@@ -472,6 +659,23 @@ static int attention_qb(int dtype, int BH, int Mq) {
   return mfma && Mq > 64 && ceil_div(Mq, 64) * BH >= 512 ? 2 : 1;
 }
 
+// Decode launches go to attn_dec_kernel: one workgroup per 16 query rows of a
+// head fills at most one round of CUs, and the key range gives each of its 8
+// waves at most two tiles.  A tuning build (SSM_TUNING defined) lets
+// SSM_ATTN_DEC override the workgroup bound (0: never); the product build
+// reads no environment variable.
+static bool attention_dec(int BH, int Mq, int Nk) {
+  int max_wg = 256;
+#ifdef SSM_TUNING
+  static const int env = [] {
+    const char* e = getenv("SSM_ATTN_DEC");
+    return e ? atoi(e) : -1;
+  }();
+  if (env >= 0) max_wg = env;
+#endif
+  return ceil_div(Mq, 16) * BH <= max_wg && ceil_div(Nk, 64) <= 16;
+}
+
 int attention_splits(int dtype, int B, int H, int Mq, int Nk, int max_splits, int* keys_per_split) {
   const int BH = B * H;
   const int qtiles = ceil_div(Mq, 64 * attention_qb(dtype, BH, Mq));
@@ -509,7 +713,16 @@ hipError_t attention(int dtype, const void* q, const void* kc, const void* vc, i
   const int S = attention_splits(dtype, B, H, Mq, Nk, ws.max_splits, &kps);
   const float scale_log2 = LOG2E / sqrtf((float)dh);
   float* opart = S > 1 ? ws.opart : nullptr;
-  if (mfma) {
+  if (mfma && S == 1 && attention_dec(BH, Mq, Nk)) {
+    const int qblocks = ceil_div(Mq, 16);
+    const dim3 grid(qblocks * BH);
+    if (dtype == ATTN_F16)
+      launch(attn_dec_kernel<f16_t>, grid, dim3(512), 0, st, (const f16_t*)q, (const f16_t*)kc,
+             (const f16_t*)vc, H, Hkv, Mq, Nk, cap, scale_log2, out, qblocks, BH, pads);
+    else
+      launch(attn_dec_kernel<bf16_t>, grid, dim3(512), 0, st, (const bf16_t*)q, (const bf16_t*)kc,
+             (const bf16_t*)vc, H, Hkv, Mq, Nk, cap, scale_log2, out, qblocks, BH, pads);
+  } else if (mfma) {
     const dim3 grid(qtiles * BH * S);
     // small grids (at most one workgroup per CU) whose splits hold two tiles or
     // more: two key groups per workgroup

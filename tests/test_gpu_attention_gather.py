@@ -59,6 +59,9 @@ def _rel(a, b):
     (1, 2, 2, 1, 1, 8),           # one query, one key
     (1, 4, 1, 64, 64, 64),        # exact tiles, 4 heads on one KV head
     (3, 2, 2, 129, 1000, 1030),   # several key tiles: split key ranges and merge
+    (1, 32, 32, 120, 472, 512),   # decode step (LLaDA-8B heads): 16 query rows per workgroup
+    (1, 28, 4, 119, 600, 640),    # decode, GQA (Dream-7B heads), two key tiles for some waves
+    (1, 32, 32, 376, 472, 512),   # block start: two key groups per workgroup
 ])
 def test_attention_matches_oracle(gpu, B, H, Hkv, n_q, n_keys, cap, dtype):
     q, k, v = _inputs(B, H, Hkv, n_q, cap, seed=B * 1000 + n_q, dtype=dtype)

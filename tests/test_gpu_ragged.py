@@ -193,11 +193,13 @@ def _ragged_cache(dec, states, prompt_lens, P_u, seed):
         st.cache = [caches[s]]
 
 
-@pytest.mark.parametrize("first", [True, False])
-def test_llada_shape_2_layers_bf16_ragged(gpu, first):
+@pytest.mark.parametrize("first,j", [(True, 3), (False, 3), (False, 7)])
+def test_llada_shape_2_layers_bf16_ragged(gpu, first, j):
     """LLaDA-8B shape (two layers, sharpened LM head), bfloat16, prompts of
-    256, 200 and 131 tokens at block 3: the block-start step (prefix rows with
-    padding, 472 rows in all) and a cached step (padding slots in the cache)."""
+    256, 200 and 131 tokens: at block 3 the block-start step (prefix rows with
+    padding, 472 rows in all) and a cached step (padding slots in the cache);
+    at the last block (no suffix left, 32 rows) a cached step, whose attention
+    takes the decode kernel (16 query rows per workgroup) over padded caches."""
     from synthetic import sharpened
     prompts = [256, 200, 131]
     wl = sharpened(WORKLOADS["llada_gen256"], 30.0).replace(batch=3)
@@ -206,7 +208,6 @@ def test_llada_shape_2_layers_bf16_ragged(gpu, first):
     w = OG.NumpyWeights(mw, dtype=np.float32)
     dec = _decoder(wl, mw, prompts)
     wls = [_own(wl, P0) for P0 in prompts]
-    j = 3
     states = []
     for s, wl_s in enumerate(wls):
         t, pi, pw, ps = mid_generation_state(wl_s, j, 7, 30 + s)

@@ -12,7 +12,9 @@
 // extra MFMA output block) runs in base 2 in float32; the scores of the next
 // tile are computed while it runs.  Split-KV over the key range fills the GPU
 // at small row counts; a merge kernel combines the per-split (max, sum,
-// output) triples in split order.
+// output) triples in split order.  Decode launches (few query rows, a short
+// key range) instead give each block of 16 query rows a workgroup of its own,
+// whose waves split the key tiles and merge in LDS (attn_dec_kernel).
 #include "internal.h"
 #include "dcheck.h"
 

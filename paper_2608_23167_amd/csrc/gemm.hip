@@ -1233,17 +1233,28 @@ __global__ void __launch_bounds__(256) lm_merge_kernel(const LMPartial* __restri
 #pragma unroll
   for (int q = 0; q < 8; ++q) { tv[q] = -INFINITY; ti[q] = 0x7fffffff; }
   float mx = -INFINITY, sm = 0.f;
-  for (int j = tid; j < n_part; j += 256) {
-    const LMPartial& p = P[j];
-    if (p.s > 0.f) {
-      if (p.m > mx) { sm = sm * expf(mx - p.m) + p.s; mx = p.m; }
-      else sm += p.s * expf(p.m - mx);
-    }
-    // a partial's values are sorted best first: stop at the first one that
-    // does not enter this thread's list
-    for (int q = 0; q < 8; ++q) {
-      if (!stat_better(p.v[q], p.id[q], tv[7], ti[7])) break;
-      stat_insert(tv, ti, p.v[q], p.id[q]);
+  // this thread's partials j = tid + 256 i, in that order; CH of them are
+  // loaded before any is folded in, so a row costs a few round trips
+  constexpr int CH = 4;
+  for (int j0 = tid; j0 < n_part; j0 += 256 * CH) {
+    LMPartial buf[CH];
+#pragma unroll
+    for (int c = 0; c < CH; ++c)
+      if (j0 + 256 * c < n_part) buf[c] = P[j0 + 256 * c];
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+      if (j0 + 256 * c >= n_part) break;
+      const LMPartial& p = buf[c];
+      if (p.s > 0.f) {
+        if (p.m > mx) { sm = sm * expf(mx - p.m) + p.s; mx = p.m; }
+        else sm += p.s * expf(p.m - mx);
+      }
+      // a partial's values are sorted best first: stop at the first one that
+      // does not enter this thread's list
+      for (int q = 0; q < 8; ++q) {
+        if (!stat_better(p.v[q], p.id[q], tv[7], ti[7])) break;
+        stat_insert(tv, ti, p.v[q], p.id[q]);
+      }
     }
   }
   // (max, sum) pairs over the workgroup: a butterfly within each wave (both

@@ -42,12 +42,12 @@ TRAFFIC = {
     # per-dispatch means of the block-start launches (grid 393216, 376 rows) and
     # the cached ones (grid 131072, 120 rows), for the one-pass layers and the
     # layers that keep the bfloat16 pair; copy kernel: 268435456 bytes read and
-    # written per launch read as 131086.3 KiB fetched and 262144.0 KiB written
+    # written per launch read as 131086.1 KiB fetched and 262144.0 KiB written
     ("llada_gen256", "gemm_gate_up"): {
-        "sources_sha256": "7a762661be79837cc63a41be7ccc4abaa1febdcf69afb28d2c17cfd16cb2a383",
-        "fetch_kib": {"start": (135930.3, 189386.6), "cached": (104448.7, 110535.2)},
+        "sources_sha256": "e9babf06dc649fb394273589dd248cba4496b0fc516fce905c7a3482e53c1c55",
+        "fetch_kib": {"start": (135810.6, 189390.7), "cached": (104448.8, 110535.8)},
         "write_kib": {"start": (9024.0, 18048.0), "cached": (2880.0, 5760.0)},
-        "fetch_scale": 262144.0 / 131086.3, "write_scale": 1.0},
+        "fetch_scale": 262144.0 / 131086.1, "write_scale": 1.0},
 }
 GEMM_SOURCES = ("gemm.hip", "internal.h", "common.h")
 

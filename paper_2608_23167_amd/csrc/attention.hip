@@ -85,6 +85,25 @@ __device__ __forceinline__ void attn_tile_of(int w, int total, int qtiles, int B
   split = v / (qtiles * BH);
 }
 
+// Four consecutive output columns col .. col + 3 of row `row` (col a multiple
+// of 4, so one 8-column chunk of the fragment order holds them): float32
+// row-major, or bfloat16 hi (and lo = the rounding remainder) in fragment order.
+__device__ __forceinline__ void store_out4(const ActOut& O, int row, int col, const float (&v)[4]) {
+  if (O.f32) {
+    *(float4*)((float*)O.hi + (size_t)row * O.ld + col) = make_float4(v[0], v[1], v[2], v[3]);
+    return;
+  }
+  const size_t idx = frag_index(row, col, O.G);
+  const uint2 hw = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+  *(uint2*)((bf16_t*)O.hi + idx) = hw;
+  if (O.lo) {
+    float r[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) r[e] = v[e] - bf2f((bf16_t)((e >> 1 ? hw.y : hw.x) >> (16 * (e & 1))));
+    *(uint2*)(O.lo + idx) = uint2{pack_bf16x2(r[0], r[1]), pack_bf16x2(r[2], r[3])};
+  }
+}
+
 // NG key groups per workgroup.  NG = 1: 4 waves walk the workgroup's key
 // range.  NG = 2 (small grids of decode steps, one workgroup per CU): two
 // groups of 4 waves take the query rows of the tile each, over the first and
@@ -361,26 +380,10 @@ __global__ void __launch_bounds__(256 * NG, NG == 1 ? 2 : 1) attn_bf16_kernel(
     // o[b][db][r] = O^T[dh 16db + 4g + r][query q]
     if (Opart == nullptr) {
       const float inv = 1.0f / l;
-      const int row = s * Mq + q;
-      if (O.f32) {
-        float* orow = (float*)O.hi + (size_t)row * O.ld + h * DH + 4 * g;
-#pragma unroll
-        for (int db = 0; db < 8; ++db)
-          *(float4*)(orow + 16 * db) = make_float4(o[b][db][0] * inv, o[b][db][1] * inv,
-                                                   o[b][db][2] * inv, o[b][db][3] * inv);
-        continue;
-      }
 #pragma unroll
       for (int db = 0; db < 8; ++db) {
-        const size_t idx = frag_index(row, h * DH + 16 * db + 4 * g, O.G);   // 4 columns, one chunk
-        float v[4], r[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = o[b][db][e] * inv;
-        const uint2 hw = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) r[e] = v[e] - bf2f((bf16_t)((e >> 1 ? hw.y : hw.x) >> (16 * (e & 1))));
-        *(uint2*)((bf16_t*)O.hi + idx) = hw;
-        if (O.lo) *(uint2*)(O.lo + idx) = uint2{pack_bf16x2(r[0], r[1]), pack_bf16x2(r[2], r[3])};
+        const float v[4] = {o[b][db][0] * inv, o[b][db][1] * inv, o[b][db][2] * inv, o[b][db][3] * inv};
+        store_out4(O, s * Mq + q, h * DH + 16 * db + 4 * g, v);
       }
     } else {
       const size_t row = ((size_t)split * BH + bh) * Mq + q;
@@ -560,23 +563,8 @@ __global__ void __launch_bounds__(512, 1) attn_dec_kernel(
   if (q >= Mq) return;
   // acc[r] = O[query q][head dimension 16 wave + 4 g + r] before the division
   const float inv = 1.0f / L;
-  const int row = s * Mq + q, col = h * DH + 16 * wave + 4 * g;
-  float v[4];
-#pragma unroll
-  for (int e = 0; e < 4; ++e) v[e] = acc[e] * inv;
-  if (O.f32) {
-    *(float4*)((float*)O.hi + (size_t)row * O.ld + col) = make_float4(v[0], v[1], v[2], v[3]);
-    return;
-  }
-  const size_t idx = frag_index(row, col, O.G);   // 4 columns, one chunk
-  const uint2 hw = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
-  *(uint2*)((bf16_t*)O.hi + idx) = hw;
-  if (O.lo) {
-    float r[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) r[e] = v[e] - bf2f((bf16_t)((e >> 1 ? hw.y : hw.x) >> (16 * (e & 1))));
-    *(uint2*)(O.lo + idx) = uint2{pack_bf16x2(r[0], r[1]), pack_bf16x2(r[2], r[3])};
-  }
+  const float v[4] = {acc[0] * inv, acc[1] * inv, acc[2] * inv, acc[3] * inv};
+  store_out4(O, s * Mq + q, h * DH + 16 * wave + 4 * g, v);
 }
 
 // float32 path: one thread per query row, keys read through the cache.

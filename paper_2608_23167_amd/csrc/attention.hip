@@ -326,8 +326,9 @@ __global__ void __launch_bounds__(256 * NG, NG == 1 ? 2 : 1) attn_bf16_kernel(
         if (t + 2 < ntile) copy_k(t + 2, t & 1);
         if (t + 1 < ntile) copy_v(t + 1, (t + 1) & 1);
         softmax_max(t, cur);
-        // one branch-free block: the next tile's score MFMAs interleave with
-        // this tile's exponentials
+        // the next tile's score MFMAs between this tile's maximum and its
+        // exponentials: the MFMAs of one wave overlap the VALU work of the
+        // other wave on the SIMD
         if (t + 1 < ntile) qk((t + 1) & 1, nxt);
         vec pb[QB][2];
         softmax_exp(cur, pb);
